@@ -1,0 +1,50 @@
+"""Pins of oracle/generate.py (the SpS loop, Algorithm 2, and ArS, Algorithm 1).
+
+* With the draft equal to the target every draft is accepted (q == p), so
+  each loop emits K + 1 tokens.
+* Greedy SpS (temperature 0) emits exactly the greedy ArS sequence: the
+  scheme preserves the target distribution, and the greedy target
+  distribution is a point mass.
+* Outputs have exactly n_new tokens, all in range, and every loop emits
+  between 1 and K + 1 tokens.
+"""
+import numpy as np
+
+from oracle import generate
+from paper_2302_01318_amd import configs, synth
+from oracle_helpers import oracle_weights, spec_of
+
+TGT = configs.ModelShape("t", 64, 2, 2, 32, 128, 40, "gelu", "f32")
+DRF = configs.ModelShape("d", 32, 1, 1, 32, 64, 40, "gelu", "f32")
+
+
+def models():
+    tw = oracle_weights(TGT, synth.weights(TGT, seed=11, std=0.3))
+    dw = oracle_weights(DRF, synth.weights(DRF, seed=12, std=0.3))
+    return spec_of(TGT), tw, spec_of(DRF), dw
+
+
+def test_draft_equal_to_target_accepts_everything():
+    ts, tw, _, _ = models()
+    prompt = synth.tokens(1, 1, 6, TGT.vocab)[0]
+    toks, acc = generate.sps_generate_one(ts, tw, ts, tw, prompt, 15, 3, 1.0, seed=3)
+    assert len(toks) == 15
+    assert all(a == 3 for a in acc)
+
+
+def test_greedy_sps_equals_greedy_ars():
+    ts, tw, ds, dw = models()
+    prompt = synth.tokens(2, 1, 5, TGT.vocab)[0]
+    sps, acc = generate.sps_generate_one(ts, tw, ds, dw, prompt, 16, 3, 0.0, seed=4)
+    ars, _ = generate.ars_generate_one(ts, tw, prompt, 16, 0.0, seed=4)
+    assert sps == ars
+    assert any(a < 3 for a in acc)      # the draft really disagrees sometimes
+
+
+def test_counts_and_ranges():
+    ts, tw, ds, dw = models()
+    prompt = synth.tokens(3, 1, 4, TGT.vocab)[0]
+    toks, acc = generate.sps_generate_one(ts, tw, ds, dw, prompt, 20, 4, 1.0, seed=5)
+    assert len(toks) == 20 and all(0 <= t < TGT.vocab for t in toks)
+    assert all(0 <= a <= 4 for a in acc)
+    assert sum(a + 1 for a in acc) >= 20 > sum(a + 1 for a in acc[:-1])
