@@ -1,0 +1,239 @@
+"""Benchmark of the SpS verify step on one MI355X.
+
+One "step" is one SpS verify step of the 70B-shaped target (d_model 8192,
+80 layers, 64 heads x 128, GELU FFN 32768, vocab 32000, bf16, 129.9 GB of
+weights resident in HBM): the transformer forward over the K+1 = 5 draft
+positions of one sequence against a 2048-token KV cache, the softmax of the
+5 target distributions and the fused modified rejection sampling. Inputs are
+synthetic and already on the device when timing starts: random-init weights
+N(0, 0.02), random bf16 prior keys/values, random tokens and draft
+distributions. Lengths are not advanced by the verify step, so every timed
+step sees the same context.
+
+Printed: one JSON line with verify-step throughput (algorithmic HBM GB/s),
+ms per step, the roofline of the dominant kernel (the weight-streaming GEMM,
+timed with HIP events around every launch on its stream), SpS and ArS tokens/s
+of the 70B target with its 3072-wide draft (prompt 2048, 128 new tokens,
+K = 4, temperature 1), and the CPU oracle timed on a bounded sample.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--K 4] [--B 1] [--ctx 2048]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "verify-step ms + HBM GB/s (70B-shape, K=4, bs=1); SpS tokens/sec at 1 GPU"
+HBM_PEAK_GBS = 8000.0
+
+
+def round_up(x, m):
+    return (x + m - 1) // m * m
+
+
+def verify_bytes(shape, B, K, ctx):
+    """Algorithmic HBM bytes of one verify step: every weight once, the KV
+    cache of every sequence once (prior context plus the K+1 new positions),
+    the new keys/values written once, the logits written and read once."""
+    es = 2 if shape.dtype == "bf16" else 4
+    M = B * (K + 1)
+    HD = shape.n_heads * shape.head_dim
+    weights = shape.n_layers * shape.matrix_bytes_per_layer() + shape.vocab * shape.d_model * es
+    gains = (2 * shape.n_layers + 1) * shape.d_model * 4
+    embed_rows = M * shape.d_model * es
+    kv_read = shape.n_layers * B * 2 * HD * (ctx + K + 1) * es
+    kv_write = shape.n_layers * M * 2 * HD * es
+    logits = 2 * M * shape.vocab * 4
+    return weights + gains + embed_rows + kv_read + kv_write + logits
+
+
+def device_model(sps, synth, shape, seed):
+    m = sps.Model(shape)
+    for (name, layer), t in synth.device_weights(shape, seed):
+        m.pack(name, layer, t)
+    return m
+
+
+def cpu_baseline(shape, K, ctx):
+    """The oracle (fp64 numpy, as it stands) on a bounded sample: one
+    full-width block of the 70B shape plus embedding and unembedding, K+1
+    positions of one sequence against a random ctx-token cache."""
+    import numpy as np
+    from oracle import model as om
+    from oracle.model import ModelSpec
+    from paper_2302_01318_amd import synth
+    one = shape.with_(n_layers=1)
+    spec = ModelSpec(one.d_model, 1, one.n_heads, one.head_dim, one.d_ff, one.vocab, one.ffn, one.dtype,
+                     one.eps, one.rope_base)
+    f = lambda t: t.float().numpy()
+    w = {k: synth.weight(one, k[0], k[1], 0) for k in synth.tensor_shapes(one)}
+    W = {"embed": f(w[("embed", -1)]), "final_norm": f(w[("final_norm", -1)]), "unembed": f(w[("unembed", -1)]),
+         "layers": [{"attn_norm": f(w[("attn_norm", 0)]), "wq": f(w[("wq", 0)]), "wk": f(w[("wk", 0)]),
+                     "wv": f(w[("wv", 0)]), "wo": f(w[("wo", 0)]), "ffn_norm": f(w[("ffn_norm", 0)]),
+                     "w1": f(w[("w1", 0)]), "w2": f(w[("w2", 0)])}]}
+    del w
+    cache = om.new_cache(spec, 1, ctx + K + 1)
+    k, v = synth.kv_prior(one, 1, 0, 1, ctx)
+    cache["k"][0, 0, :, :ctx] = k[0].double().numpy()
+    cache["v"][0, 0, :, :ctx] = v[0].double().numpy()
+    toks = synth.tokens(2, 1, K + 1, one.vocab)
+    reps = 4
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        om.forward_cached(spec, W, cache, toks, np.array([ctx]))
+    dt = (time.perf_counter() - t0) / reps
+    nbytes = verify_bytes(one, 1, K, ctx)
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "seconds_per_sample": dt, "repeats": reps,
+            "sample": "oracle fp64 forward of one full-width 70B-shaped block + embedding + unembedding, "
+                      "K+1=%d positions, B=1, ctx %d (%.2f GB algorithmic)" % (K + 1, ctx, nbytes / 1e9)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--K", type=int, default=4)
+    ap.add_argument("--B", type=int, default=1)
+    ap.add_argument("--ctx", type=int, default=2048)
+    ap.add_argument("--n-new", type=int, default=128)
+    ap.add_argument("--shape", default="70b", choices=["70b", "7b"])
+    ap.add_argument("--no-e2e", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures the verify step on one GPU; this build has no multi-GPU path "
+              "(requested --gpus %d)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2302_01318_amd import configs, sps, synth
+
+    shape = configs.SEVENTY_B if args.shape == "70b" else configs.SEVEN_B
+    dshape = configs.DRAFT_70B
+    B, K, ctx = args.B, args.K, args.ctx
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+
+    t0 = time.time()
+    target = device_model(sps, synth, shape, args.seed)
+    torch.cuda.synchronize()
+    log("target packed: %.1f GB in %.1f s" % (target.packed.numel() / 1e9, time.time() - t0))
+
+    # ---- verify step: timed region -------------------------------------------------
+    T_cap = round_up(ctx + K + 1, 32)
+    kv = sps.KVCache(shape, B, T_cap)
+    kv.buf.view(torch.bfloat16).normal_()          # random prior keys / values
+    kv.lengths.fill_(ctx)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(args.seed + 1)
+    p, _, drafts = synth.accept_case_device(args.seed + 2, B, K, shape.vocab)
+    first = torch.randint(0, shape.vocab, (B, 1), generator=gen, device="cuda", dtype=torch.int32)
+    tokens = torch.cat([first, drafts], dim=1).contiguous()
+    ws = sps.workspace(shape, B, K + 1, T_cap)
+    out = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+    nacc = torch.empty(B, dtype=torch.int32, device="cuda")
+
+    def step(i):
+        sps.verify_step(target, kv, tokens, K, 1.0, ws, p_draft=p, rng=(args.seed, i), out_tokens=out,
+                        n_accepted=nacc)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.steps):
+        step(i)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    nbytes = verify_bytes(shape, B, K, ctx)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    log("verify step: %.3f ms, %.1f GB/s (%.1f%% of %.0f GB/s)" % (ms, gbs, 100 * gbs / HBM_PEAK_GBS, HBM_PEAK_GBS))
+
+    # ---- roofline of the weight-streaming GEMM (events around every launch) --------
+    sps.profile_gemm_begin()
+    for i in range(args.steps):
+        step(i)
+    g_ms, g_n, g_bytes = sps.profile_gemm_end()
+    assert sps.device_error() == 0
+    g_avg_ms = g_ms / g_n
+    g_gbs = (g_bytes / g_n) / (g_avg_ms * 1e-3) / 1e9
+    log("gemm: %d launches, avg %.1f us, %.1f GB/s" % (g_n, g_avg_ms * 1e3, g_gbs))
+    roofline = {"bound": "hbm", "kernel": "gemm_kernel (weight-streaming skinny GEMM, all linear layers)",
+                "achieved": round(g_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(g_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                "launches_per_step": g_n // args.steps, "avg_launch_us": round(g_avg_ms * 1e3, 2),
+                "bytes_per_launch": g_bytes / g_n}
+    del kv, ws
+
+    # ---- SpS and ArS tokens/s end to end ---------------------------------------------
+    e2e = {}
+    if not args.no_e2e:
+        t0 = time.time()
+        draft = device_model(sps, synth, dshape, args.seed + 10)
+        torch.cuda.synchronize()
+        log("draft packed: %.1f GB in %.1f s" % (draft.packed.numel() / 1e9, time.time() - t0))
+        prompt = torch.randint(0, shape.vocab, (B, ctx), generator=gen, device="cuda", dtype=torch.int32)
+        Tc = round_up(ctx + args.n_new + 2 * (K + 1), 32)
+        for name, dm, k in (("sps", draft, K), ("ars", None, 0)):
+            g = sps.Generator(target, dm, B, Tc, k)
+            g.prefill(prompt)
+            torch.cuda.synchronize()
+            acc_log = []
+            t0 = time.perf_counter()
+            g.run(args.n_new, 1.0, args.seed, accepted_log=acc_log)
+            torch.cuda.synchronize()
+            dt = time.perf_counter() - t0
+            accs = [int(a[0]) for a, done in acc_log if not bool(done[0])]
+            e2e[name] = {"tokens_per_s": B * args.n_new / dt, "loops": g.loops, "seconds": dt,
+                         "mean_accepted": sum(accs) / max(1, len(accs))}
+            log("%s: %.1f tokens/s, %d loops, mean accepted %.2f" % (name, e2e[name]["tokens_per_s"], g.loops,
+                                                                     e2e[name]["mean_accepted"]))
+            del g
+        del draft
+        assert sps.device_error() == 0
+
+    result = {
+        "metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic: random-init weights N(0,0.02), random bf16 prior KV, random tokens and draft "
+                "distributions",
+        "config": {"workload": "%s-shaped target verify step + softmax + fused accept/resample" % shape.name,
+                   "K": K, "batch": B, "ctx": ctx, "bytes_per_step": nbytes,
+                   "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)},
+        "verify_ms": round(ms, 4),
+        "roofline": roofline,
+    }
+    if e2e:
+        result["sps_tokens_per_s"] = round(e2e["sps"]["tokens_per_s"], 2)
+        result["ars_tokens_per_s"] = round(e2e["ars"]["tokens_per_s"], 2)
+        result["e2e"] = {"draft": dshape.name, "prompt": ctx, "n_new": args.n_new, "K": K, "temperature": 1.0,
+                         "sps_mean_accepted": round(e2e["sps"]["mean_accepted"], 3),
+                         "sps_loops": e2e["sps"]["loops"], "ars_loops": e2e["ars"]["loops"],
+                         "paper_context": "Chinchilla 70B on 16 TPU v4: ArS 14.1 ms/token, SpS 1.92-2.46x "
+                                          "(paper Table 1); not comparable hardware"}
+    if not args.no_cpu_baseline:
+        del target
+        torch.cuda.empty_cache()
+        log("cpu baseline (oracle) ...")
+        result["cpu_baseline"] = cpu_baseline(shape, K, ctx)
+        log("cpu baseline: %.3f GB/s in %.1f s" % (result["cpu_baseline"]["value"],
+                                                    result["cpu_baseline"]["seconds_per_sample"]))
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -227,6 +227,16 @@ sps_status sps_philox_uniforms(sps_philox rng, int32_t purpose, int32_t B, int32
 sps_status sps_softmax(const float* logits, int32_t rows, int32_t V, float temperature,
                        float* probs, void* stream);
 
+/* Measurement helpers. Between begin and end, every weight-streaming GEMM
+ * launch (the linear layers: QKV, attention output, FFN, unembedding) is
+ * bracketed by HIP events on its stream. end synchronises those events and
+ * returns the summed kernel time (ms), the number of launches and their
+ * algorithmic bytes (weights + input activations + outputs, once each).
+ * Host-global state: not thread safe. */
+sps_status sps_profile_gemm_begin(void);
+sps_status sps_profile_gemm_end(float* total_ms /*host*/, int32_t* launches /*host*/,
+                                double* bytes /*host*/);
+
 /* Synchronise `stream`, return the current device's sticky error bits in
  * *flags (host) and clear them if `clear` != 0. */
 sps_status sps_device_error(void* stream, int32_t clear, int32_t* flags /*host*/);

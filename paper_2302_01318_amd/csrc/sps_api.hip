@@ -1,0 +1,546 @@
+// C ABI of libsps: argument validation, buffer layouts and launch sequencing.
+// Every entry point validates on the host before touching HIP.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/sps.h"
+#include "launch.h"
+
+// Sticky device error bits (SPS_DEV_*), one copy per device.
+__device__ int sps_dev_err;
+
+namespace {
+
+using sps::GemmArgs;
+
+constexpr int kMaxTokensPerSeq = 64;
+constexpr int kMaxRows = 160;
+constexpr int kMaxSplits = 8;
+constexpr int kMaxK = 63;
+
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+bool valid_config(const sps_config* c) {
+  if (!c) return false;
+  if (c->d_model < 32 || c->d_model % 32) return false;
+  if (c->n_layers < 1 || c->n_heads < 1) return false;
+  if (c->head_dim != 64 && c->head_dim != 128) return false;
+  if ((c->n_heads * c->head_dim) % 32) return false;
+  if (c->d_ff < 32 || c->d_ff % 32) return false;
+  if (c->vocab < 2 || c->vocab >= (1 << 24)) return false;
+  if (c->ffn_kind != SPS_FFN_GELU && c->ffn_kind != SPS_FFN_SWIGLU) return false;
+  if (c->dtype != SPS_DTYPE_F32 && c->dtype != SPS_DTYPE_BF16) return false;
+  if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f)) return false;
+  return true;
+}
+
+// Byte offsets of every tensor in the packed weight buffer.
+struct Layout {
+  int es, d, L, H, DH, HD, F, V, NU, N1;
+  bool swiglu;
+  size_t embed, final_norm, unembed, layer0, layer_stride;
+  size_t l_attn_norm, l_ffn_norm, l_qkv, l_o, l_w1, l_w2;
+  size_t total;
+};
+
+Layout make_layout(const sps_config* c) {
+  Layout L{};
+  L.es = c->dtype == SPS_DTYPE_BF16 ? 2 : 4;
+  L.d = c->d_model; L.L = c->n_layers; L.H = c->n_heads; L.DH = c->head_dim;
+  L.HD = L.H * L.DH; L.F = c->d_ff; L.V = c->vocab;
+  L.NU = (L.V + 15) / 16 * 16;
+  L.swiglu = c->ffn_kind == SPS_FFN_SWIGLU;
+  L.N1 = L.swiglu ? 2 * L.F : L.F;
+  const size_t es = L.es;
+  size_t o = 0;
+  L.embed = o; o = align256(o + static_cast<size_t>(L.V) * L.d * es);
+  L.final_norm = o; o = align256(o + static_cast<size_t>(L.d) * 4);
+  L.unembed = o; o = align256(o + static_cast<size_t>(L.NU) * L.d * es);
+  L.layer0 = o;
+  size_t lo = 0;
+  L.l_attn_norm = lo; lo = align256(lo + static_cast<size_t>(L.d) * 4);
+  L.l_ffn_norm = lo; lo = align256(lo + static_cast<size_t>(L.d) * 4);
+  L.l_qkv = lo; lo = align256(lo + static_cast<size_t>(3) * L.HD * L.d * es);
+  L.l_o = lo; lo = align256(lo + static_cast<size_t>(L.d) * L.HD * es);
+  L.l_w1 = lo; lo = align256(lo + static_cast<size_t>(L.N1) * L.d * es);
+  L.l_w2 = lo; lo = align256(lo + static_cast<size_t>(L.d) * L.F * es);
+  L.layer_stride = lo;
+  L.total = L.layer0 + L.layer_stride * L.L;
+  return L;
+}
+
+// Offsets of the forward's scratch buffers.
+struct WsLayout {
+  size_t h, x, qkvp, qrot, apart, act, resp, logits, stats, total;
+};
+
+WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
+  WsLayout w{};
+  const size_t M = static_cast<size_t>(B) * Mps;
+  const size_t es = L.es;
+  const size_t NP = sps::attn_partials(T_cap);
+  size_t o = 0;
+  w.h = o; o = align256(o + M * L.d * 4);
+  w.x = o; o = align256(o + M * std::max(L.d, L.HD) * es);
+  w.qkvp = o; o = align256(o + kMaxSplits * M * 3 * L.HD * 4);
+  w.qrot = o; o = align256(o + M * L.HD * es);
+  w.apart = o; o = align256(o + static_cast<size_t>(B) * L.H * NP * Mps * (L.DH + 2) * 4);
+  w.act = o; o = align256(o + M * L.F * es);
+  w.resp = o; o = align256(o + kMaxSplits * M * L.d * 4);
+  w.logits = o; o = align256(o + M * L.V * 4);
+  w.stats = o; o = align256(o + M * 2 * 4);
+  w.total = o;
+  return w;
+}
+
+int* device_error_ptr() {
+  static int* ptrs[64] = {nullptr};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  if (!ptrs[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(sps_dev_err)) != hipSuccess) return nullptr;
+    ptrs[dev] = static_cast<int*>(p);
+  }
+  return ptrs[dev];
+}
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+}  // namespace
+
+struct sps_model_s {
+  sps_config cfg;
+  Layout L;
+  char* base;
+};
+
+struct sps_kv_s {
+  sps_config cfg;
+  Layout L;
+  int B, T_cap;
+  char* buf;
+  int32_t* lengths;
+  size_t plane_bytes;  // one of K or V for one layer: B * H * T_cap * DH elements
+};
+
+namespace {
+
+char* layer_ptr(const sps_model_s* m, int l, size_t off) {
+  return m->base + m->L.layer0 + m->L.layer_stride * l + off;
+}
+void* kv_k(const sps_kv_s* kv, int l) { return kv->buf + kv->plane_bytes * (2 * static_cast<size_t>(l)); }
+void* kv_v(const sps_kv_s* kv, int l) { return kv->buf + kv->plane_bytes * (2 * static_cast<size_t>(l) + 1); }
+
+#define SPS_HIP(expr)                                 \
+  do {                                                \
+    if ((expr) != hipSuccess) return SPS_E_HIP;       \
+  } while (0)
+
+// Optional timing of every GEMM launch with HIP events on the launch stream
+// (sps_profile_gemm_begin / _end): the benchmark's live measurement of the
+// weight-streaming kernel.
+struct GemmProfile {
+  bool on = false;
+  std::vector<hipEvent_t> ev;   // start, stop pairs
+  std::vector<double> bytes;    // algorithmic bytes per launch
+  size_t used = 0;
+};
+GemmProfile g_prof;
+
+sps_status gemm(int dtype, const void* X, int ldx, int M, const void* W, int N, int KT, int n_valid, int epi,
+                float* out, int ldo, void* act, int lda, int force_S, hipStream_t st) {
+  GemmArgs a{};
+  a.X = X; a.ldx = ldx; a.M = M; a.W = W; a.N = N; a.KT = KT; a.n_valid = n_valid;
+  a.S = force_S > 0 ? force_S : sps::gemm_splits(dtype, N / 16, KT, M, epi);
+  a.out = out; a.ldo = ldo; a.act = act; a.lda = lda; a.epi = epi;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (g_prof.on) {
+    if (g_prof.used + 2 > g_prof.ev.size()) {
+      for (int i = 0; i < 2; ++i) {
+        hipEvent_t e;
+        SPS_HIP(hipEventCreate(&e));
+        g_prof.ev.push_back(e);
+      }
+    }
+    e0 = g_prof.ev[g_prof.used];
+    e1 = g_prof.ev[g_prof.used + 1];
+    g_prof.used += 2;
+    const double es = dtype == 1 ? 2.0 : 4.0;
+    const double rows_w = epi == sps::kEpiSwiglu ? 2.0 * n_valid : static_cast<double>(n_valid);
+    const double out_b = epi == sps::kEpiStore ? 4.0 * M * n_valid : es * M * n_valid;
+    g_prof.bytes.push_back(rows_w * KT * 32 * es + es * M * KT * 32 + out_b);
+    SPS_HIP(hipEventRecord(e0, st));
+  }
+  SPS_HIP(sps::launch_gemm(dtype, a, st));
+  if (e1) SPS_HIP(hipEventRecord(e1, st));
+  return SPS_OK;
+}
+
+// The decoder forward (Conditional Scoring section) over Mps new tokens per
+// sequence at positions lengths[b] + pos_offset + j.
+sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t* tokens, int tok_stride, int B,
+                        int Mps, int pos_offset, float* logits, char* ws_base, const WsLayout& ws, int* err,
+                        hipStream_t st) {
+  const Layout& L = m->L;
+  const int dt = m->cfg.dtype;
+  const int M = B * Mps;
+  const float eps = m->cfg.rms_eps;
+  float* h = reinterpret_cast<float*>(ws_base + ws.h);
+  void* x = ws_base + ws.x;
+  float* qkvp = reinterpret_cast<float*>(ws_base + ws.qkvp);
+  void* qrot = ws_base + ws.qrot;
+  float* apart = reinterpret_cast<float*>(ws_base + ws.apart);
+  void* act = ws_base + ws.act;
+  float* resp = reinterpret_cast<float*>(ws_base + ws.resp);
+  const int KTd = L.d / 32, KThd = L.HD / 32, KTf = L.F / 32;
+
+  SPS_HIP(sps::launch_embed_norm(dt, tokens, tok_stride, Mps, M, m->base + L.embed, L.V, L.d,
+                                 reinterpret_cast<const float*>(layer_ptr(m, 0, L.l_attn_norm)), eps, h, x, err,
+                                 st));
+  for (int l = 0; l < L.L; ++l) {
+    const int S_qkv = sps::gemm_splits(dt, 3 * L.HD / 16, KTd, M, sps::kEpiStore);
+    sps_status s = gemm(dt, x, L.d, M, layer_ptr(m, l, L.l_qkv), 3 * L.HD, KTd, 3 * L.HD, sps::kEpiStore, qkvp,
+                        3 * L.HD, nullptr, 0, S_qkv, st);
+    if (s != SPS_OK) return s;
+    SPS_HIP(sps::launch_rope_kv(dt, qkvp, S_qkv, M, L.H, L.DH, Mps, kv->lengths, pos_offset, m->cfg.rope_base,
+                                qrot, kv_k(kv, l), kv_v(kv, l), kv->T_cap, err, st));
+    SPS_HIP(sps::launch_attention(dt, qrot, kv_k(kv, l), kv_v(kv, l), kv->lengths, pos_offset, B, Mps, L.H, L.DH,
+                                  kv->T_cap, apart, x, st));
+    const int S_o = sps::gemm_splits(dt, L.d / 16, KThd, M, sps::kEpiStore);
+    s = gemm(dt, x, L.HD, M, layer_ptr(m, l, L.l_o), L.d, KThd, L.d, sps::kEpiStore, resp, L.d, nullptr, 0, S_o,
+             st);
+    if (s != SPS_OK) return s;
+    SPS_HIP(sps::launch_add_norm(dt, h, resp, S_o, M, L.d,
+                                 reinterpret_cast<const float*>(layer_ptr(m, l, L.l_ffn_norm)), eps, x, st));
+    s = gemm(dt, x, L.d, M, layer_ptr(m, l, L.l_w1), L.N1, KTd, L.F, L.swiglu ? sps::kEpiSwiglu : sps::kEpiGelu,
+             nullptr, 0, act, L.F, 1, st);
+    if (s != SPS_OK) return s;
+    const int S_2 = sps::gemm_splits(dt, L.d / 16, KTf, M, sps::kEpiStore);
+    s = gemm(dt, act, L.F, M, layer_ptr(m, l, L.l_w2), L.d, KTf, L.d, sps::kEpiStore, resp, L.d, nullptr, 0, S_2,
+             st);
+    if (s != SPS_OK) return s;
+    const float* next_gain = l + 1 < L.L ? reinterpret_cast<const float*>(layer_ptr(m, l + 1, L.l_attn_norm))
+                                         : reinterpret_cast<const float*>(m->base + L.final_norm);
+    SPS_HIP(sps::launch_add_norm(dt, h, resp, S_2, M, L.d, next_gain, eps, x, st));
+  }
+  if (logits) {
+    sps_status s = gemm(dt, x, L.d, M, m->base + L.unembed, L.NU, KTd, L.V, sps::kEpiStore, logits, L.V, nullptr,
+                        0, 1, st);
+    if (s != SPS_OK) return s;
+  }
+  return SPS_OK;
+}
+
+sps_status check_forward_args(const sps_model_s* m, const sps_kv_s* kv, int B, int Mps, size_t ws_bytes,
+                              const void* ws, WsLayout* out) {
+  if (!m || !kv || !ws) return SPS_E_INVALID;
+  if (B < 1 || Mps < 1) return SPS_E_INVALID;
+  if (Mps > kMaxTokensPerSeq || B * Mps > kMaxRows) return SPS_E_SHAPE;
+  if (B != kv->B) return SPS_E_SHAPE;
+  const sps_config& a = m->cfg;
+  const sps_config& b = kv->cfg;
+  if (a.n_layers != b.n_layers || a.n_heads != b.n_heads || a.head_dim != b.head_dim || a.dtype != b.dtype)
+    return SPS_E_SHAPE;
+  *out = make_ws(m->L, B, Mps, kv->T_cap);
+  if (ws_bytes < out->total) return SPS_E_CAPACITY;
+  return SPS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sps_status_string(int32_t status) {
+  switch (status) {
+    case SPS_OK: return "ok";
+    case SPS_E_INVALID: return "invalid argument";
+    case SPS_E_SHAPE: return "unsupported shape";
+    case SPS_E_CAPACITY: return "buffer too small";
+    case SPS_E_UNSUPPORTED: return "unsupported request";
+    case SPS_E_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int32_t sps_abi_version(void) { return 1; }
+
+size_t sps_weight_bytes(const sps_config* cfg) { return valid_config(cfg) ? make_layout(cfg).total : 0; }
+
+sps_status sps_pack_weight(const sps_config* cfg, int32_t tensor, int32_t layer, const void* src, void* packed,
+                           void* stream) {
+  if (!valid_config(cfg)) return SPS_E_SHAPE;
+  if (!src || !packed) return SPS_E_INVALID;
+  const Layout L = make_layout(cfg);
+  const bool per_layer = tensor >= SPS_W_ATTN_NORM;
+  if (tensor < SPS_W_EMBED || tensor > SPS_W_2) return SPS_E_INVALID;
+  if (per_layer && (layer < 0 || layer >= L.L)) return SPS_E_INVALID;
+  if (tensor == SPS_W_3 && !L.swiglu) return SPS_E_INVALID;
+  char* base = static_cast<char*>(packed);
+  char* lp = base + L.layer0 + L.layer_stride * (per_layer ? layer : 0);
+  const hipStream_t st = as_stream(stream);
+  const int dt = cfg->dtype;
+  const size_t es = L.es;
+  switch (tensor) {
+    case SPS_W_EMBED:
+      SPS_HIP(hipMemcpyAsync(base + L.embed, src, static_cast<size_t>(L.V) * L.d * es, hipMemcpyDeviceToDevice, st));
+      return SPS_OK;
+    case SPS_W_FINAL_NORM:
+      SPS_HIP(hipMemcpyAsync(base + L.final_norm, src, static_cast<size_t>(L.d) * 4, hipMemcpyDeviceToDevice, st));
+      return SPS_OK;
+    case SPS_W_ATTN_NORM:
+      SPS_HIP(hipMemcpyAsync(lp + L.l_attn_norm, src, static_cast<size_t>(L.d) * 4, hipMemcpyDeviceToDevice, st));
+      return SPS_OK;
+    case SPS_W_FFN_NORM:
+      SPS_HIP(hipMemcpyAsync(lp + L.l_ffn_norm, src, static_cast<size_t>(L.d) * 4, hipMemcpyDeviceToDevice, st));
+      return SPS_OK;
+    case SPS_W_UNEMBED:
+      SPS_HIP(sps::launch_pack(dt, src, L.V, L.d, base + L.unembed, L.d / 32, 0, 0, L.V, L.NU, st));
+      return SPS_OK;
+    case SPS_W_Q:
+    case SPS_W_K:
+    case SPS_W_V:
+      SPS_HIP(sps::launch_pack(dt, src, L.HD, L.d, lp + L.l_qkv, L.d / 32, 0, (tensor - SPS_W_Q) * L.HD, 0, 0, st));
+      return SPS_OK;
+    case SPS_W_O:
+      SPS_HIP(sps::launch_pack(dt, src, L.d, L.HD, lp + L.l_o, L.HD / 32, 0, 0, 0, 0, st));
+      return SPS_OK;
+    case SPS_W_1:
+      SPS_HIP(sps::launch_pack(dt, src, L.F, L.d, lp + L.l_w1, L.d / 32, L.swiglu ? 1 : 0, 0, 0, 0, st));
+      return SPS_OK;
+    case SPS_W_3:
+      SPS_HIP(sps::launch_pack(dt, src, L.F, L.d, lp + L.l_w1, L.d / 32, 1, 1, 0, 0, st));
+      return SPS_OK;
+    case SPS_W_2:
+      SPS_HIP(sps::launch_pack(dt, src, L.d, L.F, lp + L.l_w2, L.F / 32, 0, 0, 0, 0, st));
+      return SPS_OK;
+    default:
+      return SPS_E_INVALID;
+  }
+}
+
+sps_status sps_model_create(const sps_config* cfg, void* packed, sps_model_t* out) {
+  if (!out) return SPS_E_INVALID;
+  *out = nullptr;
+  if (!valid_config(cfg)) return SPS_E_SHAPE;
+  if (!packed) return SPS_E_INVALID;
+  sps_model_s* m = new (std::nothrow) sps_model_s;
+  if (!m) return SPS_E_CAPACITY;
+  m->cfg = *cfg;
+  m->L = make_layout(cfg);
+  m->base = static_cast<char*>(packed);
+  *out = m;
+  return SPS_OK;
+}
+
+void sps_model_destroy(sps_model_t model) { delete model; }
+
+size_t sps_kv_bytes(const sps_config* cfg, int32_t B, int32_t T_cap) {
+  if (!valid_config(cfg) || B < 1 || T_cap < 32 || T_cap % 32) return 0;
+  const Layout L = make_layout(cfg);
+  return static_cast<size_t>(L.L) * 2 * B * L.H * static_cast<size_t>(T_cap) * L.DH * L.es;
+}
+
+sps_status sps_kv_create(const sps_config* cfg, int32_t B, int32_t T_cap, void* kv_buf, int32_t* lengths,
+                         sps_kv_t* out) {
+  if (!out) return SPS_E_INVALID;
+  *out = nullptr;
+  if (!valid_config(cfg)) return SPS_E_SHAPE;
+  if (!kv_buf || !lengths || B < 1) return SPS_E_INVALID;
+  if (T_cap < 32 || T_cap % 32) return SPS_E_SHAPE;
+  sps_kv_s* kv = new (std::nothrow) sps_kv_s;
+  if (!kv) return SPS_E_CAPACITY;
+  kv->cfg = *cfg;
+  kv->L = make_layout(cfg);
+  kv->B = B;
+  kv->T_cap = T_cap;
+  kv->buf = static_cast<char*>(kv_buf);
+  kv->lengths = lengths;
+  kv->plane_bytes = static_cast<size_t>(B) * kv->L.H * T_cap * kv->L.DH * kv->L.es;
+  *out = kv;
+  return SPS_OK;
+}
+
+void sps_kv_destroy(sps_kv_t kv) { delete kv; }
+
+static sps_status kv_copy(sps_kv_t kv, int32_t layer, int32_t b, int32_t pos0, int32_t n, void* k, void* v,
+                          int to_cache, void* stream) {
+  if (!kv || !k || !v) return SPS_E_INVALID;
+  if (layer < 0 || layer >= kv->L.L || b < 0 || b >= kv->B || pos0 < 0 || n < 0) return SPS_E_INVALID;
+  if (pos0 + n > kv->T_cap) return SPS_E_CAPACITY;
+  const size_t seq = static_cast<size_t>(b) * kv->L.H * kv->T_cap * kv->L.DH * kv->L.es;
+  char* kc = static_cast<char*>(kv_k(kv, layer)) + seq;
+  char* vc = static_cast<char*>(kv_v(kv, layer)) + seq;
+  SPS_HIP(sps::launch_kv_copy(kv->cfg.dtype, to_cache, kc, vc, kv->L.H, kv->L.DH, kv->T_cap, pos0, n, k, v,
+                              as_stream(stream)));
+  return SPS_OK;
+}
+
+sps_status sps_kv_write(sps_kv_t kv, int32_t layer, int32_t b, int32_t pos0, int32_t n, const void* k_src,
+                        const void* v_src, void* stream) {
+  return kv_copy(kv, layer, b, pos0, n, const_cast<void*>(k_src), const_cast<void*>(v_src), 1, stream);
+}
+
+sps_status sps_kv_read(sps_kv_t kv, int32_t layer, int32_t b, int32_t pos0, int32_t n, void* k_dst, void* v_dst,
+                       void* stream) {
+  return kv_copy(kv, layer, b, pos0, n, k_dst, v_dst, 0, stream);
+}
+
+size_t sps_workspace_bytes(const sps_config* cfg, int32_t B, int32_t max_tokens_per_seq, int32_t T_cap) {
+  if (!valid_config(cfg) || B < 1 || max_tokens_per_seq < 1 || T_cap < 32) return 0;
+  return make_ws(make_layout(cfg), B, max_tokens_per_seq, T_cap).total;
+}
+
+sps_status sps_forward(sps_model_t model, sps_kv_t kv, const int32_t* tokens, int32_t tok_stride, int32_t B,
+                       int32_t M, int32_t pos_offset, float* logits_out, void* workspace, size_t ws_bytes,
+                       void* stream) {
+  WsLayout ws;
+  sps_status s = check_forward_args(model, kv, B, M, ws_bytes, workspace, &ws);
+  if (s != SPS_OK) return s;
+  if (!tokens || tok_stride < M) return SPS_E_INVALID;
+  int* err = device_error_ptr();
+  if (!err) return SPS_E_HIP;
+  return forward_impl(model, kv, tokens, tok_stride, B, M, pos_offset, logits_out, static_cast<char*>(workspace),
+                      ws, err, as_stream(stream));
+}
+
+sps_status sps_verify_step(sps_model_t target, sps_kv_t kv, const int32_t* tokens, int32_t B, int32_t K,
+                           float temperature, float* logits_out, float* q_out, const sps_accept_io* acc,
+                           void* workspace, size_t ws_bytes, void* stream) {
+  if (K < 0 || K > kMaxK) return SPS_E_INVALID;
+  if (!(temperature >= 0.f) || temperature > 1e30f) return SPS_E_INVALID;
+  WsLayout ws;
+  sps_status s = check_forward_args(target, kv, B, K + 1, ws_bytes, workspace, &ws);
+  if (s != SPS_OK) return s;
+  if (!tokens) return SPS_E_INVALID;
+  if (acc && (!acc->out_tokens || !acc->n_accepted || (K > 0 && !acc->p_draft))) return SPS_E_INVALID;
+  int* err = device_error_ptr();
+  if (!err) return SPS_E_HIP;
+  char* base = static_cast<char*>(workspace);
+  float* logits = logits_out ? logits_out : reinterpret_cast<float*>(base + ws.logits);
+  float* stats = reinterpret_cast<float*>(base + ws.stats);
+  const hipStream_t st = as_stream(stream);
+  s = forward_impl(target, kv, tokens, K + 1, B, K + 1, 0, logits, base, ws, err, st);
+  if (s != SPS_OK) return s;
+  const int V = target->cfg.vocab;
+  SPS_HIP(sps::launch_row_softmax(logits, B * (K + 1), V, temperature, stats, q_out, st));
+  if (acc)
+    SPS_HIP(sps::launch_accept_logits(acc->p_draft, logits, stats, temperature, tokens, acc->uniforms, acc->rng.seed,
+                                      acc->rng.loop, B, K, V, acc->out_tokens, acc->n_accepted, err, st));
+  return SPS_OK;
+}
+
+sps_status sps_accept_resample(const float* p_draft, const float* q_target, const int32_t* draft_tokens,
+                               const float* uniforms, sps_philox rng, int32_t B, int32_t K, int32_t V,
+                               int32_t* out_tokens, int32_t* n_accepted, void* stream) {
+  if (B < 1 || K < 0 || K > kMaxK || V < 2 || V >= (1 << 24)) return SPS_E_INVALID;
+  if (!q_target || !out_tokens || !n_accepted) return SPS_E_INVALID;
+  if (K > 0 && (!p_draft || !draft_tokens)) return SPS_E_INVALID;
+  int* err = device_error_ptr();
+  if (!err) return SPS_E_HIP;
+  SPS_HIP(sps::launch_accept_probs(p_draft, q_target, draft_tokens, uniforms, rng.seed, rng.loop, B, K, V,
+                                   out_tokens, n_accepted, err, as_stream(stream)));
+  return SPS_OK;
+}
+
+sps_status sps_draft_step(sps_model_t draft, sps_kv_t kv, const int32_t* ctx, int32_t B, int32_t K,
+                          float temperature, sps_philox rng, int32_t* tokens, float* p_out, void* workspace,
+                          size_t ws_bytes, void* stream) {
+  if (K < 0 || K > kMaxK) return SPS_E_INVALID;
+  if (!(temperature >= 0.f) || temperature > 1e30f) return SPS_E_INVALID;
+  if (!ctx || !tokens || (K > 0 && !p_out)) return SPS_E_INVALID;
+  WsLayout ws;
+  sps_status s = check_forward_args(draft, kv, B, 2, ws_bytes, workspace, &ws);
+  if (s != SPS_OK) return s;
+  int* err = device_error_ptr();
+  if (!err) return SPS_E_HIP;
+  const hipStream_t st = as_stream(stream);
+  if (K == 0) {
+    SPS_HIP(sps::launch_ctx_tokens(ctx, B, K, tokens, st));
+    return SPS_OK;
+  }
+  char* base = static_cast<char*>(workspace);
+  float* logits = reinterpret_cast<float*>(base + ws.logits);
+  const int V = draft->cfg.vocab;
+  for (int t = 0; t < K; ++t) {
+    if (t == 0)
+      s = forward_impl(draft, kv, ctx, 2, B, 2, -1, logits, base, ws, err, st);
+    else
+      s = forward_impl(draft, kv, tokens + t, K + 1, B, 1, t, logits, base, ws, err, st);
+    if (s != SPS_OK) return s;
+    SPS_HIP(sps::launch_draft_sample(logits, t == 0 ? 2 : 1, B, V, temperature, p_out, K, t, tokens, ctx, rng.seed,
+                                     rng.loop, err, st));
+  }
+  return SPS_OK;
+}
+
+sps_status sps_commit(sps_kv_t kv, const int32_t* tokens, const int32_t* out_tokens, const int32_t* n_accepted,
+                      int32_t B, int32_t K, int32_t* ctx, int32_t* seq_out, int32_t* n_out, int32_t cap,
+                      void* stream) {
+  if (!kv || !tokens || !out_tokens || !n_accepted || !ctx) return SPS_E_INVALID;
+  if (B != kv->B || K < 0 || K > kMaxK) return SPS_E_INVALID;
+  if ((seq_out == nullptr) != (n_out == nullptr)) return SPS_E_INVALID;
+  if (seq_out && cap < 1) return SPS_E_INVALID;
+  SPS_HIP(sps::launch_commit(kv->lengths, tokens, out_tokens, n_accepted, B, K, ctx, seq_out, n_out, cap,
+                             as_stream(stream)));
+  return SPS_OK;
+}
+
+sps_status sps_philox_uniforms(sps_philox rng, int32_t purpose, int32_t B, int32_t n, float* out, void* stream) {
+  if (!out || B < 0 || n < 0 || purpose < 0) return SPS_E_INVALID;
+  SPS_HIP(sps::launch_philox(rng.seed, rng.loop, purpose, B, n, out, as_stream(stream)));
+  return SPS_OK;
+}
+
+sps_status sps_softmax(const float* logits, int32_t rows, int32_t V, float temperature, float* probs, void* stream) {
+  if (!logits || !probs || rows < 0 || V < 2) return SPS_E_INVALID;
+  if (!(temperature >= 0.f) || temperature > 1e30f) return SPS_E_INVALID;
+  SPS_HIP(sps::launch_row_softmax(logits, rows, V, temperature, nullptr, probs, as_stream(stream)));
+  return SPS_OK;
+}
+
+sps_status sps_profile_gemm_begin(void) {
+  g_prof.on = true;
+  g_prof.used = 0;
+  g_prof.bytes.clear();
+  return SPS_OK;
+}
+
+sps_status sps_profile_gemm_end(float* total_ms, int32_t* launches, double* bytes) {
+  if (!total_ms || !launches || !bytes) return SPS_E_INVALID;
+  g_prof.on = false;
+  double ms = 0.0;
+  for (size_t i = 0; i + 1 < g_prof.used; i += 2) {
+    SPS_HIP(hipEventSynchronize(g_prof.ev[i + 1]));
+    float t = 0.f;
+    SPS_HIP(hipEventElapsedTime(&t, g_prof.ev[i], g_prof.ev[i + 1]));
+    ms += t;
+  }
+  double b = 0.0;
+  for (double x : g_prof.bytes) b += x;
+  *total_ms = static_cast<float>(ms);
+  *launches = static_cast<int32_t>(g_prof.used / 2);
+  *bytes = b;
+  g_prof.used = 0;
+  g_prof.bytes.clear();
+  return SPS_OK;
+}
+
+sps_status sps_device_error(void* stream, int32_t clear, int32_t* flags) {
+  if (!flags) return SPS_E_INVALID;
+  SPS_HIP(hipStreamSynchronize(as_stream(stream)));
+  int v = 0;
+  SPS_HIP(hipMemcpyFromSymbol(&v, HIP_SYMBOL(sps_dev_err), sizeof(int), 0, hipMemcpyDeviceToHost));
+  *flags = v;
+  if (clear) {
+    const int zero = 0;
+    SPS_HIP(hipMemcpyToSymbol(HIP_SYMBOL(sps_dev_err), &zero, sizeof(int), 0, hipMemcpyHostToDevice));
+  }
+  return SPS_OK;
+}
+
+}  // extern "C"

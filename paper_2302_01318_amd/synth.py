@@ -112,3 +112,19 @@ def accept_case_device(seed, B, K, V, sigma=2.0, sigma_pert=0.5, device="cuda"):
     drafts = torch.multinomial(p.reshape(B * K, V), 1, generator=gen).reshape(B, K).int() if K else \
         torch.zeros((B, 0), dtype=torch.int32, device=device)
     return p.contiguous(), q.contiguous(), drafts.contiguous()
+
+
+def device_weights(cfg, seed, std=0.02, gain_std=0.1, device="cuda"):
+    """Yield ((name, layer), tensor) for every weight, drawn on the device with
+    torch's generator (same distributions as `weights`; for models too large
+    to draw on the host, e.g. the 70B shape). One tensor is alive at a time."""
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed))
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    for key, shape in tensor_shapes(cfg).items():
+        if key[0].endswith("norm"):
+            t = torch.randn(shape, generator=gen, device=device, dtype=torch.float32).mul_(gain_std).add_(1.0)
+        else:
+            t = torch.randn(shape, generator=gen, device=device, dtype=dt).mul_(std)
+        yield key, t
+        del t

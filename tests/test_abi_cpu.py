@@ -1,0 +1,103 @@
+"""The C ABI on the host, without a GPU: the library loads, exports every
+function include/sps.h declares, and rejects invalid arguments with status
+codes before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+LIB = os.path.join(ROOT, "paper_2302_01318_amd", "libsps.so")
+
+
+@pytest.fixture(scope="module")
+def sps():
+    if not os.path.exists(LIB):
+        from paper_2302_01318_amd import build
+        build.build()
+    from paper_2302_01318_amd import sps as mod
+    return mod
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "sps.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sps_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported(sps):
+    names = declared_functions()
+    assert len(names) >= 19
+    for n in names:
+        assert hasattr(sps.lib, n), n
+    assert sorted(sps.EXPORTS) == names
+
+
+def test_status_strings(sps):
+    assert sps.lib.sps_status_string(0) == b"ok"
+    assert sps.lib.sps_status_string(5) == b"HIP runtime error"
+    assert sps.lib.sps_abi_version() == 1
+
+
+def test_config_validation_and_sizes(sps):
+    from paper_2302_01318_amd import configs
+    good = sps.config_of(configs.SEVENTY_B)
+    assert sps.lib.sps_weight_bytes(ctypes.byref(good)) >= configs.SEVENTY_B.n_params() * 2
+    for field, bad in [("d_model", 100), ("head_dim", 96), ("vocab", 1), ("vocab", 1 << 24), ("d_ff", 48),
+                       ("ffn_kind", 2), ("dtype", 3), ("n_layers", 0)]:
+        c = sps.config_of(configs.SEVENTY_B)
+        setattr(c, field, bad)
+        assert sps.lib.sps_weight_bytes(ctypes.byref(c)) == 0, field
+        h = ctypes.c_void_p()
+        assert sps.lib.sps_model_create(ctypes.byref(c), ctypes.c_void_p(1), ctypes.byref(h)) == 2
+    assert sps.lib.sps_kv_bytes(ctypes.byref(good), 1, 100) == 0          # T_cap % 32
+    assert sps.lib.sps_kv_bytes(ctypes.byref(good), 1, 2304) == 80 * 2 * 64 * 2304 * 128 * 2
+    assert sps.lib.sps_workspace_bytes(ctypes.byref(good), 0, 5, 2304) == 0
+
+
+def test_invalid_arguments_return_codes(sps):
+    Ph = sps.Philox(0, 0)
+    P = ctypes.c_void_p
+    one = P(1)
+    # accept_resample: bad K, bad V, null outputs
+    assert sps.lib.sps_accept_resample(one, one, one, None, Ph, 1, -1, 10, one, one, None) == 1
+    assert sps.lib.sps_accept_resample(one, one, one, None, Ph, 1, 64, 10, one, one, None) == 1
+    assert sps.lib.sps_accept_resample(one, one, one, None, Ph, 1, 2, 1, one, one, None) == 1
+    assert sps.lib.sps_accept_resample(one, one, one, None, Ph, 1, 2, 10, None, one, None) == 1
+    assert sps.lib.sps_accept_resample(None, one, one, None, Ph, 1, 2, 10, one, one, None) == 1
+    # forward / verify / draft / commit with null handles
+    assert sps.lib.sps_forward(None, None, one, 5, 1, 5, 0, None, one, 1 << 30, None) == 1
+    assert sps.lib.sps_verify_step(None, None, one, 1, 4, 1.0, None, None, None, one, 1 << 30, None) == 1
+    assert sps.lib.sps_verify_step(None, None, one, 1, -1, 1.0, None, None, None, one, 1 << 30, None) == 1
+    assert sps.lib.sps_draft_step(None, None, one, 1, 4, -1.0, Ph, one, one, one, 1 << 30, None) == 1
+    assert sps.lib.sps_commit(None, one, one, one, 1, 4, one, None, None, 0, None) == 1
+    assert sps.lib.sps_pack_weight(None, 0, 0, one, one, None) == 2
+    assert sps.lib.sps_philox_uniforms(Ph, 0, 1, 1, None, None) == 1
+    assert sps.lib.sps_softmax(one, 1, 1, 1.0, one, None) == 1
+    assert sps.lib.sps_device_error(None, 0, None) == 1
+
+
+def test_handles_and_shape_checks(sps):
+    from paper_2302_01318_amd import configs
+    tiny = sps.config_of(configs.TINY_TARGET)
+    other = sps.config_of(configs.TINY_DRAFT)
+    m, kv, kv2 = ctypes.c_void_p(), ctypes.c_void_p(), ctypes.c_void_p()
+    one = ctypes.c_void_p(1)
+    assert sps.lib.sps_model_create(ctypes.byref(tiny), one, ctypes.byref(m)) == 0
+    assert sps.lib.sps_kv_create(ctypes.byref(tiny), 2, 64, one, one, ctypes.byref(kv)) == 0
+    assert sps.lib.sps_kv_create(ctypes.byref(other), 2, 64, one, one, ctypes.byref(kv2)) == 0
+    bad = ctypes.c_void_p()
+    assert sps.lib.sps_kv_create(ctypes.byref(tiny), 2, 65, one, one, ctypes.byref(bad)) == 2
+    assert bad.value is None
+    need = sps.lib.sps_workspace_bytes(ctypes.byref(tiny), 2, 5, 64)
+    # workspace too small, batch mismatch, too many tokens per sequence, cache of another model
+    assert sps.lib.sps_forward(m, kv, one, 5, 2, 5, 0, None, one, need - 1, None) == 3
+    assert sps.lib.sps_forward(m, kv, one, 5, 3, 5, 0, None, one, need, None) == 2
+    assert sps.lib.sps_forward(m, kv, one, 65, 2, 65, 0, None, one, 1 << 40, None) == 2
+    assert sps.lib.sps_forward(m, kv2, one, 5, 2, 5, 0, None, one, 1 << 40, None) == 2
+    assert sps.lib.sps_kv_write(kv, 0, 0, 60, 8, one, one, None) == 3
+    assert sps.lib.sps_kv_write(kv, 4, 0, 0, 8, one, one, None) == 1
+    sps.lib.sps_model_destroy(m)
+    sps.lib.sps_kv_destroy(kv)
+    sps.lib.sps_kv_destroy(kv2)

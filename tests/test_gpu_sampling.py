@@ -1,0 +1,140 @@
+"""GPU parity of the sampling side of the hot path against the oracle:
+Philox uniforms (bit-exact), softmax with temperature (fp32 tolerance, greedy
+exact), and modified rejection sampling on given distributions (bit-exact
+tokens and accepted counts over the whole V = 32000 accept/resample grid,
+with explicit and with Philox uniforms, plus the degenerate cases)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import accept as oacc
+from oracle import philox as ophil
+from oracle import sampling as osamp
+from paper_2302_01318_amd import configs, synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("purpose", [0, 1, 2])
+def test_philox_bit_exact(sps, purpose):
+    print("philox purpose", purpose, flush=True)
+    got = sps.philox_uniforms(0x1234ABCD5678, 7, purpose, 1000, 1000).cpu().numpy()
+    want = ophil.uniforms(0x1234ABCD5678, 7, purpose, 1000, 1000)
+    np.testing.assert_array_equal(got, want)
+
+
+@pytest.mark.parametrize("T", [1.0, 0.8, 0.0])
+def test_softmax(sps, T):
+    print("softmax T", T, flush=True)
+    g = np.random.default_rng(4)
+    z = g.normal(0, 2, size=(6, 32000)).astype(np.float32)
+    z[3, 100] = z[3, 5] = z[3].max() + 1.0          # tie for greedy: lowest index wins
+    got = sps.softmax(torch.from_numpy(z).cuda(), T).cpu().numpy()
+    want = osamp.softmax(z.astype(np.float64), T)
+    if T == 0.0:
+        np.testing.assert_array_equal(got, want.astype(np.float32))
+    else:
+        np.testing.assert_allclose(got, want, rtol=2e-5, atol=1e-10)
+        np.testing.assert_allclose(got.sum(-1, dtype=np.float64), 1.0, atol=1e-5)
+
+
+def run_accept(sps, p, q, drafts, unif=None, rng=(0, 0)):
+    B, K1, V = q.shape
+    K = K1 - 1
+    dev = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to("cuda", dt)
+    out, nacc = sps.accept_resample(dev(p, torch.float32) if K else None, dev(q, torch.float32),
+                                    dev(drafts, torch.int32) if K else None,
+                                    dev(unif, torch.float32) if unif is not None else None, rng)
+    return out.cpu().numpy(), nacc.cpu().numpy()
+
+
+GRID = [(B, K) for K in configs.ACCEPT_GRID["K"] for B in configs.ACCEPT_GRID["B"]]
+
+
+@pytest.mark.parametrize("B,K", GRID)
+def test_accept_grid_bit_exact(sps, B, K):
+    V = configs.ACCEPT_GRID["V"]
+    print("accept grid B", B, "K", K, flush=True)
+    p, q, drafts = synth.accept_case(100 + K, B, K, V, configs.ACCEPT_GRID["sigma"],
+                                     configs.ACCEPT_GRID["sigma_pert"])
+    # explicit uniforms
+    unif = np.random.default_rng(B * 10 + K).random((B, K + 1)).astype(np.float32)
+    out, nacc = run_accept(sps, p, q, drafts, unif)
+    w_out, w_n, w_flags = oacc.accept_resample(p, q, drafts, unif)
+    np.testing.assert_array_equal(out, w_out)
+    np.testing.assert_array_equal(nacc, w_n)
+    assert not w_flags.any()
+    # Philox uniforms drawn inside the kernel
+    out, nacc = run_accept(sps, p, q, drafts, None, (99, 5))
+    w_out, w_n, _ = oacc.accept_resample(p, q, drafts, oacc.philox_uniforms(99, 5, B, K))
+    np.testing.assert_array_equal(out, w_out)
+    np.testing.assert_array_equal(nacc, w_n)
+    assert sps.device_error() == 0
+
+
+@pytest.mark.parametrize("sigma_pert", configs.SWEEP["sigma_pert"])
+def test_accept_acceptance_regimes(sps, sigma_pert):
+    B, K, V = 64, 4, 32000
+    p, q, drafts = synth.accept_case(7, B, K, V, 2.0, sigma_pert)
+    out, nacc = run_accept(sps, p, q, drafts, None, (3, 1))
+    w_out, w_n, _ = oacc.accept_resample(p, q, drafts, oacc.philox_uniforms(3, 1, B, K))
+    np.testing.assert_array_equal(out, w_out)
+    np.testing.assert_array_equal(nacc, w_n)
+
+
+def test_accept_degenerate_cases(sps):
+    g = np.random.default_rng(11)
+    V, K, B = 50, 3, 8
+    q = g.dirichlet(np.ones(V), size=(B, K + 1)).astype(np.float32)
+    # q == p: everything accepted for every r < 1
+    p = q[:, :K].copy()
+    drafts = np.stack([[g.choice(V, p=p[b, t].astype(np.float64) / p[b, t].astype(np.float64).sum())
+                        for t in range(K)] for b in range(B)]).astype(np.int32)
+    unif = np.full((B, K + 1), 1 - 2.0 ** -24, np.float32)
+    out, nacc = run_accept(sps, p, q, drafts, unif)
+    assert (nacc == K).all()
+    np.testing.assert_array_equal(out, oacc.accept_resample(p, q, drafts, unif)[0])
+    # p(x~) = 0, zero residual, exact ratio boundary, one-hot (greedy)
+    cases = []
+    p2 = np.full((1, 1, 4), 0.25, np.float32)
+    p2[0, 0] = [0.5, 0.5, 0.0, 0.0]
+    q2 = np.full((1, 2, 4), 0.25, np.float32)
+    for d, r in [(2, 0.999), (0, 0.5), (0, np.float32(0.5 - 2.0 ** -24)), (1, 0.99)]:
+        cases.append((p2, q2, np.array([[d]], np.int32), np.array([[r, 0.37]], np.float32)))
+    pz = np.array([[[0.5, 0.25, 0.25]]], np.float32)
+    qz = np.array([[[0.25, 0.125, 0.125], [1 / 3, 1 / 3, 1 / 3]]], np.float32)
+    for u in (0.0, 0.3, 0.7, 0.99):
+        cases.append((pz, qz, np.array([[1]], np.int32), np.array([[0.75, u]], np.float32)))
+    eye = np.eye(6, dtype=np.float32)
+    cases.append((eye[[2, 5]][None], eye[[2, 4, 1]][None], np.array([[2, 5]], np.int32),
+                  np.array([[0.9, 0.0, 0.5]], np.float32)))
+    cases.append((eye[[2, 5]][None], eye[[2, 5, 1]][None], np.array([[2, 5]], np.int32),
+                  np.array([[0.99, 0.99, 0.5]], np.float32)))
+    for p_, q_, d_, u_ in cases:
+        out, nacc = run_accept(sps, p_, q_, d_, u_)
+        w_out, w_n, _ = oacc.accept_resample(p_, q_, d_, u_)
+        np.testing.assert_array_equal(out, w_out)
+        np.testing.assert_array_equal(nacc, w_n)
+    assert sps.device_error() == 0
+
+
+def test_accept_k0_is_a_draw_from_q(sps):
+    q = np.random.default_rng(5).dirichlet(np.ones(1000), size=(16, 1)).astype(np.float32)
+    unif = np.linspace(0, 1, 16, endpoint=False, dtype=np.float32)[:, None]
+    out, nacc = run_accept(sps, None, q, None, unif)
+    w_out, w_n, _ = oacc.accept_resample(np.zeros((16, 0, 1000), np.float32), q, np.zeros((16, 0), np.int32), unif)
+    np.testing.assert_array_equal(out, w_out)
+    assert (nacc == 0).all()
+
+
+def test_accept_error_flags(sps):
+    sps.device_error()
+    p = np.full((1, 2, 3), 1 / 3, np.float32)
+    q = np.full((1, 3, 3), 1 / 3, np.float32)
+    out, nacc = run_accept(sps, p, q, np.array([[1, 7]], np.int32), np.array([[0, 0, 0.5]], np.float32))
+    assert nacc[0] == 1 and out[0, 0] == 1
+    assert sps.device_error() & sps.DEV_BAD_TOKEN
+    qz = np.zeros((1, 1, 3), np.float32)
+    out, nacc = run_accept(sps, None, qz, None, np.array([[0.3]], np.float32))
+    assert out[0, 0] == 0 and sps.device_error() & sps.DEV_EMPTY
+    assert sps.device_error() == 0
