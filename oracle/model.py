@@ -18,16 +18,19 @@ heads, layers) but not the block design. We read the architecture as:
 
 Weights are float32 arrays in nn.Linear orientation [out][in] (for bf16
 models they hold bf16-representable values). Activations and accumulation
-are fp64. For bf16 models the values a bf16 datapath stores are rounded to
-bf16 (round to nearest even) at these points: the normed activations that
-enter a matmul, q/k after rotation and v (what the KV cache holds), the
-attention output before W_o, and the FFN hidden before the down projection.
-The softmax weights of attention are not rounded. Parity against the GPU
-path is to a tolerance (1e-4 fp32, 2e-2 bf16 on logits), so the paper does
-not pin these values: "parity unpinned" by the paper; the forward itself is
-pinned by the tests in tests/test_oracle_model.py (incremental scoring equals
-full recompute; blocks equal torch fp64 library routines; RoPE equals complex
-rotation).
+are fp64. A bf16 model is read as bf16 WEIGHTS and a bf16 KV CACHE: the
+queries, keys and values of attention are rounded to bf16 (round to nearest
+even) after the rotary encoding, which is what the cache stores and what
+enters the score product; every other activation keeps full precision. (If
+the normed activations, the attention output and the FFN hidden were also
+rounded to bf16, a single last-bit difference upstream flips a large share
+of those roundings downstream, so two faithful implementations with
+different fp32 summation orders would disagree by about 1% of the logit
+scale.) Parity against the GPU path is to a tolerance (1e-4 fp32, 2e-2 bf16
+on logits); the paper prints no values to pin them, so the logits are
+"parity unpinned" by the paper; the forward itself is pinned by the tests in
+tests/test_oracle_model.py (incremental scoring equals full recompute; blocks
+equal torch fp64 library routines; RoPE equals complex rotation).
 """
 from dataclasses import dataclass
 
@@ -67,6 +70,7 @@ def round_bf16(x):
 
 
 def _store(spec, x):
+    """What the KV cache (and the score product) sees: bf16 for bf16 models."""
     return round_bf16(x) if spec.dtype == "bf16" else np.asarray(x, dtype=np.float64)
 
 
@@ -129,7 +133,7 @@ def forward_cached(spec, W, cache, tokens, lengths):
     pos = np.asarray(lengths, dtype=np.int64)[:, None] + np.arange(M)[None, :]
     h = np.asarray(W["embed"], np.float64)[tokens]                     # [B][M][d]
     for li, lw in enumerate(W["layers"]):
-        x = _store(spec, rms_norm(h, lw["attn_norm"], spec.eps))
+        x = rms_norm(h, lw["attn_norm"], spec.eps)
         q = linear(x, lw["wq"]).reshape(B, M, H, Dh)
         k = linear(x, lw["wk"]).reshape(B, M, H, Dh)
         v = linear(x, lw["wv"]).reshape(B, M, H, Dh)
@@ -146,16 +150,16 @@ def forward_cached(spec, W, cache, tokens, lengths):
                 for hh in range(H):
                     o[b, j, hh] = _attend(q[b, j, hh], cache["k"][li, b, hh, :n],
                                           cache["v"][li, b, hh, :n], scale)
-        o = _store(spec, o.reshape(B, M, H * Dh))
+        o = o.reshape(B, M, H * Dh)
         h = h + linear(o, lw["wo"])
-        x = _store(spec, rms_norm(h, lw["ffn_norm"], spec.eps))
+        x = rms_norm(h, lw["ffn_norm"], spec.eps)
         if spec.ffn == "gelu":
-            a = _store(spec, gelu_tanh(linear(x, lw["w1"])))
+            a = gelu_tanh(linear(x, lw["w1"]))
             h = h + linear(a, lw["w2"])
         else:
-            a = _store(spec, silu(linear(x, lw["wg"])) * linear(x, lw["wu"]))
+            a = silu(linear(x, lw["wg"])) * linear(x, lw["wu"])
             h = h + linear(a, lw["wd"])
-    x = _store(spec, rms_norm(h, W["final_norm"], spec.eps))
+    x = rms_norm(h, W["final_norm"], spec.eps)
     return linear(x, W["unembed"])
 
 

@@ -7,7 +7,8 @@
   depend only on the relative position.
 * The whole forward equals a torch fp64 model built from library routines
   (F.linear, F.rms_norm, F.scaled_dot_product_attention with is_causal, F.gelu),
-  for both FFN kinds, in fp32 and bf16 rounding modes.
+  for both FFN kinds, with and without bf16 rounding of the attention
+  operands (q, k, v).
 * Scoring K+1 new tokens against a KV cache equals a full causal recompute
   (the conditionals of the Conditional Scoring section are the same numbers),
   including after a rollback that overwrites uncommitted cache entries.
@@ -81,22 +82,22 @@ def torch_forward(spec, W, tokens):
 
     h = t(W["embed"])[torch.from_numpy(tokens).long()]
     for lw in W["layers"]:
-        x = rb(F.rms_norm(h, (d,), weight=t(lw["attn_norm"]), eps=spec.eps))
+        x = F.rms_norm(h, (d,), weight=t(lw["attn_norm"]), eps=spec.eps)
         q = rb(rope(F.linear(x, t(lw["wq"])).view(B, T, H, Dh)))
         k = rb(rope(F.linear(x, t(lw["wk"])).view(B, T, H, Dh)))
         v = rb(F.linear(x, t(lw["wv"])).view(B, T, H, Dh))
         o = F.scaled_dot_product_attention(q.transpose(1, 2), k.transpose(1, 2), v.transpose(1, 2),
                                            is_causal=True)
-        o = rb(o.transpose(1, 2).reshape(B, T, H * Dh))
+        o = o.transpose(1, 2).reshape(B, T, H * Dh)
         h = h + F.linear(o, t(lw["wo"]))
-        x = rb(F.rms_norm(h, (d,), weight=t(lw["ffn_norm"]), eps=spec.eps))
+        x = F.rms_norm(h, (d,), weight=t(lw["ffn_norm"]), eps=spec.eps)
         if spec.ffn == "gelu":
-            a = rb(F.gelu(F.linear(x, t(lw["w1"])), approximate="tanh"))
+            a = F.gelu(F.linear(x, t(lw["w1"])), approximate="tanh")
             h = h + F.linear(a, t(lw["w2"]))
         else:
-            a = rb(F.silu(F.linear(x, t(lw["wg"]))) * F.linear(x, t(lw["wu"])))
+            a = F.silu(F.linear(x, t(lw["wg"]))) * F.linear(x, t(lw["wu"]))
             h = h + F.linear(a, t(lw["wd"]))
-    x = rb(F.rms_norm(h, (d,), weight=t(W["final_norm"]), eps=spec.eps))
+    x = F.rms_norm(h, (d,), weight=t(W["final_norm"]), eps=spec.eps)
     return F.linear(x, t(W["unembed"])).numpy()
 
 
