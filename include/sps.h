@@ -54,7 +54,7 @@ enum { SPS_DTYPE_F32 = 0, SPS_DTYPE_BF16 = 1 };
  * table). Pre-norm blocks, RMSNorm with learned gains, multi-head attention
  * with rotate-half rotary position encoding, FFN = GELU(tanh) with two
  * matrices or SwiGLU with three, untied embedding / unembedding, no biases.
- * Supported: d_model % 32 == 0, head_dim in {64, 128},
+ * Supported: d_model % 32 == 0, d_model <= 16384, head_dim in {64, 128},
  * (n_heads * head_dim) % 32 == 0, d_ff % 32 == 0, 2 <= vocab < 2^24. */
 typedef struct {
   int32_t d_model, n_layers, n_heads, head_dim, d_ff, vocab;

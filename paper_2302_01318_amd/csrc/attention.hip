@@ -4,36 +4,118 @@
 // P + j sees positions <= P + j). The paper notes this part is bound by the
 // KV-cache reads and is nearly independent of K (Conditional Scoring section).
 //
-// Split-KV: each wave owns 128 consecutive positions (four 32-position blocks)
+// Split-KV: each wave owns 64 consecutive positions (two 32-position blocks)
 // of one (sequence, head) and up to 16 queries per query tile. Per block it
 // computes S^T = K Q^T with MFMA (A = key tile, B = Q^T), runs the online
 // softmax on the S^T registers, and accumulates O^T = V^T P^T (A = value
 // tile, B = the softmax tile as the score MFMA left it in registers, thanks
-// to the value tile layout). Each wave writes its (O, running max, running
-// sum) partial; a second kernel merges the partials of a (sequence, head,
-// query) and normalises.
+// to the value tile layout). The (O, running max, running sum) partials are
+// merged per work-group in LDS when possible; a second kernel merges the
+// partials of a (sequence, head, query) and normalises.
 #include "common.h"
 #include "launch.h"
 
 namespace sps {
 
-constexpr int kPosPerWave = 128;
+constexpr int kWavePos = 64;         // positions per wave: two 32-position blocks
+constexpr int kGroupPos = 4 * kWavePos;  // positions per work-group (4 waves)
 
+// One 32-position block for one query tile: scores, masked online softmax,
+// and accumulation of O^T. For bf16 the softmax weights enter the P V MFMA
+// as a hi + lo pair of bf16 values (p = hi + lo to ~2^-16 relative), so the
+// product is as accurate as an fp32 P at the cost of one more MFMA.
+template <typename T, int DH>
+__device__ __forceinline__ void attn_block(const Frag<T> (&kf)[2][DH / 32], const Frag<T> (&vf)[DH / 16],
+                                           const Frag<T> (&qf)[DH / 32], int pb, int qi, int qpos, bool qvalid,
+                                           int nkv, int grp, float c_log2, float& m_run, float& l_run,
+                                           f32x4 (&o)[DH / 16]) {
+  f32x4 s[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+  for (int pt = 0; pt < 2; ++pt)
+#pragma unroll
+    for (int dt = 0; dt < DH / 32; ++dt) s[pt] = mma8(s[pt], kf[pt][dt], qf[dt]);
+  float mx = -INFINITY;
+#pragma unroll
+  for (int pt = 0; pt < 2; ++pt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int pos = pb * 32 + pt * 16 + grp * 4 + r;
+      const bool valid = qvalid && pos <= qpos && pos < nkv;
+      s[pt][r] = valid ? s[pt][r] : -INFINITY;
+      mx = fmaxf(mx, s[pt][r]);
+    }
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float m_new = fmaxf(m_run, mx);
+  const float m_use = m_new == -INFINITY ? 0.f : m_new;
+  const float alpha = exp2f((m_run - m_use) * c_log2);
+  Frag<T> hi, lo;
+  float ps = 0.f;
+#pragma unroll
+  for (int pt = 0; pt < 2; ++pt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float pv = exp2f((s[pt][r] - m_use) * c_log2);
+      const T h = from_f32<T>(pv);
+      hi.v[pt * 4 + r] = h;
+      lo.v[pt * 4 + r] = from_f32<T>(pv - to_f32(h));
+      ps += pv;
+    }
+  l_run = l_run * alpha + ps;
+  m_run = m_new;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) {
+    o[dt] *= alpha;
+    o[dt] = mma8(o[dt], vf[dt], hi);
+    if (sizeof(T) == 2) o[dt] = mma8(o[dt], vf[dt], lo);
+  }
+}
+
+template <typename T, int DH>
+__device__ __forceinline__ void load_block(const T* __restrict__ kr, const T* __restrict__ vr, int pb, int lane,
+                                           int grp, int nkv, Frag<T> (&kf)[2][DH / 32], Frag<T> (&vf)[DH / 16]) {
+#pragma unroll
+  for (int pt = 0; pt < 2; ++pt)
+#pragma unroll
+    for (int dt = 0; dt < DH / 32; ++dt)
+      kf[pt][dt] = load_frag(kr + ((static_cast<size_t>(pb * 2 + pt) * (DH / 32) + dt) * 64 + lane) * 8);
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt)
+    vf[dt] = load_frag(vr + ((static_cast<size_t>(pb) * (DH / 16) + dt) * 64 + lane) * 8);
+  if (pb * 32 + 32 > nkv) {
+    // Positions past the last written one hold whatever the buffer held;
+    // their softmax weight is 0, but 0 * NaN is not, so clear them.
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int pos = pb * 32 + (e < 4 ? grp * 4 + e : 16 + grp * 4 + e - 4);
+      if (pos >= nkv) {
+#pragma unroll
+        for (int dt = 0; dt < DH / 16; ++dt) vf[dt].v[e] = from_f32<T>(0.f);
+      }
+    }
+  }
+}
+
+// Grid (ceil(T_cap / 256), H, B), 4 waves. Wave w of work-group g covers
+// positions 256 g + 64 w .. +63. With one query tile (QT == 1: up to 16 new
+// tokens per sequence, every verify and draft step) the four waves' partials
+// are merged in LDS and the work-group writes one partial per 256 positions;
+// with more query tiles (prefill chunks) every wave writes its own.
 template <typename T, int DH, int QT>
 __global__ __launch_bounds__(256) void attn_partial_kernel(const T* __restrict__ q, const T* __restrict__ kc,
                                                            const T* __restrict__ vc,
                                                            const int32_t* __restrict__ lengths, int pos_offset,
                                                            int Mps, int H, int T_cap, int NP, float c_log2,
                                                            float* __restrict__ part) {
+  constexpr bool kMerge = QT == 1;
+  constexpr int kPre = 1;   // blocks whose loads are issued together
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int b = blockIdx.z, h = blockIdx.y;
-  const int pw = blockIdx.x * 4 + wave;
-  if (pw >= NP) return;
   const int r16 = lane & 15, grp = lane >> 4;
   const int len = lengths[b] + pos_offset;        // position of query 0
   int nkv = len + Mps;
   if (nkv > T_cap) nkv = T_cap;
-  const int p0 = pw * kPosPerWave;
+  const int p0 = blockIdx.x * kGroupPos + wave * kWavePos;
   const int HD = H * DH;
   const size_t region = (static_cast<size_t>(b) * H + h) * static_cast<size_t>(T_cap) * DH;
   const T* kr = kc + region;
@@ -59,161 +141,163 @@ __global__ __launch_bounds__(256) void attn_partial_kernel(const T* __restrict__
   }
 
   int nblk = nkv > p0 ? (nkv - p0 + 31) / 32 : 0;
-  if (nblk > kPosPerWave / 32) nblk = kPosPerWave / 32;
-  for (int blk = 0; blk < nblk; ++blk) {
-    const int pb = p0 / 32 + blk;
-    Frag<T> kf[2][DH / 32];
-    Frag<T> vf[DH / 16];
+  if (nblk > kWavePos / 32) nblk = kWavePos / 32;
+  for (int b0 = 0; b0 < nblk; b0 += kPre) {
+    Frag<T> kf[kPre][2][DH / 32];
+    Frag<T> vf[kPre][DH / 16];
 #pragma unroll
-    for (int pt = 0; pt < 2; ++pt)
+    for (int u = 0; u < kPre; ++u)
+      if (b0 + u < nblk) load_block<T, DH>(kr, vr, p0 / 32 + b0 + u, lane, grp, nkv, kf[u], vf[u]);
 #pragma unroll
-      for (int dt = 0; dt < DH / 32; ++dt)
-        kf[pt][dt] = load_frag(kr + ((static_cast<size_t>(pb * 2 + pt) * (DH / 32) + dt) * 64 + lane) * 8);
+    for (int u = 0; u < kPre; ++u) {
+      if (b0 + u < nblk) {
 #pragma unroll
-    for (int dt = 0; dt < DH / 16; ++dt)
-      vf[dt] = load_frag(vr + ((static_cast<size_t>(pb) * (DH / 16) + dt) * 64 + lane) * 8);
-    if (pb * 32 + 32 > nkv) {
-      // Positions past the last written one hold whatever the buffer held;
-      // their softmax weight is 0, but 0 * NaN is not, so clear them.
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int pos = pb * 32 + (e < 4 ? grp * 4 + e : 16 + grp * 4 + e - 4);
-        if (pos >= nkv) {
-#pragma unroll
-          for (int dt = 0; dt < DH / 16; ++dt) vf[dt].v[e] = from_f32<T>(0.f);
+        for (int qt = 0; qt < QT; ++qt) {
+          const int qi = qt * 16 + r16;
+          attn_block<T, DH>(kf[u], vf[u], qf[qt], p0 / 32 + b0 + u, qi, len + qi, qi < Mps, nkv, grp, c_log2,
+                            m_run[qt], l_run[qt], o[qt]);
         }
-      }
-    }
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      f32x4 s[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-      for (int pt = 0; pt < 2; ++pt)
-#pragma unroll
-        for (int dt = 0; dt < DH / 32; ++dt) s[pt] = mma8(s[pt], kf[pt][dt], qf[qt][dt]);
-      const int qi = qt * 16 + r16;
-      const int qpos = len + qi;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int pt = 0; pt < 2; ++pt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int pos = pb * 32 + pt * 16 + grp * 4 + r;
-          const bool valid = qi < Mps && pos <= qpos && pos < nkv;
-          s[pt][r] = valid ? s[pt][r] : -INFINITY;
-          mx = fmaxf(mx, s[pt][r]);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run[qt], mx);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = exp2f((m_run[qt] - m_use) * c_log2);
-      Frag<T> pf;
-      float ps = 0.f;
-#pragma unroll
-      for (int pt = 0; pt < 2; ++pt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const T pv = from_f32<T>(exp2f((s[pt][r] - m_use) * c_log2));
-          pf.v[pt * 4 + r] = pv;
-          ps += to_f32(pv);
-        }
-      l_run[qt] = l_run[qt] * alpha + ps;
-      m_run[qt] = m_new;
-#pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt) {
-        o[qt][dt] *= alpha;
-        o[qt][dt] = mma8(o[qt][dt], vf[dt], pf);
       }
     }
   }
 
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
-    float l = l_run[qt];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    const int qi = qt * 16 + r16;
-    if (qi < Mps) {
-      float* dst = part + (((static_cast<size_t>(b) * H + h) * NP + pw) * Mps + qi) * (DH + 2);
+    l_run[qt] += __shfl_xor(l_run[qt], 16);
+    l_run[qt] += __shfl_xor(l_run[qt], 32);
+  }
+  if (kMerge) {
+    __shared__ float sm[4][16], sl[4][16];
+    __shared__ float so[4][16][DH + 1];
+    if (grp == 0) {
+      sm[wave][r16] = m_run[0];
+      sl[wave][r16] = l_run[0];
+    }
 #pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt)
+    for (int dt = 0; dt < DH / 16; ++dt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) dst[dt * 16 + grp * 4 + r] = o[qt][dt][r];
-      if (grp == 0) {
-        dst[DH] = m_run[qt];
-        dst[DH + 1] = l;
+      for (int r = 0; r < 4; ++r) so[wave][r16][dt * 16 + grp * 4 + r] = o[0][dt][r];
+    __syncthreads();
+    float* dst = part + ((static_cast<size_t>(b) * H + h) * NP + blockIdx.x) * Mps * (DH + 2);
+    for (int e = threadIdx.x; e < 16 * DH; e += blockDim.x) {
+      const int qi = e / DH, d = e % DH;
+      if (qi >= Mps) continue;
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) M = fmaxf(M, sm[w][qi]);
+      float L = 0.f, acc = 0.f;
+      if (M != -INFINITY) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const float a = sm[w][qi] == -INFINITY ? 0.f : exp2f((sm[w][qi] - M) * c_log2);
+          L += a * sl[w][qi];
+          acc += a * so[w][qi][d];
+        }
+      }
+      dst[qi * (DH + 2) + d] = acc;
+      if (d == 0) {
+        dst[qi * (DH + 2) + DH] = M;
+        dst[qi * (DH + 2) + DH + 1] = L;
+      }
+    }
+  } else {
+    const int pidx = blockIdx.x * 4 + wave;
+    if (pidx < NP) {
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        const int qi = qt * 16 + r16;
+        if (qi < Mps) {
+          float* dst = part + (((static_cast<size_t>(b) * H + h) * NP + pidx) * Mps + qi) * (DH + 2);
+#pragma unroll
+          for (int dt = 0; dt < DH / 16; ++dt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dst[dt * 16 + grp * 4 + r] = o[qt][dt][r];
+          if (grp == 0) {
+            dst[DH] = m_run[qt];
+            dst[DH + 1] = l_run[qt];
+          }
+        }
       }
     }
   }
 }
 
-// Merge the per-wave partials of one (sequence, query) for all heads and
-// normalise: o = sum_w 2^{(m_w - M) c} O_w / sum_w 2^{(m_w - M) c} l_w.
+// Merge the partials of one (sequence, query) for every head and normalise:
+// o = sum_p 2^{(m_p - M) c} O_p / sum_p 2^{(m_p - M) c} l_p. Each partial
+// covers `pp` positions.
 template <typename T, int DH>
 __global__ __launch_bounds__(DH) void attn_combine_kernel(const float* __restrict__ part, const int32_t* __restrict__ lengths,
-                                                          int pos_offset, int Mps, int H, int T_cap, int NP,
-                                                          float c_log2, T* __restrict__ o) {
+                                                          int pos_offset, int Mps, int H, int T_cap, int NP, int pp,
+                                                          float c_log2, T* __restrict__ o, size_t oplane) {
   const int row = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
   const int b = row / Mps, qi = row % Mps;
   int nkv = lengths[b] + pos_offset + Mps;
   if (nkv > T_cap) nkv = T_cap;
-  int np = (nkv + kPosPerWave - 1) / kPosPerWave;
+  int np = (nkv + pp - 1) / pp;
   if (np > NP) np = NP;
   if (np < 0) np = 0;
   const float* base = part + ((static_cast<size_t>(b) * H + h) * NP * Mps + qi) * (DH + 2);
   const size_t stride = static_cast<size_t>(Mps) * (DH + 2);
   float M = -INFINITY;
+#pragma unroll 8
   for (int p = 0; p < np; ++p) M = fmaxf(M, base[p * stride + DH]);
   float L = 0.f, acc = 0.f;
   if (M != -INFINITY) {
+#pragma unroll 8
     for (int p = 0; p < np; ++p) {
-      const float* pp = base + p * stride;
-      const float mp = pp[DH];
-      if (mp == -INFINITY) continue;
-      const float w = exp2f((mp - M) * c_log2);
-      L += w * pp[DH + 1];
-      acc += w * pp[d];
+      const float* pr = base + p * stride;
+      const float mp = pr[DH];
+      const float w = mp == -INFINITY ? 0.f : exp2f((mp - M) * c_log2);
+      L += w * pr[DH + 1];
+      acc += w * pr[d];
     }
   }
-  o[static_cast<size_t>(row) * H * DH + h * DH + d] = from_f32<T>(L > 0.f ? acc / L : 0.f);
+  store_act(o, oplane, static_cast<size_t>(row) * H * DH + h * DH + d, L > 0.f ? acc / L : 0.f);
 }
 
-int attn_partials(int T_cap) { return (T_cap + kPosPerWave - 1) / kPosPerWave; }
+// Upper bound of partials per (sequence, head): one per wave (prefill).
+int attn_partials(int T_cap) { return (T_cap + kWavePos - 1) / kWavePos; }
 
 template <typename T, int DH>
 static hipError_t attn_t(const void* q, const void* kc, const void* vc, const int32_t* lengths, int pos_offset,
-                         int B, int Mps, int H, int T_cap, float* part, void* o, hipStream_t st) {
-  const int NP = attn_partials(T_cap);
+                         int B, int Mps, int H, int T_cap, float* part, void* o, size_t oplane, hipStream_t st) {
   const float c_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(DH));
-  const dim3 grid((NP + 3) / 4, H, B);
+  const int groups = (T_cap + kGroupPos - 1) / kGroupPos;
+  const dim3 grid(groups, H, B);
   const T* qq = static_cast<const T*>(q);
   const T* kk = static_cast<const T*>(kc);
   const T* vv = static_cast<const T*>(vc);
-  if (Mps <= 16)
+  int NP, pp;
+  if (Mps <= 16) {
+    NP = groups;
+    pp = kGroupPos;
     hipLaunchKernelGGL((attn_partial_kernel<T, DH, 1>), grid, dim3(256), 0, st, qq, kk, vv, lengths, pos_offset,
                        Mps, H, T_cap, NP, c_log2, part);
-  else if (Mps <= 32)
-    hipLaunchKernelGGL((attn_partial_kernel<T, DH, 2>), grid, dim3(256), 0, st, qq, kk, vv, lengths, pos_offset,
-                       Mps, H, T_cap, NP, c_log2, part);
-  else
-    hipLaunchKernelGGL((attn_partial_kernel<T, DH, 4>), grid, dim3(256), 0, st, qq, kk, vv, lengths, pos_offset,
-                       Mps, H, T_cap, NP, c_log2, part);
+  } else {
+    NP = attn_partials(T_cap);
+    pp = kWavePos;
+    if (Mps <= 32)
+      hipLaunchKernelGGL((attn_partial_kernel<T, DH, 2>), grid, dim3(256), 0, st, qq, kk, vv, lengths, pos_offset,
+                         Mps, H, T_cap, NP, c_log2, part);
+    else
+      hipLaunchKernelGGL((attn_partial_kernel<T, DH, 4>), grid, dim3(256), 0, st, qq, kk, vv, lengths, pos_offset,
+                         Mps, H, T_cap, NP, c_log2, part);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3(B * Mps, H), dim3(DH), 0, st, part, lengths, pos_offset,
-                     Mps, H, T_cap, NP, c_log2, static_cast<T*>(o));
+                     Mps, H, T_cap, NP, pp, c_log2, static_cast<T*>(o), oplane);
   return hipGetLastError();
 }
 
 hipError_t launch_attention(int dtype, const void* q, const void* kc, const void* vc, const int32_t* lengths,
                             int pos_offset, int B, int Mps, int H, int DH, int T_cap, float* part, void* o,
-                            hipStream_t st) {
+                            size_t oplane, hipStream_t st) {
   if (dtype == 1)
-    return DH == 128 ? attn_t<bf16, 128>(q, kc, vc, lengths, pos_offset, B, Mps, H, T_cap, part, o, st)
-                     : attn_t<bf16, 64>(q, kc, vc, lengths, pos_offset, B, Mps, H, T_cap, part, o, st);
-  return DH == 128 ? attn_t<float, 128>(q, kc, vc, lengths, pos_offset, B, Mps, H, T_cap, part, o, st)
-                   : attn_t<float, 64>(q, kc, vc, lengths, pos_offset, B, Mps, H, T_cap, part, o, st);
+    return DH == 128 ? attn_t<bf16, 128>(q, kc, vc, lengths, pos_offset, B, Mps, H, T_cap, part, o, oplane, st)
+                     : attn_t<bf16, 64>(q, kc, vc, lengths, pos_offset, B, Mps, H, T_cap, part, o, oplane, st);
+  return DH == 128 ? attn_t<float, 128>(q, kc, vc, lengths, pos_offset, B, Mps, H, T_cap, part, o, oplane, st)
+                   : attn_t<float, 64>(q, kc, vc, lengths, pos_offset, B, Mps, H, T_cap, part, o, oplane, st);
 }
 
 }  // namespace sps

@@ -71,6 +71,17 @@ template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return sta
 __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ float to_f32(bf16 x) { return static_cast<float>(x); }
 
+// Activation format. fp32 models keep activations as fp32 [rows][ld]. bf16
+// models keep each activation x as two bf16 planes, hi = bf16(x) at element
+// i and lo = bf16(x - hi) at element plane + i, so that a bf16 MFMA can
+// consume x at ~2^-16 relative precision (see gemm.hip).
+__device__ __forceinline__ void store_act(float* act, size_t, size_t i, float v) { act[i] = v; }
+__device__ __forceinline__ void store_act(bf16* act, size_t plane, size_t i, float v) {
+  const bf16 h = static_cast<bf16>(v);
+  act[i] = h;
+  act[plane + i] = static_cast<bf16>(v - static_cast<float>(h));
+}
+
 // ---------------------------------------------------------------------------
 // Reductions (deterministic: fixed butterfly order, then waves in order).
 // ---------------------------------------------------------------------------

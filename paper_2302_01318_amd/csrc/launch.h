@@ -11,16 +11,20 @@ enum Epilogue { kEpiStore = 0, kEpiGelu = 1, kEpiSwiglu = 2 };
 //   kEpiStore : out[s][m][n] (fp32, row stride ldo) for split s of S
 //   kEpiGelu  : act[m][n] = gelu_tanh(Y[m][n])            (S must be 1)
 //   kEpiSwiglu: act[m][c] = silu(Y[m][gate c]) * Y[m][up c] (S must be 1)
+// X and act are in the activation format (common.h: fp32, or bf16 hi/lo
+// planes `xplane` / `aplane` elements apart); W is fp32 or bf16; split s of
+// the output lives at out + s * oplane.
 struct GemmArgs {
-  const void* X; int ldx; int M;
+  const void* X; int ldx; size_t xplane; int M;
   const void* W; int N; int KT;   // N: packed rows (16-padded as stored), KT = K / 32
   int n_valid;                    // logical output columns written (<= N; SwiGLU: F)
   int S;
-  float* out; int ldo;
-  void* act; int lda;
+  float* out; int ldo; size_t oplane;
+  void* act; int lda; size_t aplane;
   int epi;
 };
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t st);
+int gemm_max_rows(int dtype);   // rows one launch handles (larger M: several launches)
 int gemm_splits(int dtype, int NT, int KT, int M, int epi);
 
 // Pack canonical rows src[n][k] (n < n_src, k < Kd) into tile order. Row n goes
@@ -30,17 +34,19 @@ int gemm_splits(int dtype, int NT, int KT, int M, int epi);
 hipError_t launch_pack(int dtype, const void* src, int n_src, int Kd, void* dst, int KT, int kind,
                        int row_off, int zero_from, int zero_to, hipStream_t st);
 
+// Activations (x, attention output o, FFN hidden) are in the activation
+// format of common.h; `xplane` is the element distance of the lo plane.
 hipError_t launch_embed_norm(int dtype, const int32_t* tokens, int tok_stride, int Mps, int M,
                              const void* E, int V, int d, const float* gain, float eps, float* h,
-                             void* x, int* err, hipStream_t st);
+                             void* x, size_t xplane, int* err, hipStream_t st);
 hipError_t launch_add_norm(int dtype, float* h, const float* part, int S, int M, int d,
-                           const float* gain, float eps, void* x, hipStream_t st);
+                           const float* gain, float eps, void* x, size_t xplane, hipStream_t st);
 hipError_t launch_rope_kv(int dtype, const float* qkvp, int S, int M, int H, int DH, int Mps,
                           const int32_t* lengths, int pos_offset, float rope_base, void* qout,
                           void* kc, void* vc, int T_cap, int* err, hipStream_t st);
 hipError_t launch_attention(int dtype, const void* q, const void* kc, const void* vc,
                             const int32_t* lengths, int pos_offset, int B, int Mps, int H, int DH,
-                            int T_cap, float* part, void* o, hipStream_t st);
+                            int T_cap, float* part, void* o, size_t oplane, hipStream_t st);
 int attn_partials(int T_cap);
 hipError_t launch_kv_copy(int dtype, int to_cache, void* kc, void* vc, int H, int DH, int T_cap,
                           int pos0, int n, void* k, void* v, hipStream_t st);

@@ -26,7 +26,7 @@ size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 bool valid_config(const sps_config* c) {
   if (!c) return false;
-  if (c->d_model < 32 || c->d_model % 32) return false;
+  if (c->d_model < 32 || c->d_model % 32 || c->d_model > 16384) return false;
   if (c->n_layers < 1 || c->n_heads < 1) return false;
   if (c->head_dim != 64 && c->head_dim != 128) return false;
   if ((c->n_heads * c->head_dim) % 32) return false;
@@ -85,11 +85,11 @@ WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
   const size_t NP = sps::attn_partials(T_cap);
   size_t o = 0;
   w.h = o; o = align256(o + M * L.d * 4);
-  w.x = o; o = align256(o + M * std::max(L.d, L.HD) * es);
+  w.x = o; o = align256(o + M * std::max(L.d, L.HD) * 4);
   w.qkvp = o; o = align256(o + kMaxSplits * M * 3 * L.HD * 4);
   w.qrot = o; o = align256(o + M * L.HD * es);
   w.apart = o; o = align256(o + static_cast<size_t>(B) * L.H * NP * Mps * (L.DH + 2) * 4);
-  w.act = o; o = align256(o + M * L.F * es);
+  w.act = o; o = align256(o + M * L.F * 4);
   w.resp = o; o = align256(o + kMaxSplits * M * L.d * 4);
   w.logits = o; o = align256(o + M * L.V * 4);
   w.stats = o; o = align256(o + M * 2 * 4);
@@ -152,33 +152,48 @@ struct GemmProfile {
 };
 GemmProfile g_prof;
 
-sps_status gemm(int dtype, const void* X, int ldx, int M, const void* W, int N, int KT, int n_valid, int epi,
-                float* out, int ldo, void* act, int lda, int force_S, hipStream_t st) {
-  GemmArgs a{};
-  a.X = X; a.ldx = ldx; a.M = M; a.W = W; a.N = N; a.KT = KT; a.n_valid = n_valid;
-  a.S = force_S > 0 ? force_S : sps::gemm_splits(dtype, N / 16, KT, M, epi);
-  a.out = out; a.ldo = ldo; a.act = act; a.lda = lda; a.epi = epi;
-  hipEvent_t e0 = nullptr, e1 = nullptr;
-  if (g_prof.on) {
-    if (g_prof.used + 2 > g_prof.ev.size()) {
-      for (int i = 0; i < 2; ++i) {
-        hipEvent_t e;
-        SPS_HIP(hipEventCreate(&e));
-        g_prof.ev.push_back(e);
+// Y = X W^T over M rows (several launches when M exceeds one launch's rows).
+// X / act in the activation format with lo planes xplane / aplane elements
+// away; split s of a kEpiStore output at out + s * M * ldo.
+sps_status gemm(int dtype, const void* X, int ldx, size_t xplane, int M, const void* W, int N, int KT, int n_valid,
+                int epi, float* out, int ldo, void* act, int lda, size_t aplane, int S, hipStream_t st) {
+  const int cap = sps::gemm_max_rows(dtype);
+  const size_t es = dtype == 1 ? 2 : 4;   // activation element size
+  for (int m0 = 0; m0 < M; m0 += cap) {
+    const int mc = std::min(cap, M - m0);
+    GemmArgs a{};
+    a.X = static_cast<const char*>(X) + static_cast<size_t>(m0) * ldx * es;
+    a.ldx = ldx; a.xplane = xplane; a.M = mc;
+    a.W = W; a.N = N; a.KT = KT; a.n_valid = n_valid; a.S = S;
+    a.out = out ? out + static_cast<size_t>(m0) * ldo : nullptr;
+    a.ldo = ldo; a.oplane = static_cast<size_t>(M) * ldo;
+    a.act = act ? static_cast<char*>(act) + static_cast<size_t>(m0) * lda * es : nullptr;
+    a.lda = lda; a.aplane = aplane; a.epi = epi;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (g_prof.on) {
+      if (g_prof.used + 2 > g_prof.ev.size()) {
+        for (int i = 0; i < 2; ++i) {
+          hipEvent_t e;
+          SPS_HIP(hipEventCreate(&e));
+          g_prof.ev.push_back(e);
+        }
       }
+      e0 = g_prof.ev[g_prof.used];
+      e1 = g_prof.ev[g_prof.used + 1];
+      g_prof.used += 2;
+      const double wes = dtype == 1 ? 2.0 : 4.0;
+      const double rows_w = epi == sps::kEpiSwiglu ? 2.0 * n_valid : static_cast<double>(n_valid);
+      g_prof.bytes.push_back(rows_w * KT * 32 * wes + 4.0 * mc * KT * 32 + 4.0 * mc * n_valid);
+      SPS_HIP(hipEventRecord(e0, st));
     }
-    e0 = g_prof.ev[g_prof.used];
-    e1 = g_prof.ev[g_prof.used + 1];
-    g_prof.used += 2;
-    const double es = dtype == 1 ? 2.0 : 4.0;
-    const double rows_w = epi == sps::kEpiSwiglu ? 2.0 * n_valid : static_cast<double>(n_valid);
-    const double out_b = epi == sps::kEpiStore ? 4.0 * M * n_valid : es * M * n_valid;
-    g_prof.bytes.push_back(rows_w * KT * 32 * es + es * M * KT * 32 + out_b);
-    SPS_HIP(hipEventRecord(e0, st));
+    SPS_HIP(sps::launch_gemm(dtype, a, st));
+    if (e1) SPS_HIP(hipEventRecord(e1, st));
   }
-  SPS_HIP(sps::launch_gemm(dtype, a, st));
-  if (e1) SPS_HIP(hipEventRecord(e1, st));
   return SPS_OK;
+}
+
+int splits(int dtype, int N, int KT, int M, int epi) {
+  return sps::gemm_splits(dtype, N / 16, KT, std::min(M, sps::gemm_max_rows(dtype)), epi);
 }
 
 // The decoder forward (Conditional Scoring section) over Mps new tokens per
@@ -199,38 +214,40 @@ sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t*
   float* resp = reinterpret_cast<float*>(ws_base + ws.resp);
   const int KTd = L.d / 32, KThd = L.HD / 32, KTf = L.F / 32;
 
+  const size_t xplane = static_cast<size_t>(M) * std::max(L.d, L.HD);   // lo plane of x / o (bf16)
+  const size_t aplane = static_cast<size_t>(M) * L.F;                    // lo plane of the FFN hidden
   SPS_HIP(sps::launch_embed_norm(dt, tokens, tok_stride, Mps, M, m->base + L.embed, L.V, L.d,
-                                 reinterpret_cast<const float*>(layer_ptr(m, 0, L.l_attn_norm)), eps, h, x, err,
-                                 st));
+                                 reinterpret_cast<const float*>(layer_ptr(m, 0, L.l_attn_norm)), eps, h, x, xplane,
+                                 err, st));
   for (int l = 0; l < L.L; ++l) {
-    const int S_qkv = sps::gemm_splits(dt, 3 * L.HD / 16, KTd, M, sps::kEpiStore);
-    sps_status s = gemm(dt, x, L.d, M, layer_ptr(m, l, L.l_qkv), 3 * L.HD, KTd, 3 * L.HD, sps::kEpiStore, qkvp,
-                        3 * L.HD, nullptr, 0, S_qkv, st);
+    const int S_qkv = splits(dt, 3 * L.HD, KTd, M, sps::kEpiStore);
+    sps_status s = gemm(dt, x, L.d, xplane, M, layer_ptr(m, l, L.l_qkv), 3 * L.HD, KTd, 3 * L.HD, sps::kEpiStore,
+                        qkvp, 3 * L.HD, nullptr, 0, 0, S_qkv, st);
     if (s != SPS_OK) return s;
     SPS_HIP(sps::launch_rope_kv(dt, qkvp, S_qkv, M, L.H, L.DH, Mps, kv->lengths, pos_offset, m->cfg.rope_base,
                                 qrot, kv_k(kv, l), kv_v(kv, l), kv->T_cap, err, st));
     SPS_HIP(sps::launch_attention(dt, qrot, kv_k(kv, l), kv_v(kv, l), kv->lengths, pos_offset, B, Mps, L.H, L.DH,
-                                  kv->T_cap, apart, x, st));
-    const int S_o = sps::gemm_splits(dt, L.d / 16, KThd, M, sps::kEpiStore);
-    s = gemm(dt, x, L.HD, M, layer_ptr(m, l, L.l_o), L.d, KThd, L.d, sps::kEpiStore, resp, L.d, nullptr, 0, S_o,
-             st);
+                                  kv->T_cap, apart, x, xplane, st));
+    const int S_o = splits(dt, L.d, KThd, M, sps::kEpiStore);
+    s = gemm(dt, x, L.HD, xplane, M, layer_ptr(m, l, L.l_o), L.d, KThd, L.d, sps::kEpiStore, resp, L.d, nullptr, 0,
+             0, S_o, st);
     if (s != SPS_OK) return s;
     SPS_HIP(sps::launch_add_norm(dt, h, resp, S_o, M, L.d,
-                                 reinterpret_cast<const float*>(layer_ptr(m, l, L.l_ffn_norm)), eps, x, st));
-    s = gemm(dt, x, L.d, M, layer_ptr(m, l, L.l_w1), L.N1, KTd, L.F, L.swiglu ? sps::kEpiSwiglu : sps::kEpiGelu,
-             nullptr, 0, act, L.F, 1, st);
+                                 reinterpret_cast<const float*>(layer_ptr(m, l, L.l_ffn_norm)), eps, x, xplane, st));
+    s = gemm(dt, x, L.d, xplane, M, layer_ptr(m, l, L.l_w1), L.N1, KTd, L.F,
+             L.swiglu ? sps::kEpiSwiglu : sps::kEpiGelu, nullptr, 0, act, L.F, aplane, 1, st);
     if (s != SPS_OK) return s;
-    const int S_2 = sps::gemm_splits(dt, L.d / 16, KTf, M, sps::kEpiStore);
-    s = gemm(dt, act, L.F, M, layer_ptr(m, l, L.l_w2), L.d, KTf, L.d, sps::kEpiStore, resp, L.d, nullptr, 0, S_2,
-             st);
+    const int S_2 = splits(dt, L.d, KTf, M, sps::kEpiStore);
+    s = gemm(dt, act, L.F, aplane, M, layer_ptr(m, l, L.l_w2), L.d, KTf, L.d, sps::kEpiStore, resp, L.d, nullptr, 0,
+             0, S_2, st);
     if (s != SPS_OK) return s;
     const float* next_gain = l + 1 < L.L ? reinterpret_cast<const float*>(layer_ptr(m, l + 1, L.l_attn_norm))
                                          : reinterpret_cast<const float*>(m->base + L.final_norm);
-    SPS_HIP(sps::launch_add_norm(dt, h, resp, S_2, M, L.d, next_gain, eps, x, st));
+    SPS_HIP(sps::launch_add_norm(dt, h, resp, S_2, M, L.d, next_gain, eps, x, xplane, st));
   }
   if (logits) {
-    sps_status s = gemm(dt, x, L.d, M, m->base + L.unembed, L.NU, KTd, L.V, sps::kEpiStore, logits, L.V, nullptr,
-                        0, 1, st);
+    sps_status s = gemm(dt, x, L.d, xplane, M, m->base + L.unembed, L.NU, KTd, L.V, sps::kEpiStore, logits, L.V,
+                        nullptr, 0, 0, 1, st);
     if (s != SPS_OK) return s;
   }
   return SPS_OK;
