@@ -229,11 +229,14 @@ sps_status sps_softmax(const float* logits, int32_t rows, int32_t V, float tempe
 
 /* Measurement helpers. Between begin and end, every weight-streaming GEMM
  * launch (the linear layers: QKV, attention output, FFN, unembedding) is
- * bracketed by HIP events on its stream. end synchronises those events and
- * returns the summed kernel time (ms), the number of launches and their
+ * issued `repeats` (1..64) times back to back between two HIP events on its
+ * stream (the repeats recompute identical outputs; they amortise the event
+ * and dispatch latency so the per-launch time is the kernel's own). end
+ * synchronises the events and returns the summed per-launch kernel time
+ * (ms, divided by repeats), the number of distinct launches and their
  * algorithmic bytes (weights + input activations + outputs, once each).
  * Host-global state: not thread safe. */
-sps_status sps_profile_gemm_begin(void);
+sps_status sps_profile_gemm_begin(int32_t repeats);
 sps_status sps_profile_gemm_end(float* total_ms /*host*/, int32_t* launches /*host*/,
                                 double* bytes /*host*/);
 

@@ -73,7 +73,7 @@ _sig("sps_commit", c_int32, [P, P, P, P, c_int32, c_int32, P, P, P, c_int32, P])
 _sig("sps_philox_uniforms", c_int32, [Philox, c_int32, c_int32, c_int32, P, P])
 _sig("sps_softmax", c_int32, [P, c_int32, c_int32, c_float, P, P])
 _sig("sps_device_error", c_int32, [P, c_int32, ctypes.POINTER(c_int32)])
-_sig("sps_profile_gemm_begin", c_int32, [])
+_sig("sps_profile_gemm_begin", c_int32, [c_int32])
 _sig("sps_profile_gemm_end", c_int32, [ctypes.POINTER(c_float), ctypes.POINTER(c_int32),
                                        ctypes.POINTER(ctypes.c_double)])
 
@@ -263,8 +263,8 @@ def device_error(clear=True):
     return flags.value
 
 
-def profile_gemm_begin():
-    check(lib.sps_profile_gemm_begin(), "sps_profile_gemm_begin")
+def profile_gemm_begin(repeats=1):
+    check(lib.sps_profile_gemm_begin(repeats), "sps_profile_gemm_begin")
 
 
 def profile_gemm_end():
