@@ -82,6 +82,26 @@ __device__ __forceinline__ void store_act(bf16* act, size_t plane, size_t i, flo
   act[plane + i] = static_cast<bf16>(v - static_cast<float>(h));
 }
 
+// KV cache layout, per (layer, sequence, head), each of K and V holding
+// T_cap positions x DH dims in the model dtype:
+//   keys   : 16-position x 32-dim tiles, tile (p/16, d/32) in MFMA A-operand
+//            order -- element (p, d) in lane (p%16) + 16 ((d%32)/8), slot d%8.
+//   values : 32-position x 16-dim tiles, tile (p/32, d/16), element (p, d)
+//            in lane (d%16) + 16 g, slot e, where position p%32 = 4 g + e for
+//            p%32 < 16 and 16 + 4 g + (e-4) otherwise. This is the A operand
+//            of the P V product whose B operand is the softmax tile exactly
+//            as the score MFMA leaves it in registers (see attention.hip).
+__device__ __forceinline__ size_t k_offset(int p, int d, int DH) {
+  return ((static_cast<size_t>(p >> 4) * (DH >> 5) + (d >> 5)) * 64 + (p & 15) + 16 * ((d & 31) >> 3)) * 8 +
+         (d & 7);
+}
+__device__ __forceinline__ size_t v_offset(int p, int d, int DH) {
+  const int pp = p & 31;
+  const int g = pp < 16 ? (pp >> 2) : ((pp - 16) >> 2);
+  const int e = pp < 16 ? (pp & 3) : 4 + ((pp - 16) & 3);
+  return ((static_cast<size_t>(p >> 5) * (DH >> 4) + (d >> 4)) * 64 + (d & 15) + 16 * g) * 8 + e;
+}
+
 // ---------------------------------------------------------------------------
 // Reductions (deterministic: fixed butterfly order, then waves in order).
 // ---------------------------------------------------------------------------

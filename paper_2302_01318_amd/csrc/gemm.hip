@@ -20,13 +20,22 @@
 // product up to fp32 accumulation at the cost of no extra instruction (at
 // M <= 8 the lo half uses rows that would otherwise multiply zeros).
 //
-// Grid: one work-group per (16-column output tile, K split). Its waves walk
-// the split's k-tiles in chunks of U, round robin, each accumulating one
-// 16 x 16 fp32 tile per M tile with MFMA; the waves' partials are summed in
-// LDS and the epilogue applies GELU / SwiGLU or stores fp32 split partials
-// (summed by the consumer kernel, so results do not depend on atomics).
-#include <cstdlib>
-
+// Grid: one work-group per group of NTW 16-column output tiles; every
+// work-group owns its output columns over the whole K, so epilogues can
+// finish them without atomics. Its waves walk the k-tiles in chunks of U,
+// round robin, each accumulating one 16 x 16 fp32 tile per (n-tile, M tile)
+// with MFMA; the waves' partials are summed in LDS in a fixed order.
+//
+// Epilogues fuse the per-token work around each matmul:
+//  * input RMSNorm: the producer of a normed activation writes u = h * gain
+//    and per-column-group sums of squares; the consumer multiplies its
+//    output row m by rs[m] = 1/sqrt(mean h^2 + eps) (RMSNorm is linear in h
+//    once rs is known), so no separate norm kernel runs;
+//  * residual (W_O, W_2): h += Y, then u = h * gain of the next norm and the
+//    group's sums of squares;
+//  * QKV: rotary encoding of q and k (rotate-half pairs are packed side by
+//    side in one 16-row tile) and the KV-cache append;
+//  * FFN: GELU or SwiGLU.
 #include "common.h"
 #include "launch.h"
 
@@ -42,23 +51,29 @@ template <typename T> struct ActRows;
 template <> struct ActRows<bf16> { static constexpr int kRows = 8; };
 template <> struct ActRows<float> { static constexpr int kRows = 16; };
 
-template <typename T, int MT, int NTW, int WAVES, int U, int EPI, int MINW>
-__global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(MINW, 8))) void gemm_kernel(
-    const T* __restrict__ X, int ldx, size_t xplane, int M, const T* __restrict__ W, int NT, int KT, int S,
-    int n_valid, float* __restrict__ out, int ldo, size_t oplane, T* __restrict__ act, int lda, size_t aplane) {
+// Packed position of dim f of a head in a QKV tile: the rotate-half partners
+// f and f + DH/2 sit in rows r and r + 8 of the same 16-row tile.
+__host__ __device__ __forceinline__ int rope_pack_index(int f, int DH) {
+  const int half = DH / 2;
+  return f < half ? (f / 8) * 16 + f % 8 : ((f - half) / 8) * 16 + 8 + (f - half) % 8;
+}
+
+template <typename T, int MT, int NTW, int WAVES, int U, int EPI>
+__global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
   constexpr int kTile = 512;  // elements per 16 x 32 tile
   constexpr int kRows = ActRows<T>::kRows;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int nt0 = blockIdx.x * NTW, s = blockIdx.y;
-  const int kt0 = static_cast<int>((static_cast<long>(KT) * s) / S);
-  const int kt1 = static_cast<int>((static_cast<long>(KT) * (s + 1)) / S);
+  const int nt0 = blockIdx.x * NTW;
+  const int KT = p.KT, M = p.M;
   const int r16 = lane & 15, grp = lane >> 4;
+  const T* X = static_cast<const T*>(p.X);
+  const T* W = static_cast<const T*>(p.W);
 
   const T* wp[NTW];
   bool wv[NTW];
 #pragma unroll
   for (int j = 0; j < NTW; ++j) {
-    wv[j] = nt0 + j < NT;
+    wv[j] = nt0 + j < p.NT;
     wp[j] = W + static_cast<size_t>(wv[j] ? nt0 + j : 0) * KT * kTile + lane * 8;
   }
   const T* xp[MT];
@@ -66,9 +81,9 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(MINW
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     const int m = mt * kRows + (kRows == 8 ? (r16 & 7) : r16);
-    const size_t plane = kRows == 8 ? (r16 >> 3) * xplane : 0;
+    const size_t plane = kRows == 8 ? (r16 >> 3) * p.xplane : 0;
     xv[mt] = m < M;
-    xp[mt] = X + plane + static_cast<size_t>(xv[mt] ? m : 0) * ldx + grp * 8;
+    xp[mt] = X + plane + static_cast<size_t>(p.m0 + (xv[mt] ? m : 0)) * p.ldx + grp * 8;
   }
   f32x4 acc[NTW][MT];
 #pragma unroll
@@ -76,8 +91,8 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(MINW
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  int kb = kt0 + wave * U;
-  for (; kb + U <= kt1; kb += WAVES * U) {
+  int kb = wave * U;
+  for (; kb + U <= KT; kb += WAVES * U) {
     Frag<T> b[NTW][U];
     Frag<T> a[MT][U];
 #pragma unroll
@@ -96,11 +111,11 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(MINW
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[j][mt] = mma8(acc[j][mt], a[mt][u], b[j][u]);
   }
-  if (kb < kt1) {  // ragged last chunk of this wave
+  if (kb < KT) {  // ragged last chunk of this wave
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int kt = kb + u;
-      if (kt < kt1) {
+      if (kt < KT) {
         Frag<T> aa[MT];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) aa[mt] = xv[mt] ? load_frag(xp[mt] + kt * 32) : Frag<T>::zero();
@@ -114,15 +129,29 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(MINW
     }
   }
 
-  // Sum the waves' partials in LDS, then the epilogue.
+  // Sum the waves' partials in LDS (fixed order), then the epilogue.
+  constexpr int kMaxRows = MT * kRows;
   __shared__ float red[WAVES][NTW][MT][4][64];
   __shared__ float tot[NTW][MT][4][64];
+  __shared__ float s_rs[kMaxRows];
+  __shared__ float s_sq[EPI == kEpiResid ? kMaxRows : 1][NTW * 16 + 1];
 #pragma unroll
   for (int j = 0; j < NTW; ++j)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) red[wave][j][mt][r][lane] = acc[j][mt][r];
+  // Row scales of the input RMSNorm: rs[m] = 1 / sqrt(sum_g ss_in[g][m] / d + eps).
+  for (int m = wave; m < kMaxRows; m += WAVES) {
+    float v = 1.f;
+    if (p.ss_in && m < M) {
+      float s = 0.f;
+      for (int g = lane; g < p.ng_in; g += 64) s += p.ss_in[static_cast<size_t>(g) * p.Mtot + p.m0 + m];
+      s = wave_sum(s);
+      v = 1.0f / sqrtf(s * p.inv_d + p.eps);
+    }
+    if (lane == 0) s_rs[m] = v;
+  }
   __syncthreads();
   for (int e = threadIdx.x; e < NTW * MT * 256; e += WAVES * 64) {
     const int j = e / (MT * 256), mt = (e >> 8) % MT, r = (e >> 6) & 3, ln = e & 63;
@@ -132,128 +161,142 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(MINW
     tot[j][mt][r][ln] = v;
   }
   __syncthreads();
+
+  // Value of output (row i of M tile mt, column ln & 15 of n-tile j) with the
+  // lo-plane rows of a bf16 tile folded in.
+  auto out_value = [&](int j, int mt, int r, int ln) -> float {
+    return kRows == 8 ? tot[j][mt][r][ln] + tot[j][mt][r][ln + 32] : tot[j][mt][r][ln];
+  };
   for (int e = threadIdx.x; e < NTW * MT * 256; e += WAVES * 64) {
     const int j = e / (MT * 256), mt = (e >> 8) % MT, r = (e >> 6) & 3, ln = e & 63;
     const int nt = nt0 + j;
-    if (nt >= NT) continue;
     const int i = (ln >> 4) * 4 + r;          // MFMA output row
-    if (kRows == 8 && i >= 8) continue;       // lo rows are folded into their hi row
-    const int m = mt * kRows + i;
     const int col = ln & 15;
-    if (m >= M) continue;
-    const float v = kRows == 8 ? tot[j][mt][r][ln] + tot[j][mt][r][ln + 32] : tot[j][mt][r][ln];
+    const int m = mt * kRows + i;
+    if (kRows == 8 && i >= 8) continue;       // lo rows are folded into their hi row
+    if (EPI == kEpiResid) s_sq[m < kMaxRows ? m : 0][j * 16 + col] = 0.f;
+    if (nt >= p.NT || m >= M) continue;
+    const int gm = p.m0 + m;
+    const float rs = s_rs[m];
+    const float v = out_value(j, mt, r, ln) * rs;
     if (EPI == kEpiStore) {
       const int n = nt * 16 + col;
-      if (n < n_valid) out[s * oplane + static_cast<size_t>(m) * ldo + n] = v;
+      if (n < p.n_valid) p.out[static_cast<size_t>(gm) * p.ldo + n] = v;
     } else if (EPI == kEpiGelu) {
       const int n = nt * 16 + col;
-      if (n < n_valid) store_act(act, aplane, static_cast<size_t>(m) * lda + n, gelu_tanh(v));
-    } else {  // SwiGLU: packed rows 0..7 are gate columns, 8..15 the matching up columns
+      if (n < p.n_valid) store_act(static_cast<T*>(p.act), p.aplane, static_cast<size_t>(gm) * p.lda + n, gelu_tanh(v));
+    } else if (EPI == kEpiSwiglu) {  // packed rows 0..7 gate columns, 8..15 the matching up columns
       if (col < 8) {
         const int c = nt * 8 + col;
-        const float up = kRows == 8 ? tot[j][mt][r][ln + 8] + tot[j][mt][r][ln + 40] : tot[j][mt][r][ln + 8];
-        if (c < n_valid) store_act(act, aplane, static_cast<size_t>(m) * lda + c, silu(v) * up);
+        const float up = out_value(j, mt, r, ln + 8) * rs;
+        if (c < p.n_valid) store_act(static_cast<T*>(p.act), p.aplane, static_cast<size_t>(gm) * p.lda + c, silu(v) * up);
       }
+    } else if (EPI == kEpiResid) {
+      const int n = nt * 16 + col;
+      if (n < p.n_valid) {
+        float* hp = p.h + static_cast<size_t>(gm) * p.n_valid + n;
+        const float hn = *hp + v;
+        *hp = hn;
+        store_act(static_cast<T*>(p.u), p.uplane, static_cast<size_t>(gm) * p.ldu + n, hn * p.gain[n]);
+        s_sq[m][j * 16 + col] = hn * hn;
+      }
+    } else {  // kEpiQkv
+      const int n = nt * 16 + col;
+      const int HD = p.H * p.DH;
+      const int b = gm / p.Mps, jr = gm % p.Mps;
+      const int pos = p.lengths[b] + p.pos_offset + jr;
+      const bool ok = pos >= 0 && pos < p.T_cap;
+      if (!ok && n == 0) atomicOr(p.err, kErrCapacity);
+      if (n < 2 * HD) {                        // q or k: rotate the pair held by columns col, col + 8
+        if (col < 8) {
+          const int hh = (n % HD) / p.DH, pi = n % p.DH;
+          const int f = (pi / 16) * 8 + col;
+          const float x1 = v, x2 = out_value(j, mt, r, ln + 8) * rs;
+          const double inv = exp2(-2.0 * f / p.DH * log2(static_cast<double>(p.rope_base)));
+          double sn, cs;
+          sincos(static_cast<double>(pos) * inv, &sn, &cs);
+          const float c = static_cast<float>(cs), s = static_cast<float>(sn);
+          const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
+          const int half = p.DH / 2;
+          if (n < HD) {
+            T* q = static_cast<T*>(p.q) + static_cast<size_t>(gm) * HD + hh * p.DH;
+            q[f] = from_f32<T>(y1);
+            q[f + half] = from_f32<T>(y2);
+          } else if (ok) {
+            T* kr = static_cast<T*>(p.kc) + (static_cast<size_t>(b) * p.H + hh) * p.T_cap * p.DH;
+            kr[k_offset(pos, f, p.DH)] = from_f32<T>(y1);
+            kr[k_offset(pos, f + half, p.DH)] = from_f32<T>(y2);
+          }
+        }
+      } else if (ok && n < 3 * HD) {           // v: straight into the cache
+        const int hh = (n - 2 * HD) / p.DH, dd = (n - 2 * HD) % p.DH;
+        T* vr = static_cast<T*>(p.vc) + (static_cast<size_t>(b) * p.H + hh) * p.T_cap * p.DH;
+        vr[v_offset(pos, dd, p.DH)] = from_f32<T>(v);
+      }
+    }
+  }
+  if (EPI == kEpiResid) {
+    // Sums of squares of this group's columns, per row, in a fixed order.
+    __syncthreads();
+    if (static_cast<int>(threadIdx.x) < M) {
+      const int m = threadIdx.x;
+      float s = 0.f;
+      for (int c = 0; c < NTW * 16; ++c) s += s_sq[m][c];
+      p.ss_out[static_cast<size_t>(blockIdx.x) * p.Mtot + p.m0 + m] = s;
     }
   }
 }
 
-template <typename T, int MT, int NTW, int WAVES, int U, int MINW = 1>
-static hipError_t gemm_dispatch_epi(const GemmArgs& a, hipStream_t st) {
-  const int NT = a.N / 16;
-  const dim3 grid((NT + NTW - 1) / NTW, a.S), block(WAVES * 64);
-  const T* X = static_cast<const T*>(a.X);
-  const T* W = static_cast<const T*>(a.W);
-  T* act = static_cast<T*>(a.act);
-  switch (a.epi) {
-    case kEpiStore:
-      hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiStore, MINW>), grid, block, 0, st, X, a.ldx, a.xplane,
-                         a.M, W, NT, a.KT, a.S, a.n_valid, a.out, a.ldo, a.oplane, act, a.lda, a.aplane);
-      break;
-    case kEpiGelu:
-      hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiGelu, MINW>), grid, block, 0, st, X, a.ldx, a.xplane,
-                         a.M, W, NT, a.KT, a.S, a.n_valid, a.out, a.ldo, a.oplane, act, a.lda, a.aplane);
-      break;
-    default:
-      hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiSwiglu, MINW>), grid, block, 0, st, X, a.ldx, a.xplane,
-                         a.M, W, NT, a.KT, a.S, a.n_valid, a.out, a.ldo, a.oplane, act, a.lda, a.aplane);
-      break;
+// Launch shape for one launch: n-tiles per wave, waves per work-group, k-tiles
+// per chunk. A single M tile (every verify and draft step) streams two n-tiles
+// per wave with 8-wave work-groups when there are enough output tiles to fill
+// the GPU, else one n-tile per wave with 16-wave work-groups; either way about
+// 24-32 waves per CU keep 8 KiB each in flight.
+template <typename T, int MT, int NTW, int WAVES, int U>
+static hipError_t gemm_launch(const GemmParams& p, hipStream_t st) {
+  const dim3 grid((p.NT + NTW - 1) / NTW), block(WAVES * 64);
+  switch (p.epi) {
+    case kEpiStore: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiStore>), grid, block, 0, st, p); break;
+    case kEpiGelu: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiGelu>), grid, block, 0, st, p); break;
+    case kEpiSwiglu: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiSwiglu>), grid, block, 0, st, p); break;
+    case kEpiResid: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiResid>), grid, block, 0, st, p); break;
+    default: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiQkv>), grid, block, 0, st, p); break;
   }
   return hipGetLastError();
 }
 
-// Launch shape of the single-M-tile case (every verify and draft step):
-// n-tiles per wave, waves per work-group, k-tiles per chunk. Overridable with
-// SPS_GEMM_SHAPE=<index> for tuning sweeps.
-struct GemmShape { int ntw, waves, u; };
-constexpr GemmShape kShapes[] = {{1, 8, 8}, {2, 8, 8}, {2, 4, 8}, {4, 4, 4}, {1, 4, 16}, {2, 8, 4},
-                                 {2, 8, 2}, {1, 8, 4}, {2, 4, 4}, {4, 4, 2}};
-constexpr int kDefaultShape = 5;
-
-int gemm_shape_index() {
-  static int idx = -1;
-  if (idx < 0) {
-    const char* e = getenv("SPS_GEMM_SHAPE");
-    int v = e ? atoi(e) : kDefaultShape;
-    if (v < 0 || v >= static_cast<int>(sizeof(kShapes) / sizeof(kShapes[0]))) v = kDefaultShape;
-    idx = v;
-  }
-  return idx;
-}
+static int single_tile_ntw(int NT) { return (NT % 2 == 0 && NT / 2 >= 512) ? 2 : 1; }
 
 template <typename T>
-static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t st) {
+static hipError_t gemm_dispatch(const GemmParams& p, hipStream_t st) {
   constexpr bool kB = sizeof(T) == 2;
-  const int MT = (a.M + ActRows<T>::kRows - 1) / ActRows<T>::kRows;
-  if constexpr (kB) {
-    if (MT == 1) switch (gemm_shape_index()) {
-      case 1: return gemm_dispatch_epi<T, 1, 2, 8, 8>(a, st);
-      case 2: return gemm_dispatch_epi<T, 1, 2, 4, 8>(a, st);
-      case 3: return gemm_dispatch_epi<T, 1, 4, 4, 4>(a, st);
-      case 4: return gemm_dispatch_epi<T, 1, 1, 4, 16>(a, st);
-      case 5: return gemm_dispatch_epi<T, 1, 2, 8, 4>(a, st);
-      case 6: return gemm_dispatch_epi<T, 1, 2, 8, 2, 8>(a, st);
-      case 7: return gemm_dispatch_epi<T, 1, 1, 8, 4, 8>(a, st);
-      case 8: return gemm_dispatch_epi<T, 1, 2, 4, 4, 6>(a, st);
-      case 9: return gemm_dispatch_epi<T, 1, 4, 4, 2, 8>(a, st);
-      default: return gemm_dispatch_epi<T, 1, 1, 8, 8>(a, st);
-    }
+  const int MT = (p.M + ActRows<T>::kRows - 1) / ActRows<T>::kRows;
+  if (MT == 1) {
+    if (p.Mtot <= ActRows<T>::kRows && single_tile_ntw(p.NT) == 2) return gemm_launch<T, 1, 2, 8, 4>(p, st);
+    return gemm_launch<T, 1, 1, 16, 4>(p, st);
   }
   switch (MT) {
-    case 1: return gemm_dispatch_epi<T, 1, 1, 8, kB ? 8 : 4>(a, st);
-    case 2: return gemm_dispatch_epi<T, 2, 1, 8, kB ? 8 : 4>(a, st);
-    case 3: return gemm_dispatch_epi<T, 3, 1, 4, kB ? 8 : 4>(a, st);
-    case 4: return gemm_dispatch_epi<T, 4, 1, 4, kB ? 8 : 4>(a, st);
+    case 2: return gemm_launch<T, 2, 1, 8, kB ? 8 : 4>(p, st);
+    case 3: return gemm_launch<T, 3, 1, 4, kB ? 8 : 4>(p, st);
+    case 4: return gemm_launch<T, 4, 1, 4, kB ? 8 : 4>(p, st);
     case 5:
-    case 6: return gemm_dispatch_epi<T, 6, 1, 4, 4>(a, st);
+    case 6: return gemm_launch<T, 6, 1, 4, 4>(p, st);
     case 7:
-    case 8: return gemm_dispatch_epi<T, 8, 1, 4, 4>(a, st);
-    default: return gemm_dispatch_epi<T, 10, 1, 4, 2>(a, st);
+    case 8: return gemm_launch<T, 8, 1, 4, 4>(p, st);
+    default: return gemm_launch<T, 10, 1, 4, 2>(p, st);
   }
 }
 
 int gemm_max_rows(int dtype) { return 10 * (dtype == 1 ? ActRows<bf16>::kRows : ActRows<float>::kRows); }
 
-hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t st) {
-  return dtype == 1 ? gemm_dispatch<bf16>(a, st) : gemm_dispatch<float>(a, st);
+int gemm_groups(int dtype, int NT, int Mtot) {
+  const int rows = dtype == 1 ? ActRows<bf16>::kRows : ActRows<float>::kRows;
+  const int ntw = (Mtot <= rows) ? single_tile_ntw(NT) : 1;
+  return (NT + ntw - 1) / ntw;
 }
 
-int gemm_splits(int dtype, int NT, int KT, int M, int epi) {
-  if (epi != kEpiStore) return 1;
-  const int MT = (M + (dtype == 1 ? 7 : 15)) / (dtype == 1 ? 8 : 16);
-  int ntw = 1, waves = MT <= 2 ? 8 : 4;
-  int U = MT >= 9 ? 2 : ((dtype == 1 && MT <= 4) ? 8 : 4);
-  if (MT == 1 && dtype == 1) {
-    const GemmShape g = kShapes[gemm_shape_index()];
-    ntw = g.ntw; waves = g.waves; U = g.u;
-  }
-  const int groups = (NT + ntw - 1) / ntw;
-  const int per_round = waves * U;
-  int S = 2048 / (groups > 0 ? groups : 1);
-  if (S > 8) S = 8;
-  const int cap = KT / per_round;
-  if (S > cap) S = cap;
-  return S < 1 ? 1 : S;
+hipError_t launch_gemm(int dtype, const GemmParams& p, hipStream_t st) {
+  return dtype == 1 ? gemm_dispatch<bf16>(p, st) : gemm_dispatch<float>(p, st);
 }
 
 // ---------------------------------------------------------------------------
@@ -261,12 +304,14 @@ int gemm_splits(int dtype, int NT, int KT, int M, int epi) {
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ void pack_kernel(const T* __restrict__ src, int n_src, int Kd, T* __restrict__ dst, int KT,
-                            int kind, int row_off) {
+                            int kind, int row_off, int dh) {
   const int groups = Kd / 8;
   const long i = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i >= static_cast<long>(n_src) * groups) return;
   const int n = static_cast<int>(i / groups), k = static_cast<int>(i % groups) * 8;
-  const int nf = kind == 0 ? row_off + n : (n / 8) * 16 + row_off * 8 + (n % 8);
+  const int nf = kind == 0   ? row_off + n
+                 : kind == 1 ? (n / 8) * 16 + row_off * 8 + (n % 8)
+                             : row_off + (n / dh) * dh + rope_pack_index(n % dh, dh);
   const int nt = nf / 16, rr = nf % 16, kt = k / 32, grp = (k % 32) / 8;
   const size_t o = ((static_cast<size_t>(nt) * KT + kt) * 64 + rr + 16 * grp) * 8;
   const T* s = src + static_cast<size_t>(n) * Kd + k;
@@ -287,12 +332,12 @@ __global__ void pack_zero_kernel(T* __restrict__ dst, int KT, int zero_from, int
 }
 
 template <typename T>
-static hipError_t pack_t(const void* src, int n_src, int Kd, void* dst, int KT, int kind, int row_off,
+static hipError_t pack_t(const void* src, int n_src, int Kd, void* dst, int KT, int kind, int row_off, int dh,
                          int zero_from, int zero_to, hipStream_t st) {
   const long work = static_cast<long>(n_src) * (Kd / 8);
   if (work > 0)
     hipLaunchKernelGGL(pack_kernel<T>, dim3(static_cast<unsigned>((work + 255) / 256)), dim3(256), 0, st,
-                       static_cast<const T*>(src), n_src, Kd, static_cast<T*>(dst), KT, kind, row_off);
+                       static_cast<const T*>(src), n_src, Kd, static_cast<T*>(dst), KT, kind, row_off, dh);
   const long zwork = static_cast<long>(zero_to - zero_from) * KT * 4;
   if (zwork > 0)
     hipLaunchKernelGGL(pack_zero_kernel<T>, dim3(static_cast<unsigned>((zwork + 255) / 256)), dim3(256), 0,
@@ -301,9 +346,9 @@ static hipError_t pack_t(const void* src, int n_src, int Kd, void* dst, int KT, 
 }
 
 hipError_t launch_pack(int dtype, const void* src, int n_src, int Kd, void* dst, int KT, int kind,
-                       int row_off, int zero_from, int zero_to, hipStream_t st) {
-  return dtype == 1 ? pack_t<bf16>(src, n_src, Kd, dst, KT, kind, row_off, zero_from, zero_to, st)
-                    : pack_t<float>(src, n_src, Kd, dst, KT, kind, row_off, zero_from, zero_to, st);
+                       int row_off, int dh, int zero_from, int zero_to, hipStream_t st) {
+  return dtype == 1 ? pack_t<bf16>(src, n_src, Kd, dst, KT, kind, row_off, dh, zero_from, zero_to, st)
+                    : pack_t<float>(src, n_src, Kd, dst, KT, kind, row_off, dh, zero_from, zero_to, st);
 }
 
 }  // namespace sps

@@ -5,45 +5,55 @@
 
 namespace sps {
 
-enum Epilogue { kEpiStore = 0, kEpiGelu = 1, kEpiSwiglu = 2 };
+enum Epilogue { kEpiStore = 0, kEpiGelu = 1, kEpiSwiglu = 2, kEpiResid = 3, kEpiQkv = 4 };
 
 // Y = X W^T for a packed weight W (see gemm.hip). dtype: 0 fp32, 1 bf16.
-//   kEpiStore : out[s][m][n] (fp32, row stride ldo) for split s of S
-//   kEpiGelu  : act[m][n] = gelu_tanh(Y[m][n])            (S must be 1)
-//   kEpiSwiglu: act[m][c] = silu(Y[m][gate c]) * Y[m][up c] (S must be 1)
-// X and act are in the activation format (common.h: fp32, or bf16 hi/lo
-// planes `xplane` / `aplane` elements apart); W is fp32 or bf16; split s of
-// the output lives at out + s * oplane.
-struct GemmArgs {
-  const void* X; int ldx; size_t xplane; int M;
-  const void* W; int N; int KT;   // N: packed rows (16-padded as stored), KT = K / 32
-  int n_valid;                    // logical output columns written (<= N; SwiGLU: F)
-  int S;
-  float* out; int ldo; size_t oplane;
+// X, act and u are in the activation format (common.h: fp32, or bf16 hi/lo
+// planes `*plane` elements apart). Rows are global rows m0 .. m0+M-1 of a
+// forward over Mtot rows.
+//
+// Input normalisation: if ss_in != NULL, Y[m][:] *= rs[m] with
+// rs[m] = 1 / sqrt(sum_g ss_in[g * Mtot + m] / d + eps) over g < ng_in.
+// Since RMSNorm(h) W^T = rs * (h * gain) W^T, a normed matmul takes
+// u = h * gain as its input and the scale in its epilogue.
+//
+//   kEpiStore : out[m][n] = Y (fp32)
+//   kEpiGelu  : act[m][n] = gelu_tanh(Y[m][n])
+//   kEpiSwiglu: act[m][c] = silu(Y[m][gate c]) * Y[m][up c]
+//   kEpiResid : h[m][n] += Y; u[m][n] = h[m][n] * gain[n];
+//               ss_out[group * Mtot + m] = sum over the group's columns of h^2
+//   kEpiQkv   : rotate q, k (packed rope pairs), write q and append k, v to
+//               the KV cache at the row's position
+struct GemmParams {
+  const void* X; int ldx; size_t xplane;
+  int M, m0, Mtot;
+  const void* W; int NT, KT, n_valid;
+  const float* ss_in; int ng_in; float inv_d, eps;
+  float* out; int ldo;
   void* act; int lda; size_t aplane;
+  float* h; const float* gain; void* u; int ldu; size_t uplane; float* ss_out;
+  const int32_t* lengths; int pos_offset, Mps, H, DH; float rope_base; int T_cap;
+  void* q; void* kc; void* vc; int* err;
   int epi;
 };
-hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t st);
-int gemm_max_rows(int dtype);   // rows one launch handles (larger M: several launches)
-int gemm_splits(int dtype, int NT, int KT, int M, int epi);
+hipError_t launch_gemm(int dtype, const GemmParams& p, hipStream_t st);
+int gemm_max_rows(int dtype);                 // rows one launch handles
+int gemm_groups(int dtype, int NT, int Mtot); // column groups (work-groups) of a GEMM over Mtot rows
 
 // Pack canonical rows src[n][k] (n < n_src, k < Kd) into tile order. Row n goes
 // to packed row map(n): kind 0: row_off + n; kind 1: (n/8)*16 + row_off*8 + n%8
-// (SwiGLU gate: row_off 0, up: row_off 1). Rows [zero_from, zero_to) are
-// cleared.
+// (SwiGLU gate: row_off 0, up: row_off 1); kind 2: rotary pairs of heads of
+// `dh` dims side by side, row_off + head*dh + pi(f) (see gemm.hip). Rows
+// [zero_from, zero_to) are cleared.
 hipError_t launch_pack(int dtype, const void* src, int n_src, int Kd, void* dst, int KT, int kind,
-                       int row_off, int zero_from, int zero_to, hipStream_t st);
+                       int row_off, int dh, int zero_from, int zero_to, hipStream_t st);
 
 // Activations (x, attention output o, FFN hidden) are in the activation
 // format of common.h; `xplane` is the element distance of the lo plane.
-hipError_t launch_embed_norm(int dtype, const int32_t* tokens, int tok_stride, int Mps, int M,
-                             const void* E, int V, int d, const float* gain, float eps, float* h,
-                             void* x, size_t xplane, int* err, hipStream_t st);
-hipError_t launch_add_norm(int dtype, float* h, const float* part, int S, int M, int d,
-                           const float* gain, float eps, void* x, size_t xplane, hipStream_t st);
-hipError_t launch_rope_kv(int dtype, const float* qkvp, int S, int M, int H, int DH, int Mps,
-                          const int32_t* lengths, int pos_offset, float rope_base, void* qout,
-                          void* kc, void* vc, int T_cap, int* err, hipStream_t st);
+// h[m] = E[token]; u[m] = h[m] * gain; ss[m] = sum h[m]^2 (one group).
+hipError_t launch_embed(int dtype, const int32_t* tokens, int tok_stride, int Mps, int M, const void* E,
+                        int V, int d, const float* gain, float* h, void* u, size_t uplane, float* ss,
+                        int* err, hipStream_t st);
 hipError_t launch_attention(int dtype, const void* q, const void* kc, const void* vc,
                             const int32_t* lengths, int pos_offset, int B, int Mps, int H, int DH,
                             int T_cap, float* part, void* o, size_t oplane, hipStream_t st);

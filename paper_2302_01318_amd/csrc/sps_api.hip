@@ -15,11 +15,10 @@ __device__ int sps_dev_err;
 
 namespace {
 
-using sps::GemmArgs;
+using sps::GemmParams;
 
 constexpr int kMaxTokensPerSeq = 64;
 constexpr int kMaxRows = 160;
-constexpr int kMaxSplits = 8;
 constexpr int kMaxK = 63;
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
@@ -75,22 +74,23 @@ Layout make_layout(const sps_config* c) {
 
 // Offsets of the forward's scratch buffers.
 struct WsLayout {
-  size_t h, x, qkvp, qrot, apart, act, resp, logits, stats, total;
+  size_t h, x, o, q, apart, act, ss_a, ss_b, logits, stats, total;
 };
 
 WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
   WsLayout w{};
   const size_t M = static_cast<size_t>(B) * Mps;
-  const size_t es = L.es;
   const size_t NP = sps::attn_partials(T_cap);
+  const size_t ng = (L.d + 15) / 16;   // column groups a residual GEMM can produce
   size_t o = 0;
-  w.h = o; o = align256(o + M * L.d * 4);
-  w.x = o; o = align256(o + M * std::max(L.d, L.HD) * 4);
-  w.qkvp = o; o = align256(o + kMaxSplits * M * 3 * L.HD * 4);
-  w.qrot = o; o = align256(o + M * L.HD * es);
+  w.h = o; o = align256(o + M * L.d * 4);                 // residual stream (fp32)
+  w.x = o; o = align256(o + M * L.d * 4);                 // u = h * gain (activation format)
+  w.o = o; o = align256(o + M * L.HD * 4);                // attention output (activation format)
+  w.q = o; o = align256(o + M * L.HD * L.es);             // rotated queries (model dtype)
   w.apart = o; o = align256(o + static_cast<size_t>(B) * L.H * NP * Mps * (L.DH + 2) * 4);
-  w.act = o; o = align256(o + M * L.F * 4);
-  w.resp = o; o = align256(o + kMaxSplits * M * L.d * 4);
+  w.act = o; o = align256(o + M * L.F * 4);               // FFN hidden (activation format)
+  w.ss_a = o; o = align256(o + ng * M * 4);               // per-group sums of squares of h
+  w.ss_b = o; o = align256(o + ng * M * 4);
   w.logits = o; o = align256(o + M * L.V * 4);
   w.stats = o; o = align256(o + M * 2 * 4);
   w.total = o;
@@ -153,23 +153,13 @@ struct GemmProfile {
 };
 GemmProfile g_prof;
 
-// Y = X W^T over M rows (several launches when M exceeds one launch's rows).
-// X / act in the activation format with lo planes xplane / aplane elements
-// away; split s of a kEpiStore output at out + s * M * ldo.
-sps_status gemm(int dtype, const void* X, int ldx, size_t xplane, int M, const void* W, int N, int KT, int n_valid,
-                int epi, float* out, int ldo, void* act, int lda, size_t aplane, int S, hipStream_t st) {
+// Y = X W^T over p.Mtot rows (several launches when they exceed one launch's
+// rows). Fields M and m0 of p are set per launch.
+sps_status gemm(int dtype, GemmParams p, hipStream_t st) {
   const int cap = sps::gemm_max_rows(dtype);
-  const size_t es = dtype == 1 ? 2 : 4;   // activation element size
-  for (int m0 = 0; m0 < M; m0 += cap) {
-    const int mc = std::min(cap, M - m0);
-    GemmArgs a{};
-    a.X = static_cast<const char*>(X) + static_cast<size_t>(m0) * ldx * es;
-    a.ldx = ldx; a.xplane = xplane; a.M = mc;
-    a.W = W; a.N = N; a.KT = KT; a.n_valid = n_valid; a.S = S;
-    a.out = out ? out + static_cast<size_t>(m0) * ldo : nullptr;
-    a.ldo = ldo; a.oplane = static_cast<size_t>(M) * ldo;
-    a.act = act ? static_cast<char*>(act) + static_cast<size_t>(m0) * lda * es : nullptr;
-    a.lda = lda; a.aplane = aplane; a.epi = epi;
+  for (int m0 = 0; m0 < p.Mtot; m0 += cap) {
+    p.m0 = m0;
+    p.M = std::min(cap, p.Mtot - m0);
     hipEvent_t e0 = nullptr, e1 = nullptr;
     if (g_prof.on) {
       if (g_prof.used + 2 > g_prof.ev.size()) {
@@ -183,73 +173,101 @@ sps_status gemm(int dtype, const void* X, int ldx, size_t xplane, int M, const v
       e1 = g_prof.ev[g_prof.used + 1];
       g_prof.used += 2;
       const double wes = dtype == 1 ? 2.0 : 4.0;
-      const double rows_w = epi == sps::kEpiSwiglu ? 2.0 * n_valid : static_cast<double>(n_valid);
-      g_prof.bytes.push_back(rows_w * KT * 32 * wes + 4.0 * mc * KT * 32 + 4.0 * mc * n_valid);
+      const double rows_w = p.epi == sps::kEpiSwiglu ? 2.0 * p.n_valid : static_cast<double>(p.n_valid);
+      g_prof.bytes.push_back(rows_w * p.KT * 32 * wes + 4.0 * p.M * p.KT * 32 + 4.0 * p.M * p.n_valid);
       SPS_HIP(hipEventRecord(e0, st));
     }
     const int reps = g_prof.on ? g_prof.repeats : 1;   // repeated launches recompute identical outputs
-    for (int r = 0; r < reps; ++r) SPS_HIP(sps::launch_gemm(dtype, a, st));
+    for (int r = 0; r < reps; ++r) SPS_HIP(sps::launch_gemm(dtype, p, st));
     if (e1) SPS_HIP(hipEventRecord(e1, st));
   }
   return SPS_OK;
 }
 
-int splits(int dtype, int N, int KT, int M, int epi) {
-  return sps::gemm_splits(dtype, N / 16, KT, std::min(M, sps::gemm_max_rows(dtype)), epi);
-}
-
 // The decoder forward (Conditional Scoring section) over Mps new tokens per
-// sequence at positions lengths[b] + pos_offset + j.
+// sequence at positions lengths[b] + pos_offset + j. Per layer: QKV GEMM
+// (input RMSNorm scale, rotary encoding, KV append), attention, W_O GEMM
+// (residual add, next norm's input), W_1 GEMM (norm scale, GELU / SwiGLU),
+// W_2 GEMM (residual add, next norm's input).
 sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t* tokens, int tok_stride, int B,
                         int Mps, int pos_offset, float* logits, char* ws_base, const WsLayout& ws, int* err,
                         hipStream_t st) {
   const Layout& L = m->L;
   const int dt = m->cfg.dtype;
   const int M = B * Mps;
-  const float eps = m->cfg.rms_eps;
   float* h = reinterpret_cast<float*>(ws_base + ws.h);
   void* x = ws_base + ws.x;
-  float* qkvp = reinterpret_cast<float*>(ws_base + ws.qkvp);
-  void* qrot = ws_base + ws.qrot;
+  void* o = ws_base + ws.o;
+  void* q = ws_base + ws.q;
   float* apart = reinterpret_cast<float*>(ws_base + ws.apart);
   void* act = ws_base + ws.act;
-  float* resp = reinterpret_cast<float*>(ws_base + ws.resp);
+  float* ss_cur = reinterpret_cast<float*>(ws_base + ws.ss_a);
+  float* ss_nxt = reinterpret_cast<float*>(ws_base + ws.ss_b);
+  const size_t uplane = static_cast<size_t>(M) * L.d;    // lo planes of the activation format
+  const size_t oplane = static_cast<size_t>(M) * L.HD;
+  const size_t aplane = static_cast<size_t>(M) * L.F;
   const int KTd = L.d / 32, KThd = L.HD / 32, KTf = L.F / 32;
+  const float inv_d = 1.0f / static_cast<float>(L.d);
 
-  const size_t xplane = static_cast<size_t>(M) * std::max(L.d, L.HD);   // lo plane of x / o (bf16)
-  const size_t aplane = static_cast<size_t>(M) * L.F;                    // lo plane of the FFN hidden
-  SPS_HIP(sps::launch_embed_norm(dt, tokens, tok_stride, Mps, M, m->base + L.embed, L.V, L.d,
-                                 reinterpret_cast<const float*>(layer_ptr(m, 0, L.l_attn_norm)), eps, h, x, xplane,
-                                 err, st));
+  GemmParams base{};
+  base.Mtot = M;
+  base.inv_d = inv_d;
+  base.eps = m->cfg.rms_eps;
+
+  SPS_HIP(sps::launch_embed(dt, tokens, tok_stride, Mps, M, m->base + L.embed, L.V, L.d,
+                            reinterpret_cast<const float*>(layer_ptr(m, 0, L.l_attn_norm)), h, x, uplane, ss_cur,
+                            err, st));
+  int ng = 1;
   for (int l = 0; l < L.L; ++l) {
-    const int S_qkv = splits(dt, 3 * L.HD, KTd, M, sps::kEpiStore);
-    sps_status s = gemm(dt, x, L.d, xplane, M, layer_ptr(m, l, L.l_qkv), 3 * L.HD, KTd, 3 * L.HD, sps::kEpiStore,
-                        qkvp, 3 * L.HD, nullptr, 0, 0, S_qkv, st);
+    GemmParams p = base;                     // QKV: norm scale, rotary encoding, KV append
+    p.X = x; p.ldx = L.d; p.xplane = uplane;
+    p.W = layer_ptr(m, l, L.l_qkv); p.NT = 3 * L.HD / 16; p.KT = KTd; p.n_valid = 3 * L.HD;
+    p.ss_in = ss_cur; p.ng_in = ng;
+    p.lengths = kv->lengths; p.pos_offset = pos_offset; p.Mps = Mps; p.H = L.H; p.DH = L.DH;
+    p.rope_base = m->cfg.rope_base; p.T_cap = kv->T_cap; p.q = q; p.kc = kv_k(kv, l); p.vc = kv_v(kv, l);
+    p.err = err; p.epi = sps::kEpiQkv;
+    sps_status s = gemm(dt, p, st);
     if (s != SPS_OK) return s;
-    SPS_HIP(sps::launch_rope_kv(dt, qkvp, S_qkv, M, L.H, L.DH, Mps, kv->lengths, pos_offset, m->cfg.rope_base,
-                                qrot, kv_k(kv, l), kv_v(kv, l), kv->T_cap, err, st));
-    SPS_HIP(sps::launch_attention(dt, qrot, kv_k(kv, l), kv_v(kv, l), kv->lengths, pos_offset, B, Mps, L.H, L.DH,
-                                  kv->T_cap, apart, x, xplane, st));
-    const int S_o = splits(dt, L.d, KThd, M, sps::kEpiStore);
-    s = gemm(dt, x, L.HD, xplane, M, layer_ptr(m, l, L.l_o), L.d, KThd, L.d, sps::kEpiStore, resp, L.d, nullptr, 0,
-             0, S_o, st);
+
+    SPS_HIP(sps::launch_attention(dt, q, kv_k(kv, l), kv_v(kv, l), kv->lengths, pos_offset, B, Mps, L.H, L.DH,
+                                  kv->T_cap, apart, o, oplane, st));
+
+    p = base;                                // W_O: residual add, input of the FFN norm
+    p.X = o; p.ldx = L.HD; p.xplane = oplane;
+    p.W = layer_ptr(m, l, L.l_o); p.NT = L.d / 16; p.KT = KThd; p.n_valid = L.d;
+    p.h = h; p.gain = reinterpret_cast<const float*>(layer_ptr(m, l, L.l_ffn_norm));
+    p.u = x; p.ldu = L.d; p.uplane = uplane; p.ss_out = ss_nxt; p.epi = sps::kEpiResid;
+    s = gemm(dt, p, st);
     if (s != SPS_OK) return s;
-    SPS_HIP(sps::launch_add_norm(dt, h, resp, S_o, M, L.d,
-                                 reinterpret_cast<const float*>(layer_ptr(m, l, L.l_ffn_norm)), eps, x, xplane, st));
-    s = gemm(dt, x, L.d, xplane, M, layer_ptr(m, l, L.l_w1), L.N1, KTd, L.F,
-             L.swiglu ? sps::kEpiSwiglu : sps::kEpiGelu, nullptr, 0, act, L.F, aplane, 1, st);
+    const int ng_o = sps::gemm_groups(dt, L.d / 16, M);
+
+    p = base;                                // W_1: norm scale, GELU / SwiGLU
+    p.X = x; p.ldx = L.d; p.xplane = uplane;
+    p.W = layer_ptr(m, l, L.l_w1); p.NT = L.N1 / 16; p.KT = KTd; p.n_valid = L.F;
+    p.ss_in = ss_nxt; p.ng_in = ng_o;
+    p.act = act; p.lda = L.F; p.aplane = aplane;
+    p.epi = L.swiglu ? sps::kEpiSwiglu : sps::kEpiGelu;
+    s = gemm(dt, p, st);
     if (s != SPS_OK) return s;
-    const int S_2 = splits(dt, L.d, KTf, M, sps::kEpiStore);
-    s = gemm(dt, act, L.F, aplane, M, layer_ptr(m, l, L.l_w2), L.d, KTf, L.d, sps::kEpiStore, resp, L.d, nullptr, 0,
-             0, S_2, st);
+
+    p = base;                                // W_2: residual add, input of the next norm
+    p.X = act; p.ldx = L.F; p.xplane = aplane;
+    p.W = layer_ptr(m, l, L.l_w2); p.NT = L.d / 16; p.KT = KTf; p.n_valid = L.d;
+    p.h = h;
+    p.gain = l + 1 < L.L ? reinterpret_cast<const float*>(layer_ptr(m, l + 1, L.l_attn_norm))
+                         : reinterpret_cast<const float*>(m->base + L.final_norm);
+    p.u = x; p.ldu = L.d; p.uplane = uplane; p.ss_out = ss_cur; p.epi = sps::kEpiResid;
+    s = gemm(dt, p, st);
     if (s != SPS_OK) return s;
-    const float* next_gain = l + 1 < L.L ? reinterpret_cast<const float*>(layer_ptr(m, l + 1, L.l_attn_norm))
-                                         : reinterpret_cast<const float*>(m->base + L.final_norm);
-    SPS_HIP(sps::launch_add_norm(dt, h, resp, S_2, M, L.d, next_gain, eps, x, xplane, st));
+    ng = sps::gemm_groups(dt, L.d / 16, M);
   }
   if (logits) {
-    sps_status s = gemm(dt, x, L.d, xplane, M, m->base + L.unembed, L.NU, KTd, L.V, sps::kEpiStore, logits, L.V,
-                        nullptr, 0, 0, 1, st);
+    GemmParams p = base;                     // final norm scale + unembedding
+    p.X = x; p.ldx = L.d; p.xplane = uplane;
+    p.W = m->base + L.unembed; p.NT = L.NU / 16; p.KT = KTd; p.n_valid = L.V;
+    p.ss_in = ss_cur; p.ng_in = ng;
+    p.out = logits; p.ldo = L.V; p.epi = sps::kEpiStore;
+    sps_status s = gemm(dt, p, st);
     if (s != SPS_OK) return s;
   }
   return SPS_OK;
@@ -318,24 +336,27 @@ sps_status sps_pack_weight(const sps_config* cfg, int32_t tensor, int32_t layer,
       SPS_HIP(hipMemcpyAsync(lp + L.l_ffn_norm, src, static_cast<size_t>(L.d) * 4, hipMemcpyDeviceToDevice, st));
       return SPS_OK;
     case SPS_W_UNEMBED:
-      SPS_HIP(sps::launch_pack(dt, src, L.V, L.d, base + L.unembed, L.d / 32, 0, 0, L.V, L.NU, st));
+      SPS_HIP(sps::launch_pack(dt, src, L.V, L.d, base + L.unembed, L.d / 32, 0, 0, 0, L.V, L.NU, st));
       return SPS_OK;
-    case SPS_W_Q:
+    case SPS_W_Q:   // rotary partners side by side (kind 2)
     case SPS_W_K:
+      SPS_HIP(sps::launch_pack(dt, src, L.HD, L.d, lp + L.l_qkv, L.d / 32, 2, (tensor - SPS_W_Q) * L.HD, L.DH, 0,
+                               0, st));
+      return SPS_OK;
     case SPS_W_V:
-      SPS_HIP(sps::launch_pack(dt, src, L.HD, L.d, lp + L.l_qkv, L.d / 32, 0, (tensor - SPS_W_Q) * L.HD, 0, 0, st));
+      SPS_HIP(sps::launch_pack(dt, src, L.HD, L.d, lp + L.l_qkv, L.d / 32, 0, 2 * L.HD, 0, 0, 0, st));
       return SPS_OK;
     case SPS_W_O:
-      SPS_HIP(sps::launch_pack(dt, src, L.d, L.HD, lp + L.l_o, L.HD / 32, 0, 0, 0, 0, st));
+      SPS_HIP(sps::launch_pack(dt, src, L.d, L.HD, lp + L.l_o, L.HD / 32, 0, 0, 0, 0, 0, st));
       return SPS_OK;
     case SPS_W_1:
-      SPS_HIP(sps::launch_pack(dt, src, L.F, L.d, lp + L.l_w1, L.d / 32, L.swiglu ? 1 : 0, 0, 0, 0, st));
+      SPS_HIP(sps::launch_pack(dt, src, L.F, L.d, lp + L.l_w1, L.d / 32, L.swiglu ? 1 : 0, 0, 0, 0, 0, st));
       return SPS_OK;
     case SPS_W_3:
-      SPS_HIP(sps::launch_pack(dt, src, L.F, L.d, lp + L.l_w1, L.d / 32, 1, 1, 0, 0, st));
+      SPS_HIP(sps::launch_pack(dt, src, L.F, L.d, lp + L.l_w1, L.d / 32, 1, 1, 0, 0, 0, st));
       return SPS_OK;
     case SPS_W_2:
-      SPS_HIP(sps::launch_pack(dt, src, L.d, L.F, lp + L.l_w2, L.F / 32, 0, 0, 0, 0, st));
+      SPS_HIP(sps::launch_pack(dt, src, L.d, L.F, lp + L.l_w2, L.F / 32, 0, 0, 0, 0, 0, st));
       return SPS_OK;
     default:
       return SPS_E_INVALID;
