@@ -122,6 +122,123 @@ def cpu_baseline(shape, K, ctx):
                       "K+1=%d positions, B=1, ctx %d (%.2f GB algorithmic)" % (K + 1, ctx, nbytes / 1e9)}
 
 
+def timed(fn, steps, warmup):
+    import torch
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        fn(i)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def sweep(args):
+    """The 70B-shaped verify step over K in {1,2,3,4,6,8}, B in {1,4,16}, KV
+    context in {2048, 8192}, plus the accept stage on synthetic draft/target
+    pairs with perturbation sigma in {0.1, 0.5, 1.0} and the SpS tokens/s those
+    acceptance rates imply with the measured draft and verify times."""
+    import torch
+    from paper_2302_01318_amd import configs, sps, synth
+    shape, dshape = configs.SEVENTY_B, configs.DRAFT_70B
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+    target = device_model(sps, synth, shape, args.seed)
+    rows = []
+    verify_ms = {}
+    for ctx in configs.SWEEP["ctx"]:
+        for B in configs.SWEEP["B"]:
+            T_cap = round_up(ctx + max(configs.SWEEP["K"]) + 1, 32)
+            need = sps.lib.sps_kv_bytes(__import__("ctypes").byref(sps.config_of(shape)), B, T_cap)
+            free = torch.cuda.mem_get_info()[0]
+            if need + (4 << 30) > free:
+                for K in configs.SWEEP["K"]:
+                    rows.append({"ctx": ctx, "B": B, "K": K, "status": "OOM",
+                                 "kv_gb": round(need / 1e9, 1), "free_gb": round(free / 1e9, 1)})
+                log("ctx %d B %d: KV %.1f GB does not fit (%.1f GB free)" % (ctx, B, need / 1e9, free / 1e9))
+                continue
+            kv = sps.KVCache(shape, B, T_cap)
+            kv.buf.view(torch.bfloat16).normal_()
+            kv.lengths.fill_(ctx)
+            for K in configs.SWEEP["K"]:
+                p, _, drafts = synth.accept_case_device(args.seed + K, B, K, shape.vocab)
+                first = torch.randint(0, shape.vocab, (B, 1), device="cuda", dtype=torch.int32)
+                tokens = torch.cat([first, drafts], dim=1).contiguous()
+                ws = sps.workspace(shape, B, K + 1, T_cap)
+                out = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+                nacc = torch.empty(B, dtype=torch.int32, device="cuda")
+                ms = timed(lambda i: sps.verify_step(target, kv, tokens, K, 1.0, ws, p_draft=p, rng=(args.seed, i),
+                                                     out_tokens=out, n_accepted=nacc), 5, 2)
+                nbytes = verify_bytes(shape, B, K, ctx)
+                rows.append({"ctx": ctx, "B": B, "K": K, "status": "ok", "ms": round(ms, 3),
+                             "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                             "frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                             "tokens_scored_per_s": round(B * (K + 1) / (ms * 1e-3), 1)})
+                verify_ms[(ctx, B, K)] = ms
+                log("ctx %5d B %2d K %d: %.3f ms, %.0f GB/s" % (ctx, B, K, ms, rows[-1]["gbs"]))
+                del ws, p, tokens
+            del kv
+            torch.cuda.empty_cache()
+    # draft time per token (B = 1, ctx 2048)
+    draft = device_model(sps, synth, dshape, args.seed + 10)
+    T_cap = round_up(2048 + 16, 32)
+    kvd = sps.KVCache(dshape, 1, T_cap)
+    kvd.buf.view(torch.bfloat16).normal_()
+    kvd.lengths.fill_(2048)
+    wsd = sps.workspace(dshape, 1, 2, T_cap)
+    ctx_tok = torch.randint(0, shape.vocab, (1, 2), device="cuda", dtype=torch.int32)
+    draft_ms = {}
+    for K in configs.SWEEP["K"]:
+        toks = torch.empty((1, K + 1), dtype=torch.int32, device="cuda")
+        pbuf = torch.empty((1, K, shape.vocab), device="cuda")
+        draft_ms[K] = timed(lambda i: sps.draft_step(draft, kvd, ctx_tok, K, 1.0, (args.seed, i), toks, pbuf, wsd),
+                            5, 2)
+        log("draft step K %d: %.3f ms" % (K, draft_ms[K]))
+    # accept stage acceptance for sigma_pert, and the implied SpS tokens/s at B = 1, ctx 2048
+    proj = []
+    for sig in configs.SWEEP["sigma_pert"]:
+        for K in configs.SWEEP["K"]:
+            Bs = 256
+            p, q, drafts = synth.accept_case_device(args.seed + 100 + K, Bs, K, shape.vocab, 2.0, sig)
+            _, nacc = sps.accept_resample(p, q, drafts, None, (args.seed, 7))
+            a = float(nacc.float().mean().item())
+            t_loop = draft_ms[K] + verify_ms[(2048, 1, K)]
+            proj.append({"sigma_pert": sig, "K": K, "mean_accepted": round(a, 3),
+                         "tokens_per_loop": round(a + 1, 3), "loop_ms": round(t_loop, 3),
+                         "sps_tokens_per_s": round((a + 1) / (t_loop * 1e-3), 1)})
+    return {"verify": rows, "draft_ms": {str(k): round(v, 3) for k, v in draft_ms.items()}, "projection": proj,
+            "note": "SpS tokens/s projected from measured draft-step and verify-step times and the acceptance "
+                    "the GPU accept kernel measures on synthetic pairs (z_q ~ N(0,4), z_p = z_q + N(0, sigma^2))"}
+
+
+def accept_grid(args):
+    """Accept/resample alone: V 32000, K in {1,2,4,8}, B in {1,8,64}, Philox
+    uniforms drawn in the kernel; inputs resident in HBM."""
+    import torch
+    from paper_2302_01318_amd import configs, sps, synth
+    g = configs.ACCEPT_GRID
+    rows = []
+    for K in g["K"]:
+        for B in g["B"]:
+            p, q, drafts = synth.accept_case_device(args.seed + K * 100 + B, B, K, g["V"], g["sigma"],
+                                                     g["sigma_pert"])
+            out = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+            nacc = torch.empty(B, dtype=torch.int32, device="cuda")
+            ms = timed(lambda i: sps.accept_resample(p, q, drafts, None, (args.seed, i), out, nacc), 50, 5)
+            naive = B * (2 * K + 1) * g["V"] * 4
+            needed = B * (2 * g["V"] * 4 + 2 * K * 4 + (K + 1) * 4 + 4)
+            rows.append({"B": B, "K": K, "us": round(ms * 1e3, 2),
+                         "gbs_needed_bytes": round(needed / (ms * 1e-3) / 1e9, 1),
+                         "naive_bytes": naive, "needed_bytes": needed,
+                         "mean_accepted": round(float(nacc.float().mean().item()), 3)})
+            print("B %2d K %d: %.2f us" % (B, K, ms * 1e3), file=sys.stderr, flush=True)
+    return {"accept": rows,
+            "note": "needed bytes: one target row and one draft row of V fp32 per sequence (the residual or "
+                    "bonus draw) plus the 2K gathered probabilities; naive: every p and q row"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -135,6 +252,8 @@ def main():
     ap.add_argument("--no-e2e", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--sweep", action="store_true", help="70B verify over K, B, ctx (+ accept-stage projection)")
+    ap.add_argument("--accept-grid", action="store_true", help="accept/resample alone over the B x K grid")
     ap.add_argument("--no-roofline-pass", action="store_true",
                     help="skip the second pass that times every GEMM launch with events")
     args = ap.parse_args()
@@ -142,6 +261,11 @@ def main():
         print("bench.py measures the verify step on one GPU; this build has no multi-GPU path "
               "(requested --gpus %d)" % args.gpus, file=sys.stderr)
         sys.exit(2)
+
+    if args.sweep or args.accept_grid:
+        res = sweep(args) if args.sweep else accept_grid(args)
+        print(json.dumps(res), flush=True)
+        return
 
     import torch
     from paper_2302_01318_amd import configs, sps, synth
@@ -216,7 +340,7 @@ def main():
 
     # ---- SpS and ArS tokens/s end to end ---------------------------------------------
     e2e = {}
-    if not args.no_e2e:
+    if not args.no_e2e and args.shape == "70b":
         t0 = time.time()
         draft = device_model(sps, synth, dshape, args.seed + 10)
         torch.cuda.synchronize()

@@ -134,7 +134,11 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
   __shared__ float red[WAVES][NTW][MT][4][64];
   __shared__ float tot[NTW][MT][4][64];
   __shared__ float s_rs[kMaxRows];
-  __shared__ float s_sq[EPI == kEpiResid ? kMaxRows : 1][NTW * 16 + 1];
+  // Squares of the residual outputs reuse the wave-partial buffer, which is
+  // dead once `tot` holds the sums.
+  constexpr int kSqLd = NTW * 16 + 1;
+  static_assert(kMaxRows * kSqLd <= WAVES * NTW * MT * 256, "square buffer must fit the partial buffer");
+  float (*s_sq)[kSqLd] = reinterpret_cast<float (*)[kSqLd]>(&red[0][0][0][0][0]);
 #pragma unroll
   for (int j = 0; j < NTW; ++j)
 #pragma unroll
@@ -238,8 +242,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
   if (EPI == kEpiResid) {
     // Sums of squares of this group's columns, per row, in a fixed order.
     __syncthreads();
-    if (static_cast<int>(threadIdx.x) < M) {
-      const int m = threadIdx.x;
+    for (int m = threadIdx.x; m < M; m += WAVES * 64) {
       float s = 0.f;
       for (int c = 0; c < NTW * 16; ++c) s += s_sq[m][c];
       p.ss_out[static_cast<size_t>(blockIdx.x) * p.Mtot + p.m0 + m] = s;
@@ -283,11 +286,18 @@ static hipError_t gemm_dispatch(const GemmParams& p, hipStream_t st) {
     case 6: return gemm_launch<T, 6, 1, 4, 4>(p, st);
     case 7:
     case 8: return gemm_launch<T, 8, 1, 4, 4>(p, st);
-    default: return gemm_launch<T, 10, 1, 4, 2>(p, st);
+    case 9:
+    case 10: return gemm_launch<T, 10, 1, 4, 2>(p, st);
+    case 11:
+    case 12:
+    case 13:
+    case 14: return gemm_launch<T, 14, 1, 2, 2>(p, st);
+    default: return gemm_launch<T, 20, 1, 2, 1>(p, st);
   }
 }
 
-int gemm_max_rows(int dtype) { return 10 * (dtype == 1 ? ActRows<bf16>::kRows : ActRows<float>::kRows); }
+// One launch covers up to 160 rows (20 M tiles of 8 bf16 rows, 10 of 16 fp32).
+int gemm_max_rows(int dtype) { return dtype == 1 ? 20 * ActRows<bf16>::kRows : 10 * ActRows<float>::kRows; }
 
 int gemm_groups(int dtype, int NT, int Mtot) {
   const int rows = dtype == 1 ? ActRows<bf16>::kRows : ActRows<float>::kRows;

@@ -90,6 +90,14 @@ def test_small_bf16_many_rows(sps):
     verify_parity(sps, SMALL.with_(ffn="swiglu"), 4, 8, [64, 1, 130, 33], 4, 2e-2)
 
 
+@pytest.mark.parametrize("B,K", [(12, 8), (16, 8)])
+def test_small_bf16_large_batch(sps, B, K):
+    # 108 and 144 rows: the widest single GEMM launches (14 and 20 M tiles)
+    g = np.random.default_rng(B)
+    verify_parity(sps, SMALL.with_(ffn="gelu"), B, K, [int(x) for x in g.integers(0, 200, B)], 40 + B, 2e-2,
+                  check_kv=False)
+
+
 def test_small_fp32_greedy(sps):
     verify_parity(sps, SMALL.with_(dtype="f32"), 2, 4, [20, 77], 5, 1e-4, T=0.0)
 
