@@ -37,26 +37,10 @@
 //    side in one 16-row tile) and the KV-cache append;
 //  * FFN: GELU or SwiGLU.
 #include "common.h"
+#include "gemm_epi.h"
 #include "launch.h"
 
 namespace sps {
-
-__device__ __forceinline__ float gelu_tanh(float x) {
-  const float k0 = 0.7978845608028654f, k1 = 0.044715f;
-  return 0.5f * x * (1.0f + tanhf(k0 * (x + k1 * x * x * x)));
-}
-__device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
-
-template <typename T> struct ActRows;
-template <> struct ActRows<bf16> { static constexpr int kRows = 8; };
-template <> struct ActRows<float> { static constexpr int kRows = 16; };
-
-// Packed position of dim f of a head in a QKV tile: the rotate-half partners
-// f and f + DH/2 sit in rows r and r + 8 of the same 16-row tile.
-__host__ __device__ __forceinline__ int rope_pack_index(int f, int DH) {
-  const int half = DH / 2;
-  return f < half ? (f / 8) * 16 + f % 8 : ((f - half) / 8) * 16 + 8 + (f - half) % 8;
-}
 
 template <typename T, int MT, int NTW, int WAVES, int U, int EPI>
 __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
@@ -145,15 +129,9 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) red[wave][j][mt][r][lane] = acc[j][mt][r];
-  // Row scales of the input RMSNorm: rs[m] = 1 / sqrt(sum_g ss_in[g][m] / d + eps).
+  // Row scales of the input RMSNorm.
   for (int m = wave; m < kMaxRows; m += WAVES) {
-    float v = 1.f;
-    if (p.ss_in && m < M) {
-      float s = 0.f;
-      for (int g = lane; g < p.ng_in; g += 64) s += p.ss_in[static_cast<size_t>(g) * p.Mtot + p.m0 + m];
-      s = wave_sum(s);
-      v = 1.0f / sqrtf(s * p.inv_d + p.eps);
-    }
+    const float v = norm_scale(p, m, lane);
     if (lane == 0) s_rs[m] = v;
   }
   __syncthreads();
@@ -183,61 +161,9 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
     const int gm = p.m0 + m;
     const float rs = s_rs[m];
     const float v = out_value(j, mt, r, ln) * rs;
-    if (EPI == kEpiStore) {
-      const int n = nt * 16 + col;
-      if (n < p.n_valid) p.out[static_cast<size_t>(gm) * p.ldo + n] = v;
-    } else if (EPI == kEpiGelu) {
-      const int n = nt * 16 + col;
-      if (n < p.n_valid) store_act(static_cast<T*>(p.act), p.aplane, static_cast<size_t>(gm) * p.lda + n, gelu_tanh(v));
-    } else if (EPI == kEpiSwiglu) {  // packed rows 0..7 gate columns, 8..15 the matching up columns
-      if (col < 8) {
-        const int c = nt * 8 + col;
-        const float up = out_value(j, mt, r, ln + 8) * rs;
-        if (c < p.n_valid) store_act(static_cast<T*>(p.act), p.aplane, static_cast<size_t>(gm) * p.lda + c, silu(v) * up);
-      }
-    } else if (EPI == kEpiResid) {
-      const int n = nt * 16 + col;
-      if (n < p.n_valid) {
-        float* hp = p.h + static_cast<size_t>(gm) * p.n_valid + n;
-        const float hn = *hp + v;
-        *hp = hn;
-        store_act(static_cast<T*>(p.u), p.uplane, static_cast<size_t>(gm) * p.ldu + n, hn * p.gain[n]);
-        s_sq[m][j * 16 + col] = hn * hn;
-      }
-    } else {  // kEpiQkv
-      const int n = nt * 16 + col;
-      const int HD = p.H * p.DH;
-      const int b = gm / p.Mps, jr = gm % p.Mps;
-      const int pos = p.lengths[b] + p.pos_offset + jr;
-      const bool ok = pos >= 0 && pos < p.T_cap;
-      if (!ok && n == 0) atomicOr(p.err, kErrCapacity);
-      if (n < 2 * HD) {                        // q or k: rotate the pair held by columns col, col + 8
-        if (col < 8) {
-          const int hh = (n % HD) / p.DH, pi = n % p.DH;
-          const int f = (pi / 16) * 8 + col;
-          const float x1 = v, x2 = out_value(j, mt, r, ln + 8) * rs;
-          const double inv = exp2(-2.0 * f / p.DH * log2(static_cast<double>(p.rope_base)));
-          double sn, cs;
-          sincos(static_cast<double>(pos) * inv, &sn, &cs);
-          const float c = static_cast<float>(cs), s = static_cast<float>(sn);
-          const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
-          const int half = p.DH / 2;
-          if (n < HD) {
-            T* q = static_cast<T*>(p.q) + static_cast<size_t>(gm) * HD + hh * p.DH;
-            q[f] = from_f32<T>(y1);
-            q[f + half] = from_f32<T>(y2);
-          } else if (ok) {
-            T* kr = static_cast<T*>(p.kc) + (static_cast<size_t>(b) * p.H + hh) * p.T_cap * p.DH;
-            kr[k_offset(pos, f, p.DH)] = from_f32<T>(y1);
-            kr[k_offset(pos, f + half, p.DH)] = from_f32<T>(y2);
-          }
-        }
-      } else if (ok && n < 3 * HD) {           // v: straight into the cache
-        const int hh = (n - 2 * HD) / p.DH, dd = (n - 2 * HD) % p.DH;
-        T* vr = static_cast<T*>(p.vc) + (static_cast<size_t>(b) * p.H + hh) * p.T_cap * p.DH;
-        vr[v_offset(pos, dd, p.DH)] = from_f32<T>(v);
-      }
-    }
+    const float v2 = (EPI == kEpiSwiglu || EPI == kEpiQkv) && col < 8 ? out_value(j, mt, r, ln + 8) * rs : 0.f;
+    const float sq = epilogue_element<T, EPI>(p, gm, nt, col, v, v2);
+    if (EPI == kEpiResid && nt * 16 + col < p.n_valid) s_sq[m][j * 16 + col] = sq;
   }
   if (EPI == kEpiResid) {
     // Sums of squares of this group's columns, per row, in a fixed order.
@@ -270,43 +196,49 @@ static hipError_t gemm_launch(const GemmParams& p, hipStream_t st) {
 
 static int single_tile_ntw(int NT) { return (NT % 2 == 0 && NT / 2 >= 512) ? 2 : 1; }
 
-template <typename T>
-static hipError_t gemm_dispatch(const GemmParams& p, hipStream_t st) {
-  constexpr bool kB = sizeof(T) == 2;
+// fp32 models (16-row M tiles) at any row count, bf16 models at <= 8 rows.
+// bf16 launches over more rows go to the wide kernel (gemm_wide.hip).
+static hipError_t gemm_dispatch_f32(const GemmParams& p, hipStream_t st) {
+  using T = float;
   const int MT = (p.M + ActRows<T>::kRows - 1) / ActRows<T>::kRows;
   if (MT == 1) {
     if (p.Mtot <= ActRows<T>::kRows && single_tile_ntw(p.NT) == 2) return gemm_launch<T, 1, 2, 8, 4>(p, st);
     return gemm_launch<T, 1, 1, 16, 4>(p, st);
   }
   switch (MT) {
-    case 2: return gemm_launch<T, 2, 1, 8, kB ? 8 : 4>(p, st);
-    case 3: return gemm_launch<T, 3, 1, 4, kB ? 8 : 4>(p, st);
-    case 4: return gemm_launch<T, 4, 1, 4, kB ? 8 : 4>(p, st);
+    case 2: return gemm_launch<T, 2, 1, 8, 4>(p, st);
+    case 3: return gemm_launch<T, 3, 1, 4, 4>(p, st);
+    case 4: return gemm_launch<T, 4, 1, 4, 4>(p, st);
     case 5:
     case 6: return gemm_launch<T, 6, 1, 4, 4>(p, st);
     case 7:
     case 8: return gemm_launch<T, 8, 1, 4, 4>(p, st);
-    case 9:
-    case 10: return gemm_launch<T, 10, 1, 4, 2>(p, st);
-    case 11:
-    case 12:
-    case 13:
-    case 14: return gemm_launch<T, 14, 1, 2, 2>(p, st);
-    default: return gemm_launch<T, 20, 1, 2, 1>(p, st);
+    default: return gemm_launch<T, 10, 1, 4, 2>(p, st);
   }
+}
+
+static hipError_t gemm_dispatch_bf16(const GemmParams& p, hipStream_t st) {
+  using T = bf16;
+  if (gemm_is_wide(1, p.Mtot)) return launch_gemm_wide(p, wide_plan(p.NT, p.KT, p.M), st);
+  if (p.M > ActRows<T>::kRows) return hipErrorInvalidValue;
+  if (single_tile_ntw(p.NT) == 2) return gemm_launch<T, 1, 2, 8, 4>(p, st);
+  return gemm_launch<T, 1, 1, 16, 4>(p, st);
 }
 
 // One launch covers up to 160 rows (20 M tiles of 8 bf16 rows, 10 of 16 fp32).
 int gemm_max_rows(int dtype) { return dtype == 1 ? 20 * ActRows<bf16>::kRows : 10 * ActRows<float>::kRows; }
 
+bool gemm_is_wide(int dtype, int Mtot) { return dtype == 1 && Mtot > ActRows<bf16>::kRows; }
+
 int gemm_groups(int dtype, int NT, int Mtot) {
+  if (gemm_is_wide(dtype, Mtot)) return wide_groups(NT);
   const int rows = dtype == 1 ? ActRows<bf16>::kRows : ActRows<float>::kRows;
   const int ntw = (Mtot <= rows) ? single_tile_ntw(NT) : 1;
   return (NT + ntw - 1) / ntw;
 }
 
 hipError_t launch_gemm(int dtype, const GemmParams& p, hipStream_t st) {
-  return dtype == 1 ? gemm_dispatch<bf16>(p, st) : gemm_dispatch<float>(p, st);
+  return dtype == 1 ? gemm_dispatch_bf16(p, st) : gemm_dispatch_f32(p, st);
 }
 
 // ---------------------------------------------------------------------------

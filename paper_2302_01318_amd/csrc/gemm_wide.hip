@@ -1,0 +1,311 @@
+// Wide skinny GEMM for bf16 models at 9..160 rows (batched verify steps:
+// M = B (K+1) with several sequences). Same packed weights, activation format
+// and epilogues as gemm.hip; what changes is who shares what.
+//
+// The single-tile kernel lets every wave load its own copy of the activation
+// fragments it multiplies. At MT M tiles that is MT activation bytes per
+// weight byte through the vector caches, and above MT = 1 that traffic, not
+// HBM, sets the speed. Here:
+//
+//  * a work-group of 4 waves owns 8 consecutive n-tiles (128 output columns)
+//    and one contiguous range of the k-tiles; wave w multiplies n-tiles
+//    2w and 2w + 1 by all MT M tiles;
+//  * per chunk of KC k-tiles the work-group copies the MT x KC activation
+//    fragments once into LDS with global_load_lds (16 B per lane, each
+//    wave instruction one fragment in register order), so the four waves
+//    share them, and every wave streams its own weight fragments from HBM
+//    into registers;
+//  * where N is too small to give every CU a work-group (the d_model-wide
+//    outputs), the k range is split S ways (split-K): each split writes its
+//    fp32 partial tile to the workspace and a second kernel sums the splits
+//    in split order and runs the epilogue. (A last-arriving-split fixup
+//    inside one kernel would need device-scope fences, which on this GPU
+//    write back and invalidate the L2 and cost more than the launch.)
+#include <algorithm>
+
+#include "common.h"
+#include "gemm_epi.h"
+#include "launch.h"
+
+namespace sps {
+
+constexpr int kWideWaves = 4;                      // waves per work-group
+constexpr int kWideNtw = 2;                        // n-tiles per wave
+constexpr int kWideNg = kWideWaves * kWideNtw;     // n-tiles per work-group (column group)
+
+// Partial tile of one wave: kWideNtw x MT fragments of 32 lanes x 4 floats
+// (the hi rows after folding the lo rows in), in register order.
+template <int MT> constexpr int wide_part_floats() { return kWideNtw * MT * 128; }
+
+// Waves per SIMD the register allocation must allow (the compiler would
+// otherwise hoist every LDS fragment read of a chunk into registers).
+template <int MT> constexpr int wide_waves_per_simd() { return MT <= 6 ? 3 : MT <= 12 ? 2 : 1; }
+
+// Accumulate chunks [c0, c1) of column group g into acc, then fold the
+// lo-plane rows (lanes 32-63) into their hi rows (lanes 0-31).
+template <int MT, int KC>
+__device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0, int c1, bf16x8 (*s_a)[64],
+                                              f32x4 (&acc)[kWideNtw][MT]) {
+  using T = bf16;
+  constexpr int kTile = 512;                       // elements per 16 x 32 tile
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ntw = g * kWideNg + wave * kWideNtw;   // first n-tile of this wave
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int KT = p.KT, M = p.M;
+  const T* W = static_cast<const T*>(p.W);
+
+  const T* wp[kWideNtw];
+  bool wv[kWideNtw];
+#pragma unroll
+  for (int j = 0; j < kWideNtw; ++j) {
+    wv[j] = ntw + j < p.NT;
+    wp[j] = W + static_cast<size_t>(wv[j] ? ntw + j : 0) * KT * kTile + lane * 8;
+  }
+  // This lane's activation row in each M tile: row mt*8 + r16%8 of plane
+  // r16/8. Rows past M read row 0; their outputs are never stored.
+  const int arow = r16 & 7;
+  const T* xbase = static_cast<const T*>(p.X) + (r16 >> 3) * p.xplane + grp * 8;
+
+#pragma unroll
+  for (int j = 0; j < kWideNtw; ++j)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int c = c0; c < c1; ++c) {
+    const int kb = c * KC;
+    // Activation fragments of the chunk into LDS, fragment f = mt * KC + u.
+    for (int f = wave; f < MT * KC; f += kWideWaves) {
+      const int mt = f / KC, u = f % KC;
+      if (kb + u < KT) {
+        const int m = mt * 8 + arow;
+        const T* src = xbase + static_cast<size_t>(p.m0 + (m < M ? m : 0)) * p.ldx + (kb + u) * 32;
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src), reinterpret_cast<void*>(&s_a[f][0]),
+                                         16, 0, 0);
+      }
+    }
+    Frag<T> b[kWideNtw][KC];
+#pragma unroll
+    for (int j = 0; j < kWideNtw; ++j)
+#pragma unroll
+      for (int u = 0; u < KC; ++u)
+        b[j][u] = wv[j] && kb + u < KT ? load_frag_stream(wp[j] + static_cast<size_t>(kb + u) * kTile)
+                                       : Frag<T>::zero();
+    __builtin_amdgcn_s_waitcnt(0);                 // the LDS copies have landed
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < KC; ++u) {
+      if (kb + u < KT) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          Frag<T> a;
+          a.v = s_a[mt * KC + u][lane];
+#pragma unroll
+          for (int j = 0; j < kWideNtw; ++j) acc[j][mt] = mma8(acc[j][mt], a, b[j][u]);
+        }
+      }
+    }
+    __syncthreads();                               // chunk consumed before the next overwrites it
+  }
+#pragma unroll
+  for (int j = 0; j < kWideNtw; ++j)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[j][mt][r] += __shfl_xor(acc[j][mt][r], 32);
+}
+
+// Epilogue of column group g from the folded tile in acc. ep is LDS for the
+// group's output tile [8 n-tiles][MT][8 rows][16 columns], s_rs for MT*8
+// row scales.
+template <int MT, int EPI>
+__device__ __forceinline__ void wide_epilogue(const GemmParams& p, int g, const f32x4 (&acc)[kWideNtw][MT],
+                                              float* ep, float* s_rs) {
+  using T = bf16;
+  constexpr int kMaxRows = MT * 8;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int M = p.M;
+  if (lane < 32) {
+#pragma unroll
+    for (int j = 0; j < kWideNtw; ++j)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          ep[(((wave * kWideNtw + j) * MT + mt) * 8 + (lane >> 4) * 4 + r) * 16 + (lane & 15)] = acc[j][mt][r];
+  }
+  // Row scales of the input RMSNorm.
+  for (int m = wave; m < kMaxRows; m += kWideWaves) {
+    const float v = norm_scale(p, m, lane);
+    if (lane == 0) s_rs[m] = v;
+  }
+  __syncthreads();
+
+  for (int e = threadIdx.x; e < kWideNg * MT * 128; e += kWideWaves * 64) {
+    const int jj = e / (MT * 128), mt = (e >> 7) % MT, i = (e >> 4) & 7, col = e & 15;
+    const int m = mt * 8 + i, nt = g * kWideNg + jj;
+    if (m >= M || nt >= p.NT) {
+      if (EPI == kEpiResid) ep[e] = 0.f;
+      continue;
+    }
+    const float rs = s_rs[m];
+    const float v = ep[e] * rs;
+    const float v2 = (EPI == kEpiSwiglu || EPI == kEpiQkv) && col < 8 ? ep[e + 8] * rs : 0.f;
+    const float sq = epilogue_element<T, EPI>(p, p.m0 + m, nt, col, v, v2);
+    if (EPI == kEpiResid) ep[e] = sq;              // only this thread reads element e here
+  }
+  if (EPI == kEpiResid) {
+    // Sums of squares of the group's 128 columns per row, in a fixed order.
+    __syncthreads();
+    for (int m = threadIdx.x; m < M; m += kWideWaves * 64) {
+      const int mt = m >> 3, i = m & 7;
+      float sum = 0.f;
+      for (int jj = 0; jj < kWideNg; ++jj)
+        for (int c = 0; c < 16; ++c) sum += ep[((jj * MT + mt) * 8 + i) * 16 + c];
+      p.ss_out[static_cast<size_t>(g) * p.Mtot + p.m0 + m] = sum;
+    }
+  }
+}
+
+// One work-group per column group over the whole k range, epilogue fused.
+template <int MT, int KC, int EPI>
+__global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT>())))
+void gemm_wide_kernel(const GemmParams p, int chunks) {
+  __shared__ bf16x8 s_a[MT * KC][64];              // one chunk of activation fragments
+  __shared__ float s_rs[MT * 8];
+  // The epilogue's output tile reuses the chunk buffer, dead after the loop.
+  static_assert(kWideNg * MT * 128 * sizeof(float) <= sizeof(s_a), "output tile must fit the chunk buffer");
+  f32x4 acc[kWideNtw][MT];
+  wide_mainloop<MT, KC>(p, blockIdx.x, 0, chunks, s_a, acc);
+  wide_epilogue<MT, EPI>(p, blockIdx.x, acc, reinterpret_cast<float*>(&s_a[0][0]), s_rs);
+}
+
+// Split s of column group g (work-group g + s G): chunks [s C / S, (s+1) C / S)
+// into the partial buffer.
+template <int MT, int KC>
+__global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT>())))
+void gemm_wide_split_kernel(const GemmParams p, int S, int chunks) {
+  __shared__ bf16x8 s_a[MT * KC][64];
+  const int G = (p.NT + kWideNg - 1) / kWideNg;
+  const int g = blockIdx.x % G, s = blockIdx.x / G;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c0 = static_cast<int>(static_cast<long>(s) * chunks / S);
+  const int c1 = static_cast<int>(static_cast<long>(s + 1) * chunks / S);
+  f32x4 acc[kWideNtw][MT];
+  wide_mainloop<MT, KC>(p, g, c0, c1, s_a, acc);
+  if (lane < 32) {
+    float* mine = p.part + ((static_cast<size_t>(s) * G + g) * kWideWaves + wave) * wide_part_floats<MT>();
+#pragma unroll
+    for (int j = 0; j < kWideNtw; ++j)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        *reinterpret_cast<f32x4*>(mine + ((j * MT + mt) * 32 + lane) * 4) = acc[j][mt];
+  }
+}
+
+// Sum of the S partials of column group g = blockIdx.x, in split order, then
+// the epilogue.
+template <int MT, int EPI>
+__global__ __launch_bounds__(kWideWaves * 64) void gemm_wide_reduce_kernel(const GemmParams p, int S) {
+  __shared__ float ep[kWideNg * MT * 128];
+  __shared__ float s_rs[MT * 8];
+  const int G = (p.NT + kWideNg - 1) / kWideNg;
+  const int g = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  f32x4 acc[kWideNtw][MT];
+#pragma unroll
+  for (int j = 0; j < kWideNtw; ++j)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (lane < 32) {
+    for (int s = 0; s < S; ++s) {
+      const float* src = p.part + ((static_cast<size_t>(s) * G + g) * kWideWaves + wave) * wide_part_floats<MT>();
+#pragma unroll
+      for (int j = 0; j < kWideNtw; ++j)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          acc[j][mt] += *reinterpret_cast<const f32x4*>(src + ((j * MT + mt) * 32 + lane) * 4);
+    }
+  }
+  wide_epilogue<MT, EPI>(p, g, acc, ep, s_rs);
+}
+
+// ---------------------------------------------------------------------------
+// Launch planning.
+// ---------------------------------------------------------------------------
+static const int kWideMT[] = {2, 3, 4, 5, 6, 8, 10, 12, 14, 16, 18, 20};
+
+// k-tiles per chunk: the chunk's MT x KC KiB of LDS leaves room for two to
+// three work-groups per CU and holds the output tile (4 MT KiB).
+static constexpr int wide_kc(int MT) { return MT <= 6 ? 8 : 4; }
+
+WidePlan wide_plan(int NT, int KT, int M) {
+  WidePlan w{};
+  const int mt = (M + 7) / 8;
+  w.MT = 20;
+  for (int v : kWideMT)
+    if (v >= mt) { w.MT = v; break; }
+  w.KC = wide_kc(w.MT);
+  w.G = (NT + kWideNg - 1) / kWideNg;
+  w.chunks = (KT + w.KC - 1) / w.KC;
+  // Split until the launch holds about two work-groups per CU (one above
+  // 12 M tiles, where registers allow one wave per SIMD).
+  const int target = w.MT <= 12 ? 512 : 256;
+  int S = (target + w.G - 1) / w.G;
+  S = std::min(S, 16);
+  S = std::min(S, std::max(1, w.chunks / 2));
+  w.S = std::max(S, 1);
+  return w;
+}
+
+size_t wide_part_bytes(const WidePlan& w) {
+  return w.S > 1 ? static_cast<size_t>(w.S) * w.G * kWideWaves * kWideNtw * w.MT * 128 * sizeof(float) : 0;
+}
+
+int wide_groups(int NT) { return (NT + kWideNg - 1) / kWideNg; }
+
+template <int MT, int KC = wide_kc(MT)>
+static hipError_t wide_launch(const GemmParams& p, const WidePlan& w, hipStream_t st) {
+  const dim3 block(kWideWaves * 64);
+  if (w.S > 1) {
+    hipLaunchKernelGGL((gemm_wide_split_kernel<MT, KC>), dim3(w.G * w.S), block, 0, st, p, w.S, w.chunks);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    switch (p.epi) {
+      case kEpiStore: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiStore>), dim3(w.G), block, 0, st, p, w.S); break;
+      case kEpiGelu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiGelu>), dim3(w.G), block, 0, st, p, w.S); break;
+      case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiSwiglu>), dim3(w.G), block, 0, st, p, w.S); break;
+      case kEpiResid: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiResid>), dim3(w.G), block, 0, st, p, w.S); break;
+      default: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiQkv>), dim3(w.G), block, 0, st, p, w.S); break;
+    }
+    return hipGetLastError();
+  }
+  const dim3 grid(w.G);
+  switch (p.epi) {
+    case kEpiStore: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, kEpiStore>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiGelu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, kEpiGelu>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, kEpiSwiglu>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiResid: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, kEpiResid>), grid, block, 0, st, p, w.chunks); break;
+    default: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, kEpiQkv>), grid, block, 0, st, p, w.chunks); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_wide(const GemmParams& p, const WidePlan& w, hipStream_t st) {
+  if (w.S > 1 && !p.part) return hipErrorInvalidValue;
+  switch (w.MT) {
+    case 2: return wide_launch<2>(p, w, st);
+    case 3: return wide_launch<3>(p, w, st);
+    case 4: return wide_launch<4>(p, w, st);
+    case 5: return wide_launch<5>(p, w, st);
+    case 6: return wide_launch<6>(p, w, st);
+    case 8: return wide_launch<8>(p, w, st);
+    case 10: return wide_launch<10>(p, w, st);
+    case 12: return wide_launch<12>(p, w, st);
+    case 14: return wide_launch<14>(p, w, st);
+    case 16: return wide_launch<16>(p, w, st);
+    case 18: return wide_launch<18>(p, w, st);
+    default: return wide_launch<20>(p, w, st);
+  }
+}
+
+}  // namespace sps

@@ -34,11 +34,21 @@ struct GemmParams {
   float* h; const float* gain; void* u; int ldu; size_t uplane; float* ss_out;
   const int32_t* lengths; int pos_offset, Mps, H, DH; float rope_base; int T_cap;
   void* q; void* kc; void* vc; int* err;
+  float* part;             // split-K partials (wide GEMM)
   int epi;
 };
 hipError_t launch_gemm(int dtype, const GemmParams& p, hipStream_t st);
 int gemm_max_rows(int dtype);                 // rows one launch handles
-int gemm_groups(int dtype, int NT, int Mtot); // column groups (work-groups) of a GEMM over Mtot rows
+int gemm_groups(int dtype, int NT, int Mtot); // column groups (ss_out groups) of a GEMM over Mtot rows
+
+// Wide GEMM (bf16, more than 8 rows; gemm_wide.hip): M tiles, k-tiles per
+// chunk, column groups, k splits and chunks of one launch.
+struct WidePlan { int MT, KC, G, S, chunks; };
+bool gemm_is_wide(int dtype, int Mtot);
+WidePlan wide_plan(int NT, int KT, int M);
+size_t wide_part_bytes(const WidePlan& w);    // workspace for the split-K partials
+int wide_groups(int NT);
+hipError_t launch_gemm_wide(const GemmParams& p, const WidePlan& w, hipStream_t st);
 
 // Pack canonical rows src[n][k] (n < n_src, k < Kd) into tile order. Row n goes
 // to packed row map(n): kind 0: row_off + n; kind 1: (n/8)*16 + row_off*8 + n%8

@@ -74,14 +74,32 @@ Layout make_layout(const sps_config* c) {
 
 // Offsets of the forward's scratch buffers.
 struct WsLayout {
-  size_t h, x, o, q, apart, act, ss_a, ss_b, logits, stats, total;
+  size_t h, x, o, q, apart, act, ss_a, ss_b, logits, stats, gpart, total;
 };
+
+// The GEMMs of one forward as (n-tiles, k-tiles).
+void forward_gemms(const Layout& L, int out[5][2]) {
+  const int shapes[5][2] = {{3 * L.HD / 16, L.d / 32}, {L.d / 16, L.HD / 32}, {L.N1 / 16, L.d / 32},
+                            {L.d / 16, L.F / 32}, {L.NU / 16, L.d / 32}};
+  std::memcpy(out, shapes, sizeof(shapes));
+}
 
 WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
   WsLayout w{};
+  const int dt = L.es == 2 ? 1 : 0;
   const size_t M = static_cast<size_t>(B) * Mps;
   const size_t NP = sps::attn_partials(T_cap);
   const size_t ng = (L.d + 15) / 16;   // column groups a residual GEMM can produce
+  // Split-K partials of the wide GEMM (bf16, more than 8 rows).
+  size_t part = 0;
+  if (sps::gemm_is_wide(dt, static_cast<int>(M))) {
+    int g[5][2];
+    forward_gemms(L, g);
+    for (int i = 0; i < 5; ++i) {
+      const sps::WidePlan p = sps::wide_plan(g[i][0], g[i][1], static_cast<int>(M));
+      part = std::max(part, sps::wide_part_bytes(p));
+    }
+  }
   size_t o = 0;
   w.h = o; o = align256(o + M * L.d * 4);                 // residual stream (fp32)
   w.x = o; o = align256(o + M * L.d * 4);                 // u = h * gain (activation format)
@@ -93,6 +111,7 @@ WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
   w.ss_b = o; o = align256(o + ng * M * 4);
   w.logits = o; o = align256(o + M * L.V * 4);
   w.stats = o; o = align256(o + M * 2 * 4);
+  w.gpart = o; o = align256(o + part);
   w.total = o;
   return w;
 }
@@ -177,7 +196,9 @@ sps_status gemm(int dtype, GemmParams p, hipStream_t st) {
       g_prof.bytes.push_back(rows_w * p.KT * 32 * wes + 4.0 * p.M * p.KT * 32 + 4.0 * p.M * p.n_valid);
       SPS_HIP(hipEventRecord(e0, st));
     }
-    const int reps = g_prof.on ? g_prof.repeats : 1;   // repeated launches recompute identical outputs
+    // Repeats redo the launch's work (a residual epilogue adds its output
+    // again), so a profiled forward is for timing only.
+    const int reps = g_prof.on ? g_prof.repeats : 1;
     for (int r = 0; r < reps; ++r) SPS_HIP(sps::launch_gemm(dtype, p, st));
     if (e1) SPS_HIP(hipEventRecord(e1, st));
   }
@@ -213,6 +234,7 @@ sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t*
   base.Mtot = M;
   base.inv_d = inv_d;
   base.eps = m->cfg.rms_eps;
+  base.part = reinterpret_cast<float*>(ws_base + ws.gpart);
 
   SPS_HIP(sps::launch_embed(dt, tokens, tok_stride, Mps, M, m->base + L.embed, L.V, L.d,
                             reinterpret_cast<const float*>(layer_ptr(m, 0, L.l_attn_norm)), h, x, uplane, ss_cur,
@@ -432,7 +454,12 @@ sps_status sps_kv_read(sps_kv_t kv, int32_t layer, int32_t b, int32_t pos0, int3
 
 size_t sps_workspace_bytes(const sps_config* cfg, int32_t B, int32_t max_tokens_per_seq, int32_t T_cap) {
   if (!valid_config(cfg) || B < 1 || max_tokens_per_seq < 1 || T_cap < 32) return 0;
-  return make_ws(make_layout(cfg), B, max_tokens_per_seq, T_cap).total;
+  // Every call with up to max_tokens_per_seq tokens must fit (the split-K
+  // partials of fewer rows can need more room than those of more rows).
+  const Layout L = make_layout(cfg);
+  size_t total = 0;
+  for (int mps = 1; mps <= max_tokens_per_seq; ++mps) total = std::max(total, make_ws(L, B, mps, T_cap).total);
+  return total;
 }
 
 sps_status sps_forward(sps_model_t model, sps_kv_t kv, const int32_t* tokens, int32_t tok_stride, int32_t B,

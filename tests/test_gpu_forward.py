@@ -149,3 +149,13 @@ def test_full_width_layer(sps, shape):
     """One full-width block + unembedding at K = 4, B = 1 against a 2048-token
     prior context: the per-layer kernels in the benchmark's launch shapes."""
     verify_parity(sps, shape.with_(n_layers=1), 1, 4, [2048], 21, 2e-2)
+
+
+@pytest.mark.parametrize("shape,B,K", [(configs.SEVENTY_B, 4, 4), (configs.SEVENTY_B, 16, 8),
+                                       (configs.SEVEN_B, 16, 1)], ids=["70b-B4K4", "70b-B16K8", "7b-B16K1"])
+def test_full_width_layer_batched(sps, shape, B, K):
+    """Batched full-width blocks: the wide GEMM in the sweep's launch shapes,
+    split-K (partials + reduction kernel) on the d_model-wide outputs."""
+    g = np.random.default_rng(100 * B + K)
+    verify_parity(sps, shape.with_(n_layers=1), B, K, [int(x) for x in g.integers(200, 600, B)], 31 + B, 2e-2,
+                  check_kv=False)
