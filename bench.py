@@ -32,14 +32,18 @@ METRIC = "verify-step ms + HBM GB/s (70B-shape, K=4, bs=1); SpS tokens/sec at 1 
 HBM_PEAK_GBS = 8000.0
 GEMM_REPEATS = 8                 # back-to-back launches per event bracket in the roofline pass
 CALIBRATION_BYTES = 1 << 30      # plain device copy whose HBM counters calibrate FETCH/WRITE_SIZE
-GEMM_SOURCE = os.path.join(ROOT, "paper_2302_01318_amd", "csrc", "gemm.hip")
+# Sources of the single-tile GEMM kernel (the one the traffic counters were taken on).
+GEMM_SOURCES = [os.path.join(ROOT, "paper_2302_01318_amd", "csrc", f) for f in ("gemm.hip", "gemm_epi.h", "common.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
 
 
-def source_digest(path):
+def source_digest(paths):
     import hashlib
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in paths:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic():
@@ -50,7 +54,7 @@ def measured_traffic():
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("gemm_source_sha256_16") != source_digest(GEMM_SOURCE):
+    if t.get("gemm_source_sha256_16") != source_digest(GEMM_SOURCES):
         return None
     return t.get("hbm_bytes_per_launch")
 
