@@ -219,18 +219,21 @@ def sweep(args):
 
 def accept_grid(args):
     """Accept/resample alone: V 32000, K in {1,2,4,8}, B in {1,8,64}, Philox
-    uniforms drawn in the kernel; inputs resident in HBM."""
+    uniforms drawn in the kernel; inputs resident in HBM, four input sets
+    used in turn."""
     import torch
     from paper_2302_01318_amd import configs, sps, synth
     g = configs.ACCEPT_GRID
     rows = []
     for K in g["K"]:
         for B in g["B"]:
-            p, q, drafts = synth.accept_case_device(args.seed + K * 100 + B, B, K, g["V"], g["sigma"],
-                                                     g["sigma_pert"])
+            # 4 input sets used in turn, so that the 256 MB MALL cannot serve a repeat
+            sets = [synth.accept_case_device(args.seed + K * 100 + B + 7 * j, B, K, g["V"], g["sigma"],
+                                             g["sigma_pert"]) for j in range(4)]
             out = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
             nacc = torch.empty(B, dtype=torch.int32, device="cuda")
-            ms = timed(lambda i: sps.accept_resample(p, q, drafts, None, (args.seed, i), out, nacc), 50, 5)
+            ms = timed(lambda i: sps.accept_resample(sets[i % 4][0], sets[i % 4][1], sets[i % 4][2], None,
+                                                     (args.seed, i), out, nacc), 52, 4)
             naive = B * (2 * K + 1) * g["V"] * 4
             needed = B * (2 * g["V"] * 4 + 2 * K * 4 + (K + 1) * 4 + 4)
             rows.append({"B": B, "K": K, "us": round(ms * 1e3, 2),

@@ -6,10 +6,11 @@
 // exactly the result of a serial loop: weights w_i = floor(x_i 2^32) for
 // probabilities x_i (0 for x_i <= 0 or NaN, 2^32 for x_i >= 1), total W,
 // threshold t = floor(m W / 2^24) for the grid index m = floor(u 2^24) of the
-// uniform, result = smallest i whose inclusive prefix sum exceeds t. Each
-// thread owns a contiguous chunk of the vocabulary; one block-wide uint64
-// scan gives every chunk its exclusive prefix, and the one chunk containing
-// the threshold is walked serially.
+// uniform, result = smallest i whose inclusive prefix sum exceeds t. Wave w
+// of the work-group owns one contiguous segment of the vocabulary and reads
+// it 64 consecutive entries at a time; the 16 segment totals give every
+// segment its exclusive prefix, and only the wave whose segment holds the
+// threshold scans it again to find the index.
 #include "common.h"
 #include "launch.h"
 #include "philox.h"
@@ -17,11 +18,17 @@
 namespace sps {
 
 constexpr int kSampleThreads = 1024;
+constexpr int kPerLane = 32;            // row entries per thread read together (row statistics)
+constexpr int kTotalBatch = 8;          // entries per lane read together (segment totals)
+constexpr int kScanPerLane = 16;        // entries per lane of the threshold search (registers)
 
+// Branch-free (selects only), so that loops over a row keep their loads in
+// flight together: floor(x 2^32) for x in (0, 1), 2^32 for x >= 1, 0 for
+// x <= 0 or NaN.
 __device__ __forceinline__ uint64_t fixed_weight(float x) {
-  if (!(x > 0.f)) return 0;
-  if (x >= 1.f) return 1ull << 32;
-  return static_cast<uint64_t>(static_cast<double>(x) * 4294967296.0);
+  const double d = x > 0.f ? fmin(static_cast<double>(x), 1.0) : 0.0;
+  const double f = fmin(d * 4294967296.0, 4294967295.0);        // d = 1 adds the missing unit below
+  return static_cast<uint64_t>(static_cast<uint32_t>(f)) + (d >= 1.0 ? 1u : 0u);
 }
 
 __device__ __forceinline__ uint64_t grid_threshold(float u, uint64_t W) {
@@ -40,12 +47,15 @@ struct RowStat { float a, b; };
 // used wherever q or p is materialised, so exported probabilities and the
 // values the accept test sees are identical bit for bit.
 __device__ __forceinline__ float prob_of(float z, RowStat st, float inv_t, int i) {
-  if (st.b < 0.f) return i == static_cast<int>(st.a) ? 1.f : 0.f;
   const float t = __fsub_rn(__fmul_rn(z, inv_t), st.a);
-  return __fdiv_rn(expf(t), st.b);
+  const float v = __fdiv_rn(expf(t), st.b);
+  const float g = i == __float2int_rz(st.a) ? 1.f : 0.f;        // greedy row: one-hot at the arg-max
+  return st.b < 0.f ? g : v;
 }
 
-__device__ RowStat row_stat(const float* __restrict__ z, int V, float temperature, float* red, int* ired) {
+// red: __shared__ float[32], ired: __shared__ int[16].
+__device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, float temperature, float* red,
+                                          int* ired) {
   RowStat st;
   if (temperature == 0.f) {
     float best = -INFINITY;
@@ -70,22 +80,78 @@ __device__ RowStat row_stat(const float* __restrict__ z, int V, float temperatur
     st.b = -1.f;
     return st;
   }
+  // Rows of up to kPerLane * blockDim entries are read once into registers
+  // (all loads in flight together), then max and sum of exp(x - max) come
+  // from the registers; longer rows keep a running (max, sum) per thread.
   const float inv_t = 1.0f / temperature;
-  float mx = -INFINITY;
-  for (int i = threadIdx.x; i < V; i += blockDim.x) mx = fmaxf(mx, __fmul_rn(z[i], inv_t));
-  mx = block_max(mx, red);
-  float s = 0.f;
-  for (int i = threadIdx.x; i < V; i += blockDim.x) s += expf(__fsub_rn(__fmul_rn(z[i], inv_t), mx));
-  s = block_sum(s, red);
+  float mx = -INFINITY, sm = 0.f;
+  if (V <= kPerLane * static_cast<int>(blockDim.x)) {
+    float x[kPerLane];
+#pragma unroll
+    for (int k = 0; k < kPerLane; ++k)   // all loads first (clamped: none behind a branch)
+      x[k] = z[min(threadIdx.x + k * blockDim.x, static_cast<unsigned>(V - 1))];
+#pragma unroll
+    for (int k = 0; k < kPerLane; ++k) {
+      x[k] = threadIdx.x + k * blockDim.x < static_cast<unsigned>(V) ? __fmul_rn(x[k], inv_t) : -INFINITY;
+      mx = fmaxf(mx, x[k]);
+    }
+    if (mx > -INFINITY) {
+#pragma unroll
+      for (int k = 0; k < kPerLane; ++k) sm += expf(x[k] - mx);
+    }
+  } else {
+    for (int i = threadIdx.x; i < V; i += blockDim.x) {
+      const float x = __fmul_rn(z[i], inv_t);
+      if (x > mx) {
+        sm = sm * expf(mx - x) + 1.f;
+        mx = x;
+      } else if (x > -INFINITY) {
+        sm += expf(x - mx);
+      }
+    }
+  }
+  auto merge = [](float& m, float& s2, float om, float os) {
+    const float nm = fmaxf(m, om);
+    if (nm == -INFINITY) return;
+    s2 = s2 * expf(m - nm) + os * expf(om - nm);
+    m = nm;
+  };
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float om = __shfl_xor(mx, o), os = __shfl_xor(sm, o);
+    merge(mx, sm, om, os);
+  }
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) { red[threadIdx.x >> 6] = mx; red[16 + (threadIdx.x >> 6)] = sm; }
+  __syncthreads();
+  mx = red[0];
+  sm = red[16];
+  for (int w = 1; w < static_cast<int>(blockDim.x >> 6); ++w) merge(mx, sm, red[w], red[16 + w]);
   st.a = mx;
-  st.b = s;
+  st.b = sm;
   return st;
+}
+
+// pr[i] = prob_of(z[i]) for the whole row, 8 loads per thread in flight.
+__device__ __forceinline__ void write_probs(const float* __restrict__ z, int V, RowStat st, float inv_t,
+                                            float* __restrict__ pr) {
+  const int bd = blockDim.x;
+  for (int base = 0; base < V; base += 8 * bd) {
+    float zz[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) zz[k] = z[min(base + k * bd + static_cast<int>(threadIdx.x), V - 1)];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int i = base + k * bd + threadIdx.x;
+      if (i < V) pr[i] = prob_of(zz[k], st, inv_t, i);
+    }
+  }
 }
 
 __global__ __launch_bounds__(kSampleThreads) void row_softmax_kernel(const float* __restrict__ logits, int V,
                                                                      float temperature, RowStat* __restrict__ stats,
                                                                      float* __restrict__ probs) {
-  __shared__ float red[16];
+  __shared__ float red[32];
   __shared__ int ired[16];
   const int row = blockIdx.x;
   const float* z = logits + static_cast<size_t>(row) * V;
@@ -93,16 +159,127 @@ __global__ __launch_bounds__(kSampleThreads) void row_softmax_kernel(const float
   if (threadIdx.x == 0 && stats) stats[row] = st;
   if (probs) {
     const float inv_t = temperature == 0.f ? 0.f : 1.0f / temperature;
-    float* pr = probs + static_cast<size_t>(row) * V;
-    for (int i = threadIdx.x; i < V; i += blockDim.x) pr[i] = prob_of(z[i], st, inv_t, i);
+    write_probs(z, V, st, inv_t, probs + static_cast<size_t>(row) * V);
   }
 }
 
-// Target probabilities given as a [rows][V] array.
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
+  const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), o);
+  const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), o);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += shfl_xor_u64(v, o);
+  return v;
+}
+__device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint64_t o = shfl_up_u64(v, d);
+    if (lane >= d) v += o;
+  }
+  return v;
+}
+
+// Segment [b0, b1) of the vocabulary owned by this wave: a multiple of 64
+// entries, the waves' segments in order.
+struct Segment { int b0, b1; };
+__device__ __forceinline__ Segment wave_segment(int V) {
+  const int nw = blockDim.x >> 6, w = threadIdx.x >> 6;
+  const int S = ((V + nw - 1) / nw + 63) & ~63;
+  const int b0 = min(V, w * S);
+  return Segment{b0, min(V, b0 + S)};
+}
+
+// Total of the weights wf(i) over this wave's segment (every lane gets it).
+// Lane l reads entries base + 64 k + l: every load instruction is coalesced.
+template <class WF>
+__device__ __forceinline__ uint64_t segment_total(WF wf, Segment sg) {
+  const int lane = threadIdx.x & 63;
+  uint64_t loc = 0;
+  for (int base = sg.b0; base < sg.b1; base += 64 * kTotalBatch) {
+    // Indexes past the segment read its last entry and are masked after
+    // the load, so that no load sits behind a branch and a batch is in
+    // flight together.
+#pragma unroll
+    for (int k = 0; k < kTotalBatch; ++k) {
+      const int i = base + 64 * k + lane;
+      const uint64_t x = wf(min(i, sg.b1 - 1));
+      loc += i < sg.b1 ? x : 0;
+    }
+  }
+  return wave_sum_u64(loc);
+}
+
+// Block-wide integer inverse-CDF draw with weights wf(i), i < V, given every
+// wave's segment total `tot` (from segment_total). s_tot is __shared__
+// uint64_t[16 + 1], s_res a __shared__ int. Returns the drawn index to every
+// thread, or -1 when all weights are zero (W == 0). The wave whose segment
+// holds the threshold reads it again (now cache-resident) with lane l owning
+// kScanPerLane consecutive entries of a super-chunk, scans the lane totals and
+// lets the one lane whose range holds the threshold walk its registers.
+template <class WF>
+__device__ int block_draw(WF wf, Segment sg, uint64_t tot, float u, uint64_t* s_tot, int* s_res) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  __syncthreads();                         // s_tot / s_res free from any previous draw
+  if (lane == 0) s_tot[wave] = tot;
+  if (threadIdx.x == 0) *s_res = -1;
+  __syncthreads();
+  uint64_t off = 0, W = 0;
+  for (int w = 0; w < nw; ++w) {
+    const uint64_t t = s_tot[w];
+    off += w < wave ? t : 0;
+    W += t;
+  }
+  if (W == 0) return -1;                   // uniform over the block
+  const uint64_t thr = grid_threshold(u, W);
+  if (off <= thr && thr < off + tot) {     // the crossing lies in this wave's segment
+    uint64_t run = off;
+    for (int base = sg.b0; base < sg.b1; base += 64 * kScanPerLane) {
+      uint64_t w[kScanPerLane];
+      uint64_t lt = 0;
+      const int c0 = base + kScanPerLane * lane;
+#pragma unroll
+      for (int k = 0; k < kScanPerLane; ++k) {
+        const uint64_t x = wf(min(c0 + k, sg.b1 - 1));
+        w[k] = c0 + k < sg.b1 ? x : 0;
+        lt += w[k];
+      }
+      const uint64_t inc = wave_incl_scan_u64(lt);
+      const uint64_t all = (static_cast<uint64_t>(__shfl(static_cast<uint32_t>(inc >> 32), 63)) << 32) |
+                           __shfl(static_cast<uint32_t>(inc), 63);
+      if (run + all > thr) {               // wave-uniform
+        const uint64_t ex = run + inc - lt;
+        if (ex <= thr && thr < ex + lt) {  // exactly one lane
+          uint64_t acc = ex;
+          int hit = -1;                    // first entry whose inclusive prefix exceeds thr
+#pragma unroll
+          for (int k = 0; k < kScanPerLane; ++k) {
+            acc += w[k];
+            if (hit < 0 && acc > thr) hit = k;
+          }
+          *s_res = c0 + hit;
+        }
+        break;
+      }
+      run += all;
+    }
+  }
+  __syncthreads();
+  return *s_res;
+}
+
+// Target probabilities given as a [rows][V] array; row(r)(i) = q_r(i).
 struct QProbs {
   const float* q;
   int V;
-  __device__ float operator()(int row, int i) const { return q[static_cast<size_t>(row) * V + i]; }
+  struct Row {
+    const float* q;
+    __device__ float operator()(int i) const { return q[i]; }
+  };
+  __device__ Row row(int r) const { return Row{q + static_cast<size_t>(r) * V}; }
 };
 // Target probabilities formed on the fly from logits and row statistics.
 struct QLogits {
@@ -110,9 +287,13 @@ struct QLogits {
   const RowStat* st;
   float inv_t;
   int V;
-  __device__ float operator()(int row, int i) const {
-    return prob_of(z[static_cast<size_t>(row) * V + i], st[row], inv_t, i);
-  }
+  struct Row {
+    const float* z;
+    RowStat st;
+    float inv_t;
+    __device__ float operator()(int i) const { return prob_of(z[i], st, inv_t, i); }
+  };
+  __device__ Row row(int r) const { return Row{z + static_cast<size_t>(r) * V, st[r], inv_t}; }
 };
 
 // One block per sequence. drafts[b * dstride + doff + t] is x~_{t+1}.
@@ -137,7 +318,7 @@ __global__ __launch_bounds__(kSampleThreads) void accept_kernel(QS qs, const flo
         bad = true;
         rejected = true;
       } else {
-        const float rho = qs(b * (K + 1) + tid, x);
+        const float rho = qs.row(b * (K + 1) + tid)(x);
         const float pi = p[(static_cast<size_t>(b) * K + tid) * V + x];
         const float r = unif ? unif[b * (K + 1) + tid] : philox_uniform(seed, loop, 1, b, tid);
         rejected = !(static_cast<double>(r) * static_cast<double>(pi) < static_cast<double>(rho));
@@ -154,43 +335,23 @@ __global__ __launch_bounds__(kSampleThreads) void accept_kernel(QS qs, const flo
   const bool resid = a < K;
   const float* prow = p + (static_cast<size_t>(b) * K + (resid ? a : 0)) * V;
 
-  // 2. weights of (q - p)_+ (or q for the bonus / the zero-residual fallback)
-  const int C = (V + blockDim.x - 1) / blockDim.x;
-  const int i0 = min(V, tid * C), i1 = min(V, i0 + C);
-  auto weight = [&](int i, bool use_resid) -> uint64_t {
-    const uint64_t wq = fixed_weight(qs(row, i));
-    if (!use_resid) return wq;
-    const uint64_t wp = fixed_weight(prow[i]);
-    return wq > wp ? wq - wp : 0;
+  // 2. draw from (q - p)_+ (or q for the bonus / the zero-residual fallback)
+  const Segment sg = wave_segment(V);
+  const typename QS::Row qr = qs.row(row);
+  auto wq = [&](int i) -> uint64_t { return fixed_weight(qr(i)); };
+  auto wr = [&](int i) -> uint64_t {
+    const uint64_t x = fixed_weight(qr(i)), y = fixed_weight(prow[i]);
+    return x > y ? x - y : 0;
   };
-  bool use_resid = resid;
-  uint64_t loc = 0;
-  for (int i = i0; i < i1; ++i) loc += weight(i, use_resid);
-  uint64_t W;
-  uint64_t ex = block_exscan_u64(loc, wsum, &W);
-  if (use_resid && W == 0) {
-    use_resid = false;
-    loc = 0;
-    for (int i = i0; i < i1; ++i) loc += weight(i, false);
-    ex = block_exscan_u64(loc, wsum, &W);
+  const float u = unif ? unif[b * (K + 1) + K] : philox_uniform(seed, loop, 2, b, 0);
+  int y = -1;
+  if (resid) y = block_draw(wr, sg, segment_total(wr, sg), u, wsum, &s_y);
+  if (y < 0) y = block_draw(wq, sg, segment_total(wq, sg), u, wsum, &s_y);
+  if (y < 0) {
+    y = 0;
+    if (tid == 0) atomicOr(err, kErrEmpty);
   }
-
-  // 3. inverse CDF draw
-  if (W > 0) {
-    const float u = unif ? unif[b * (K + 1) + K] : philox_uniform(seed, loop, 2, b, 0);
-    const uint64_t thr = grid_threshold(u, W);
-    if (ex <= thr && thr < ex + loc) {
-      uint64_t acc = ex;
-      for (int i = i0; i < i1; ++i) {
-        acc += weight(i, use_resid);
-        if (acc > thr) { s_y = i; break; }
-      }
-    }
-  } else if (tid == 0) {
-    atomicOr(err, kErrEmpty);
-  }
-  __syncthreads();
-  if (tid <= K) out[static_cast<size_t>(b) * (K + 1) + tid] = tid < a ? dr[tid] : (tid == a ? s_y : -1);
+  if (tid <= K) out[static_cast<size_t>(b) * (K + 1) + tid] = tid < a ? dr[tid] : (tid == a ? y : -1);
   if (tid == 0) n_acc[b] = a;
 }
 
@@ -199,7 +360,7 @@ __global__ __launch_bounds__(kSampleThreads) void accept_kernel(QS qs, const flo
 __global__ __launch_bounds__(kSampleThreads) void draft_sample_kernel(
     const float* __restrict__ logits, int Mps, int V, float temperature, float* __restrict__ p_out, int K, int t,
     int32_t* __restrict__ tokens, const int32_t* __restrict__ ctx, uint64_t seed, uint64_t loop, int* err) {
-  __shared__ float red[16];
+  __shared__ float red[32];
   __shared__ int ired[16];
   __shared__ uint64_t wsum[17];
   __shared__ int s_y;
@@ -207,31 +368,16 @@ __global__ __launch_bounds__(kSampleThreads) void draft_sample_kernel(
   const float* z = logits + (static_cast<size_t>(b) * Mps + Mps - 1) * V;
   const RowStat st = row_stat(z, V, temperature, red, ired);
   const float inv_t = temperature == 0.f ? 0.f : 1.0f / temperature;
-  float* pr = p_out + (static_cast<size_t>(b) * K + t) * V;
-  for (int i = tid; i < V; i += blockDim.x) pr[i] = prob_of(z[i], st, inv_t, i);
-  const int C = (V + blockDim.x - 1) / blockDim.x;
-  const int i0 = min(V, tid * C), i1 = min(V, i0 + C);
-  uint64_t loc = 0;
-  for (int i = i0; i < i1; ++i) loc += fixed_weight(prob_of(z[i], st, inv_t, i));
-  uint64_t W;
-  const uint64_t ex = block_exscan_u64(loc, wsum, &W);
-  if (tid == 0) s_y = 0;
-  __syncthreads();
-  if (W > 0) {
-    const uint64_t thr = grid_threshold(philox_uniform(seed, loop, 0, b, t), W);
-    if (ex <= thr && thr < ex + loc) {
-      uint64_t acc = ex;
-      for (int i = i0; i < i1; ++i) {
-        acc += fixed_weight(prob_of(z[i], st, inv_t, i));
-        if (acc > thr) { s_y = i; break; }
-      }
-    }
-  } else if (tid == 0) {
-    atomicOr(err, kErrEmpty);
+  write_probs(z, V, st, inv_t, p_out + (static_cast<size_t>(b) * K + t) * V);
+  const Segment sg = wave_segment(V);
+  auto wp = [&](int i) -> uint64_t { return fixed_weight(prob_of(z[i], st, inv_t, i)); };
+  int y = block_draw(wp, sg, segment_total(wp, sg), philox_uniform(seed, loop, 0, b, t), wsum, &s_y);
+  if (y < 0) {
+    y = 0;
+    if (tid == 0) atomicOr(err, kErrEmpty);
   }
-  __syncthreads();
   if (tid == 0) {
-    tokens[static_cast<size_t>(b) * (K + 1) + t + 1] = s_y;
+    tokens[static_cast<size_t>(b) * (K + 1) + t + 1] = y;
     if (t == 0) tokens[static_cast<size_t>(b) * (K + 1)] = ctx[2 * b + 1];
   }
 }
