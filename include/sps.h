@@ -230,8 +230,10 @@ sps_status sps_softmax(const float* logits, int32_t rows, int32_t V, float tempe
 /* Measurement helpers. Between begin and end, every weight-streaming GEMM
  * launch (the linear layers: QKV, attention output, FFN, unembedding) is
  * issued `repeats` (1..64) times back to back between two HIP events on its
- * stream (the repeats recompute identical outputs; they amortise the event
- * and dispatch latency so the per-launch time is the kernel's own). end
+ * stream (the repeats amortise the event and dispatch latency so the
+ * per-launch time is the kernel's own; they redo the launch's work, so a
+ * residual epilogue adds its output once per repeat and a profiled forward
+ * is for timing only). end
  * synchronises the events and returns the summed per-launch kernel time
  * (ms, divided by repeats), the number of distinct launches and their
  * algorithmic bytes (weights + input activations + outputs, once each).
