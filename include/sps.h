@@ -74,6 +74,26 @@ typedef struct {
 
 enum { SPS_PURPOSE_DRAFT = 0, SPS_PURPOSE_ACCEPT = 1, SPS_PURPOSE_RESAMPLE = 2 };
 
+/* Probability modifiers applied alike to the draft and the target
+ * distributions before modified rejection sampling (Modified Rejection
+ * Sampling section, closing paragraph; Table 1 uses nucleus sampling):
+ *  - temperature T >= 0: softmax(logits / T); T == 0 is greedy (one-hot
+ *    argmax, lowest index on ties; top_k / top_p are then ignored);
+ *  - top_k: keep the top_k highest-ranked entries (0 or >= V: off);
+ *  - top_p in [0, 1]: nucleus -- among what top-k kept, keep the shortest
+ *    prefix of the ranking whose mass reaches top_p, at least one entry
+ *    (1: off).
+ * Ranking is by the draw weight floor(x 2^32), larger first, ties by lower
+ * index; masses are integer sums of those weights and the nucleus threshold
+ * is floor(floor(top_p 2^24) W / 2^24) of the kept total W; kept entries are
+ * renormalised as x / (fp32(S) 2^-32) with S their exact integer weight sum.
+ * With either modifier on, V must be <= 32768 (SPS_E_UNSUPPORTED else). */
+typedef struct {
+  float temperature;
+  int32_t top_k;
+  float top_p;
+} sps_sampling;
+
 /* Weight tensors, in canonical row-major nn.Linear orientation [out][in] and
  * the model dtype, except the gains (always fp32):
  *   EMBED [V][d], FINAL_NORM [d], UNEMBED [V][d],
@@ -167,14 +187,14 @@ typedef struct {
 /* The SpS verify step (Algorithm 2): one target forward over
  * tokens[b] = (x_n, x~_1..x~_K) ([B][K+1] int32) at positions
  * lengths[b]..lengths[b]+K, i.e. the K+1 conditionals q(.|x_1..x_n),
- * ..., q(.|x_1..x_n, x~_1..x~_K) in one call; then q = softmax(logits / T)
- * (T == 0: one-hot argmax, lowest index on ties) and, if acc != NULL, the
+ * ..., q(.|x_1..x_n, x~_1..x~_K) in one call; then q = the modified
+ * softmax(logits / T) of `sampling` and, if acc != NULL, the
  * modified rejection sampling of the drafts. K == 0 is auto-regressive
  * sampling (Algorithm 1): one token drawn from q. logits_out [B][K+1][V] and
  * q_out [B][K+1][V] are optional. KV entries are written but lengths are not
  * advanced (see sps_commit). */
 sps_status sps_verify_step(sps_model_t target, sps_kv_t kv, const int32_t* tokens, int32_t B,
-                           int32_t K, float temperature, float* logits_out, float* q_out,
+                           int32_t K, sps_sampling sampling, float* logits_out, float* q_out,
                            const sps_accept_io* acc, void* workspace, size_t ws_bytes,
                            void* stream);
 
@@ -201,11 +221,12 @@ sps_status sps_accept_resample(const float* p_draft, const float* q_target,
  * last committed token and the newest, not yet scored one. Step 1 runs the
  * draft over both (re-writing position lengths[b]-1 in the draft cache is
  * harmless and keeps every step one shape); step t >= 2 runs it over x~_{t-1}.
- * Each step forms p_t = softmax(logits / T), writes it to p_out[b][t-1][:],
+ * Each step forms p_t = the modified softmax(logits / T) of `sampling`,
+ * writes it to p_out[b][t-1][:],
  * and draws x~_t with Philox purpose DRAFT, j = t-1. Writes the verify input
  * tokens[b] = (ctx[b][1], x~_1..x~_K) ([B][K+1]). Requires lengths[b] >= 1. */
 sps_status sps_draft_step(sps_model_t draft, sps_kv_t kv, const int32_t* ctx, int32_t B,
-                          int32_t K, float temperature, sps_philox rng, int32_t* tokens,
+                          int32_t K, sps_sampling sampling, sps_philox rng, int32_t* tokens,
                           float* p_out, void* workspace, size_t ws_bytes, void* stream);
 
 /* End of an SpS loop, on the device (no host synchronisation): for each
@@ -222,9 +243,10 @@ sps_status sps_commit(sps_kv_t kv, const int32_t* tokens, const int32_t* out_tok
 sps_status sps_philox_uniforms(sps_philox rng, int32_t purpose, int32_t B, int32_t n,
                                float* out, void* stream);
 
-/* probs[r][:] = softmax(logits[r][:] / T) for `rows` rows of V fp32 values,
- * the same arithmetic as the q the verify step feeds to acceptance. */
-sps_status sps_softmax(const float* logits, int32_t rows, int32_t V, float temperature,
+/* probs[r][:] = the modified softmax(logits[r][:] / T) of `sampling` for
+ * `rows` rows of V fp32 values, the same arithmetic as the q the verify step
+ * feeds to acceptance. */
+sps_status sps_softmax(const float* logits, int32_t rows, int32_t V, sps_sampling sampling,
                        float* probs, void* stream);
 
 /* Measurement helpers. Between begin and end, every weight-streaming GEMM

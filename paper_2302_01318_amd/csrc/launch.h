@@ -72,18 +72,23 @@ hipError_t launch_kv_copy(int dtype, int to_cache, void* kc, void* vc, int H, in
                           int pos0, int n, void* k, void* v, hipStream_t st);
 
 // Sampling.
-hipError_t launch_row_softmax(const float* logits, int rows, int V, float temperature,
-                              float* stats, float* probs, hipStream_t st);
+// Row statistics (stats, row_stat_bytes() each, may be NULL) and, if probs
+// != NULL, the probabilities after temperature and the top-k / nucleus
+// modifiers (top_k <= 0 or >= V: off; top_p >= 1: off).
+hipError_t launch_row_softmax(const float* logits, int rows, int V, float temperature, int top_k, float top_p,
+                              void* stats, float* probs, hipStream_t st);
+size_t row_stat_bytes();
+int modifier_max_vocab();        // largest vocabulary the top-k / nucleus cut-off handles
 hipError_t launch_accept_probs(const float* p, const float* q, const int32_t* drafts,
                                const float* unif, uint64_t seed, uint64_t loop, int B, int K,
                                int V, int32_t* out, int32_t* n_acc, int* err, hipStream_t st);
-hipError_t launch_accept_logits(const float* p, const float* logits, const float* stats,
+hipError_t launch_accept_logits(const float* p, const float* logits, const void* stats,
                                 float temperature, const int32_t* tokens, const float* unif,
                                 uint64_t seed, uint64_t loop, int B, int K, int V, int32_t* out,
                                 int32_t* n_acc, int* err, hipStream_t st);
 hipError_t launch_draft_sample(const float* logits, int Mps, int B, int V, float temperature,
-                               float* p_out, int K, int t, int32_t* tokens, const int32_t* ctx,
-                               uint64_t seed, uint64_t loop, int* err, hipStream_t st);
+                               int top_k, float top_p, float* p_out, int K, int t, int32_t* tokens,
+                               const int32_t* ctx, uint64_t seed, uint64_t loop, int* err, hipStream_t st);
 hipError_t launch_commit(int32_t* lengths, const int32_t* tokens, const int32_t* out,
                          const int32_t* n_acc, int B, int K, int32_t* ctx, int32_t* seq_out,
                          int32_t* n_out, int cap, hipStream_t st);

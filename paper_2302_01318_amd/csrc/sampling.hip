@@ -22,6 +22,26 @@ constexpr int kPerLane = 32;            // row entries per thread read together 
 constexpr int kTotalBatch = 8;          // entries per lane read together (segment totals)
 constexpr int kScanPerLane = 16;        // entries per lane of the threshold search (registers)
 
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
+  const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), o);
+  const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), o);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += shfl_xor_u64(v, o);
+  return v;
+}
+__device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint64_t o = shfl_up_u64(v, d);
+    if (lane >= d) v += o;
+  }
+  return v;
+}
+
 // Branch-free (selects only), so that loops over a row keep their loads in
 // flight together: floor(x 2^32) for x in (0, 1), 2^32 for x >= 1, 0 for
 // x <= 0 or NaN.
@@ -39,9 +59,15 @@ __device__ __forceinline__ uint64_t grid_threshold(float u, uint64_t W) {
   return m * (W >> 24) + ((m * (W & 0xFFFFFFull)) >> 24);
 }
 
-// Row statistics of softmax(z / T): (max of z/T, sum of exp(z/T - max)); for
-// T == 0 (greedy) (index of the first maximum, -1).
-struct RowStat { float a, b; };
+// Row statistics of softmax(z / T): (a, b) = (max of z/T, sum of
+// exp(z/T - max)), for T == 0 (greedy) (index of the first maximum, -1).
+// With a top-k / nucleus modifier, s > 0 is the renormaliser and tau the
+// smallest kept ranking key (see row_cutoff); s == 0 means unmodified.
+struct RowStat {
+  float a, b, s;
+  uint32_t pad;
+  uint64_t tau;
+};
 
 // Probability of entry i of a row. The same expression (no contraction) is
 // used wherever q or p is materialised, so exported probabilities and the
@@ -53,10 +79,29 @@ __device__ __forceinline__ float prob_of(float z, RowStat st, float inv_t, int i
   return st.b < 0.f ? g : v;
 }
 
+// Ranking key of the top-k / nucleus modifiers: the draw weight above the
+// complement of the index, so larger keys rank first, equal weights rank
+// by lower index, and every entry's key is distinct and >= 1 (V < 2^24).
+__device__ __forceinline__ uint64_t rank_key(uint64_t w, int i) {
+  return (w << 24) | static_cast<uint64_t>(0xFFFFFF - i);
+}
+
+// The probability the sampling stages use: prob_of, then the modifiers'
+// cut and renormalisation x / s (branch-free).
+__device__ __forceinline__ float prob_final(float z, const RowStat& st, float inv_t, int i) {
+  const float x = prob_of(z, st, inv_t, i);
+  const bool keep = rank_key(fixed_weight(x), i) >= st.tau;
+  const float y = __fdiv_rn(x, st.s);
+  return st.s > 0.f ? (keep ? y : 0.f) : x;
+}
+
 // red: __shared__ float[32], ired: __shared__ int[16].
 __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, float temperature, float* red,
                                           int* ired) {
   RowStat st;
+  st.s = 0.f;
+  st.pad = 0;
+  st.tau = 0;
   if (temperature == 0.f) {
     float best = -INFINITY;
     int bi = 0x7fffffff;
@@ -132,8 +177,137 @@ __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, 
   return st;
 }
 
-// pr[i] = prob_of(z[i]) for the whole row, 8 loads per thread in flight.
-__device__ __forceinline__ void write_probs(const float* __restrict__ z, int V, RowStat st, float inv_t,
+// Scratch of row_cutoff (LDS).
+struct CutScratch {
+  uint64_t hist[256];
+  uint64_t prefix, need;
+  uint64_t wsum[16];
+};
+
+// The row's draw weights for the cut-off, in LDS (dynamic shared memory of
+// cutoff_lds_bytes(V)): the low 32 bits of every weight and a bitmask of the
+// weights equal to 2^32 (x >= 1).
+struct RowKeys {
+  uint32_t* wl;    // [V]
+  uint32_t* big;   // [ceil(V / 32)]
+  int V;
+  __device__ __forceinline__ uint64_t weight(int i) const {
+    return static_cast<uint64_t>(wl[i]) | (static_cast<uint64_t>((big[i >> 5] >> (i & 31)) & 1u) << 32);
+  }
+  __device__ __forceinline__ uint64_t key(int i) const { return rank_key(weight(i), i); }
+};
+
+// Sum of the weights of keys >= lo, over the block.
+__device__ __forceinline__ uint64_t kept_weight(const RowKeys& rk, uint64_t lo, CutScratch& sc) {
+  uint64_t v = 0;
+#pragma unroll 4
+  for (int i = threadIdx.x; i < rk.V; i += blockDim.x) v += rk.key(i) >= lo ? rk.weight(i) : 0;
+  v = wave_sum_u64(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sc.wsum[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint64_t t = 0;
+  for (int w = 0; w < static_cast<int>(blockDim.x >> 6); ++w) t += sc.wsum[w];
+  return t;
+}
+
+// Radix select over the row's keys: the key tau such that the count
+// (WEIGHTED: the weight) of keys >= max(tau, lo) reaches `need` (>= 1) while
+// that of keys > tau does not. Eight passes of 8-bit digits from the top;
+// per pass a 256-bin LDS histogram of the keys that match the digits chosen
+// so far. Digit 0 (the leading zeros of the many small weights) is summed
+// per thread and added once per wave.
+template <bool WEIGHTED>
+__device__ __forceinline__ uint64_t radix_select(const RowKeys& rk, uint64_t lo, uint64_t need, CutScratch& sc) {
+  const int tid = threadIdx.x;
+  uint64_t P = 0;
+  for (int sh = 56; sh >= 0; sh -= 8) {
+    for (int b = tid; b < 256; b += blockDim.x) sc.hist[b] = 0;
+    __syncthreads();
+    const uint64_t hm = sh + 8 >= 64 ? 0 : ~((1ull << (sh + 8)) - 1);
+    uint64_t zero = 0;
+#pragma unroll 4
+    for (int i = tid; i < rk.V; i += blockDim.x) {
+      const uint64_t key = rk.key(i);
+      const bool in = key >= lo && (key & hm) == (P & hm);
+      const uint32_t d = static_cast<uint32_t>(key >> sh) & 255u;
+      const uint64_t v = WEIGHTED ? rk.weight(i) : 1;
+      if (in && d == 0) zero += v;
+      else if (in && v) atomicAdd(reinterpret_cast<unsigned long long*>(&sc.hist[d]), v);
+    }
+    zero = wave_sum_u64(zero);
+    if ((tid & 63) == 0 && zero) atomicAdd(reinterpret_cast<unsigned long long*>(&sc.hist[0]), zero);
+    __syncthreads();
+    if (tid == 0) {
+      uint64_t c = 0;
+      int b = 255;
+      for (; b > 0; --b) {
+        if (c + sc.hist[b] >= need) break;
+        c += sc.hist[b];
+      }
+      sc.prefix = P | (static_cast<uint64_t>(b) << sh);
+      sc.need = need - c;
+    }
+    __syncthreads();
+    P = sc.prefix;
+    need = sc.need;
+  }
+  return P;
+}
+
+// LDS bytes row_cutoff needs for a row of V entries.
+__host__ __device__ __forceinline__ size_t cutoff_lds_bytes(int V) {
+  return (static_cast<size_t>(V) + (V + 31) / 32) * sizeof(uint32_t);
+}
+
+// Top-k / nucleus cut-off of one row whose probabilities are pf(i), i < V,
+// applied in that order: top-k keeps the top_k highest keys (1 <= top_k <
+// V), nucleus then keeps the shortest prefix of the ranking among those
+// whose weight total reaches floor(floor(top_p 2^24) W_k / 2^24) (top_p <
+// 1), at least one entry. Sets st.tau to the smallest kept key and
+// st.s = fp32(S) 2^-32 for the kept weight total S (0, i.e. unmodified, if
+// S == 0). Block-wide; lds holds cutoff_lds_bytes(V) bytes.
+template <class PF>
+__device__ __forceinline__ void row_cutoff(PF pf, int V, int top_k, float top_p, RowStat& st, CutScratch& sc,
+                                           uint32_t* lds) {
+  RowKeys rk{lds, lds + V, V};
+  for (int j = threadIdx.x; j < (V + 31) / 32; j += blockDim.x) rk.big[j] = 0;
+  __syncthreads();
+  const int bd = blockDim.x;
+  for (int base = 0; base < V; base += 8 * bd) {
+    float x[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) x[k] = pf(min(base + k * bd + static_cast<int>(threadIdx.x), V - 1));
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int i = base + k * bd + threadIdx.x;
+      const uint64_t w = fixed_weight(x[k]);
+      if (i < V) {
+        rk.wl[i] = static_cast<uint32_t>(w);
+        if (w >> 32) atomicOr(&rk.big[i >> 5], 1u << (i & 31));
+      }
+    }
+  }
+  __syncthreads();
+  uint64_t tau = 1;
+  if (top_k >= 1 && top_k < V) tau = radix_select<false>(rk, 1, static_cast<uint64_t>(top_k), sc);
+  if (top_p < 1.f) {
+    const uint64_t target = grid_threshold(top_p, kept_weight(rk, tau, sc));
+    const uint64_t tp = target == 0 ? radix_select<false>(rk, tau, 1, sc) : radix_select<true>(rk, tau, target, sc);
+    tau = tp > tau ? tp : tau;
+  }
+  const uint64_t S = kept_weight(rk, tau, sc);
+  st.tau = tau;
+  st.s = S == 0 ? 0.f : __ull2float_rn(S) * 2.3283064365386963e-10f;   // * 2^-32, exact
+}
+
+// Whether the modifiers change a row (greedy rows are never modified).
+__device__ __forceinline__ bool modifiers_active(float temperature, int top_k, float top_p, int V) {
+  return temperature > 0.f && ((top_k >= 1 && top_k < V) || top_p < 1.f);
+}
+
+// pr[i] = prob_final(z[i]) for the whole row, 8 loads per thread in flight.
+__device__ __forceinline__ void write_probs(const float* __restrict__ z, int V, const RowStat& st, float inv_t,
                                             float* __restrict__ pr) {
   const int bd = blockDim.x;
   for (int base = 0; base < V; base += 8 * bd) {
@@ -143,44 +317,29 @@ __device__ __forceinline__ void write_probs(const float* __restrict__ z, int V, 
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const int i = base + k * bd + threadIdx.x;
-      if (i < V) pr[i] = prob_of(zz[k], st, inv_t, i);
+      if (i < V) pr[i] = prob_final(zz[k], st, inv_t, i);
     }
   }
 }
 
 __global__ __launch_bounds__(kSampleThreads) void row_softmax_kernel(const float* __restrict__ logits, int V,
-                                                                     float temperature, RowStat* __restrict__ stats,
+                                                                     float temperature, int top_k, float top_p,
+                                                                     RowStat* __restrict__ stats,
                                                                      float* __restrict__ probs) {
   __shared__ float red[32];
   __shared__ int ired[16];
+  __shared__ CutScratch sc;
+  extern __shared__ uint32_t s_rowkeys[];
   const int row = blockIdx.x;
   const float* z = logits + static_cast<size_t>(row) * V;
-  const RowStat st = row_stat(z, V, temperature, red, ired);
+  RowStat st = row_stat(z, V, temperature, red, ired);
+  const float inv_t = temperature == 0.f ? 0.f : 1.0f / temperature;
+  if (modifiers_active(temperature, top_k, top_p, V)) {
+    const RowStat base = st;
+    row_cutoff([&](int i) { return prob_of(z[i], base, inv_t, i); }, V, top_k, top_p, st, sc, s_rowkeys);
+  }
   if (threadIdx.x == 0 && stats) stats[row] = st;
-  if (probs) {
-    const float inv_t = temperature == 0.f ? 0.f : 1.0f / temperature;
-    write_probs(z, V, st, inv_t, probs + static_cast<size_t>(row) * V);
-  }
-}
-
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
-  const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), o);
-  const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), o);
-  return (static_cast<uint64_t>(hi) << 32) | lo;
-}
-__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += shfl_xor_u64(v, o);
-  return v;
-}
-__device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint64_t o = shfl_up_u64(v, d);
-    if (lane >= d) v += o;
-  }
-  return v;
+  if (probs) write_probs(z, V, st, inv_t, probs + static_cast<size_t>(row) * V);
 }
 
 // Segment [b0, b1) of the vocabulary owned by this wave: a multiple of 64
@@ -291,7 +450,7 @@ struct QLogits {
     const float* z;
     RowStat st;
     float inv_t;
-    __device__ float operator()(int i) const { return prob_of(z[i], st, inv_t, i); }
+    __device__ float operator()(int i) const { return prob_final(z[i], st, inv_t, i); }
   };
   __device__ Row row(int r) const { return Row{z + static_cast<size_t>(r) * V, st[r], inv_t}; }
 };
@@ -358,19 +517,26 @@ __global__ __launch_bounds__(kSampleThreads) void accept_kernel(QS qs, const flo
 // Draft step t: p_t = softmax(logits of the last row of each sequence / T),
 // written to p_out[b][t][:], and x~_{t+1} drawn from it into tokens[b][t+1].
 __global__ __launch_bounds__(kSampleThreads) void draft_sample_kernel(
-    const float* __restrict__ logits, int Mps, int V, float temperature, float* __restrict__ p_out, int K, int t,
-    int32_t* __restrict__ tokens, const int32_t* __restrict__ ctx, uint64_t seed, uint64_t loop, int* err) {
+    const float* __restrict__ logits, int Mps, int V, float temperature, int top_k, float top_p,
+    float* __restrict__ p_out, int K, int t, int32_t* __restrict__ tokens, const int32_t* __restrict__ ctx,
+    uint64_t seed, uint64_t loop, int* err) {
   __shared__ float red[32];
   __shared__ int ired[16];
   __shared__ uint64_t wsum[17];
   __shared__ int s_y;
+  __shared__ CutScratch sc;
+  extern __shared__ uint32_t s_rowkeys[];
   const int b = blockIdx.x, tid = threadIdx.x;
   const float* z = logits + (static_cast<size_t>(b) * Mps + Mps - 1) * V;
-  const RowStat st = row_stat(z, V, temperature, red, ired);
+  RowStat st = row_stat(z, V, temperature, red, ired);
   const float inv_t = temperature == 0.f ? 0.f : 1.0f / temperature;
+  if (modifiers_active(temperature, top_k, top_p, V)) {
+    const RowStat base = st;
+    row_cutoff([&](int i) { return prob_of(z[i], base, inv_t, i); }, V, top_k, top_p, st, sc, s_rowkeys);
+  }
   write_probs(z, V, st, inv_t, p_out + (static_cast<size_t>(b) * K + t) * V);
   const Segment sg = wave_segment(V);
-  auto wp = [&](int i) -> uint64_t { return fixed_weight(prob_of(z[i], st, inv_t, i)); };
+  auto wp = [&](int i) -> uint64_t { return fixed_weight(prob_final(z[i], st, inv_t, i)); };
   int y = block_draw(wp, sg, segment_total(wp, sg), philox_uniform(seed, loop, 0, b, t), wsum, &s_y);
   if (y < 0) {
     y = 0;
@@ -409,11 +575,33 @@ __global__ void philox_kernel(uint64_t seed, uint64_t loop, int purpose, int B, 
                           static_cast<uint32_t>(i % n));
 }
 
-hipError_t launch_row_softmax(const float* logits, int rows, int V, float temperature, float* stats, float* probs,
-                              hipStream_t st) {
+// Dynamic LDS of a sampling launch: the cut-off's row weights when a
+// modifier is on (above the default 64 KiB limit the kernel is opted in
+// once per process to the CU's full LDS).
+static hipError_t cutoff_lds(const void* kernel, float temperature, int top_k, float top_p, int V, size_t* bytes) {
+  const bool on = temperature > 0.f && ((top_k >= 1 && top_k < V) || top_p < 1.f);
+  *bytes = on ? (cutoff_lds_bytes(V) + 15) / 16 * 16 : 0;
+  if (*bytes > 65536) {
+    static bool opted[2] = {false, false};
+    const int which = kernel == reinterpret_cast<const void*>(&row_softmax_kernel) ? 0 : 1;
+    if (!opted[which]) {
+      const hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 140 * 1024);
+      if (e != hipSuccess) return e;
+      opted[which] = true;
+    }
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_row_softmax(const float* logits, int rows, int V, float temperature, int top_k, float top_p,
+                              void* stats, float* probs, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(row_softmax_kernel, dim3(rows), dim3(kSampleThreads), 0, st, logits, V, temperature,
-                     reinterpret_cast<RowStat*>(stats), probs);
+  size_t lds = 0;
+  const hipError_t e = cutoff_lds(reinterpret_cast<const void*>(&row_softmax_kernel), temperature, top_k, top_p, V,
+                                  &lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(row_softmax_kernel, dim3(rows), dim3(kSampleThreads), lds, st, logits, V, temperature, top_k,
+                     top_p, reinterpret_cast<RowStat*>(stats), probs);
   return hipGetLastError();
 }
 
@@ -425,7 +613,7 @@ hipError_t launch_accept_probs(const float* p, const float* q, const int32_t* dr
   return hipGetLastError();
 }
 
-hipError_t launch_accept_logits(const float* p, const float* logits, const float* stats, float temperature,
+hipError_t launch_accept_logits(const float* p, const float* logits, const void* stats, float temperature,
                                 const int32_t* tokens, const float* unif, uint64_t seed, uint64_t loop, int B,
                                 int K, int V, int32_t* out, int32_t* n_acc, int* err, hipStream_t st) {
   const float inv_t = temperature == 0.f ? 0.f : 1.0f / temperature;
@@ -435,11 +623,15 @@ hipError_t launch_accept_logits(const float* p, const float* logits, const float
   return hipGetLastError();
 }
 
-hipError_t launch_draft_sample(const float* logits, int Mps, int B, int V, float temperature, float* p_out, int K,
-                               int t, int32_t* tokens, const int32_t* ctx, uint64_t seed, uint64_t loop, int* err,
-                               hipStream_t st) {
-  hipLaunchKernelGGL(draft_sample_kernel, dim3(B), dim3(kSampleThreads), 0, st, logits, Mps, V, temperature, p_out,
-                     K, t, tokens, ctx, seed, loop, err);
+hipError_t launch_draft_sample(const float* logits, int Mps, int B, int V, float temperature, int top_k,
+                               float top_p, float* p_out, int K, int t, int32_t* tokens, const int32_t* ctx,
+                               uint64_t seed, uint64_t loop, int* err, hipStream_t st) {
+  size_t lds = 0;
+  const hipError_t e = cutoff_lds(reinterpret_cast<const void*>(&draft_sample_kernel), temperature, top_k, top_p, V,
+                                  &lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(draft_sample_kernel, dim3(B), dim3(kSampleThreads), lds, st, logits, Mps, V, temperature, top_k,
+                     top_p, p_out, K, t, tokens, ctx, seed, loop, err);
   return hipGetLastError();
 }
 
@@ -467,5 +659,9 @@ hipError_t launch_philox(uint64_t seed, uint64_t loop, int purpose, int B, int n
                      purpose, B, n, out);
   return hipGetLastError();
 }
+
+size_t row_stat_bytes() { return sizeof(RowStat); }
+
+int modifier_max_vocab() { return kPerLane * kSampleThreads; }
 
 }  // namespace sps

@@ -110,10 +110,19 @@ WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
   w.ss_a = o; o = align256(o + ng * M * 4);               // per-group sums of squares of h
   w.ss_b = o; o = align256(o + ng * M * 4);
   w.logits = o; o = align256(o + M * L.V * 4);
-  w.stats = o; o = align256(o + M * 2 * 4);
+  w.stats = o; o = align256(o + M * sps::row_stat_bytes());
   w.gpart = o; o = align256(o + part);
   w.total = o;
   return w;
+}
+
+// Host-side check of the sampling parameters for a vocabulary of V.
+sps_status check_sampling(const sps_sampling& sp, int V) {
+  if (!(sp.temperature >= 0.f) || sp.temperature > 1e30f) return SPS_E_INVALID;
+  if (sp.top_k < 0 || !(sp.top_p >= 0.f && sp.top_p <= 1.f)) return SPS_E_INVALID;
+  const bool mod = sp.temperature > 0.f && ((sp.top_k >= 1 && sp.top_k < V) || sp.top_p < 1.f);
+  if (mod && V > sps::modifier_max_vocab()) return SPS_E_UNSUPPORTED;
+  return SPS_OK;
 }
 
 int* device_error_ptr() {
@@ -326,7 +335,7 @@ const char* sps_status_string(int32_t status) {
   }
 }
 
-int32_t sps_abi_version(void) { return 1; }
+int32_t sps_abi_version(void) { return 2; }
 
 size_t sps_weight_bytes(const sps_config* cfg) { return valid_config(cfg) ? make_layout(cfg).total : 0; }
 
@@ -476,12 +485,14 @@ sps_status sps_forward(sps_model_t model, sps_kv_t kv, const int32_t* tokens, in
 }
 
 sps_status sps_verify_step(sps_model_t target, sps_kv_t kv, const int32_t* tokens, int32_t B, int32_t K,
-                           float temperature, float* logits_out, float* q_out, const sps_accept_io* acc,
+                           sps_sampling sampling, float* logits_out, float* q_out, const sps_accept_io* acc,
                            void* workspace, size_t ws_bytes, void* stream) {
   if (K < 0 || K > kMaxK) return SPS_E_INVALID;
-  if (!(temperature >= 0.f) || temperature > 1e30f) return SPS_E_INVALID;
+  if (!target) return SPS_E_INVALID;
+  sps_status s = check_sampling(sampling, target->cfg.vocab);
+  if (s != SPS_OK) return s;
   WsLayout ws;
-  sps_status s = check_forward_args(target, kv, B, K + 1, ws_bytes, workspace, &ws);
+  s = check_forward_args(target, kv, B, K + 1, ws_bytes, workspace, &ws);
   if (s != SPS_OK) return s;
   if (!tokens) return SPS_E_INVALID;
   if (acc && (!acc->out_tokens || !acc->n_accepted || (K > 0 && !acc->p_draft))) return SPS_E_INVALID;
@@ -489,15 +500,17 @@ sps_status sps_verify_step(sps_model_t target, sps_kv_t kv, const int32_t* token
   if (!err) return SPS_E_HIP;
   char* base = static_cast<char*>(workspace);
   float* logits = logits_out ? logits_out : reinterpret_cast<float*>(base + ws.logits);
-  float* stats = reinterpret_cast<float*>(base + ws.stats);
+  void* stats = base + ws.stats;
   const hipStream_t st = as_stream(stream);
   s = forward_impl(target, kv, tokens, K + 1, B, K + 1, 0, logits, base, ws, err, st);
   if (s != SPS_OK) return s;
   const int V = target->cfg.vocab;
-  SPS_HIP(sps::launch_row_softmax(logits, B * (K + 1), V, temperature, stats, q_out, st));
+  SPS_HIP(sps::launch_row_softmax(logits, B * (K + 1), V, sampling.temperature, sampling.top_k, sampling.top_p,
+                                  stats, q_out, st));
   if (acc)
-    SPS_HIP(sps::launch_accept_logits(acc->p_draft, logits, stats, temperature, tokens, acc->uniforms, acc->rng.seed,
-                                      acc->rng.loop, B, K, V, acc->out_tokens, acc->n_accepted, err, st));
+    SPS_HIP(sps::launch_accept_logits(acc->p_draft, logits, stats, sampling.temperature, tokens, acc->uniforms,
+                                      acc->rng.seed, acc->rng.loop, B, K, V, acc->out_tokens, acc->n_accepted, err,
+                                      st));
   return SPS_OK;
 }
 
@@ -515,13 +528,14 @@ sps_status sps_accept_resample(const float* p_draft, const float* q_target, cons
 }
 
 sps_status sps_draft_step(sps_model_t draft, sps_kv_t kv, const int32_t* ctx, int32_t B, int32_t K,
-                          float temperature, sps_philox rng, int32_t* tokens, float* p_out, void* workspace,
+                          sps_sampling sampling, sps_philox rng, int32_t* tokens, float* p_out, void* workspace,
                           size_t ws_bytes, void* stream) {
   if (K < 0 || K > kMaxK) return SPS_E_INVALID;
-  if (!(temperature >= 0.f) || temperature > 1e30f) return SPS_E_INVALID;
-  if (!ctx || !tokens || (K > 0 && !p_out)) return SPS_E_INVALID;
+  if (!draft || !ctx || !tokens || (K > 0 && !p_out)) return SPS_E_INVALID;
+  sps_status s = check_sampling(sampling, draft->cfg.vocab);
+  if (s != SPS_OK) return s;
   WsLayout ws;
-  sps_status s = check_forward_args(draft, kv, B, 2, ws_bytes, workspace, &ws);
+  s = check_forward_args(draft, kv, B, 2, ws_bytes, workspace, &ws);
   if (s != SPS_OK) return s;
   int* err = device_error_ptr();
   if (!err) return SPS_E_HIP;
@@ -539,8 +553,8 @@ sps_status sps_draft_step(sps_model_t draft, sps_kv_t kv, const int32_t* ctx, in
     else
       s = forward_impl(draft, kv, tokens + t, K + 1, B, 1, t, logits, base, ws, err, st);
     if (s != SPS_OK) return s;
-    SPS_HIP(sps::launch_draft_sample(logits, t == 0 ? 2 : 1, B, V, temperature, p_out, K, t, tokens, ctx, rng.seed,
-                                     rng.loop, err, st));
+    SPS_HIP(sps::launch_draft_sample(logits, t == 0 ? 2 : 1, B, V, sampling.temperature, sampling.top_k,
+                                     sampling.top_p, p_out, K, t, tokens, ctx, rng.seed, rng.loop, err, st));
   }
   return SPS_OK;
 }
@@ -563,10 +577,13 @@ sps_status sps_philox_uniforms(sps_philox rng, int32_t purpose, int32_t B, int32
   return SPS_OK;
 }
 
-sps_status sps_softmax(const float* logits, int32_t rows, int32_t V, float temperature, float* probs, void* stream) {
-  if (!logits || !probs || rows < 0 || V < 2) return SPS_E_INVALID;
-  if (!(temperature >= 0.f) || temperature > 1e30f) return SPS_E_INVALID;
-  SPS_HIP(sps::launch_row_softmax(logits, rows, V, temperature, nullptr, probs, as_stream(stream)));
+sps_status sps_softmax(const float* logits, int32_t rows, int32_t V, sps_sampling sampling, float* probs,
+                       void* stream) {
+  if (!logits || !probs || rows < 0 || V < 2 || V >= (1 << 24)) return SPS_E_INVALID;
+  const sps_status s = check_sampling(sampling, V);
+  if (s != SPS_OK) return s;
+  SPS_HIP(sps::launch_row_softmax(logits, rows, V, sampling.temperature, sampling.top_k, sampling.top_p, nullptr,
+                                  probs, as_stream(stream)));
   return SPS_OK;
 }
 

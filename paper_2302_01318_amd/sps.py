@@ -39,6 +39,15 @@ class Philox(ctypes.Structure):
     _fields_ = [("seed", c_uint64), ("loop", c_uint64)]
 
 
+class Sampling(ctypes.Structure):
+    """Temperature, top-k and nucleus parameters (sps_sampling)."""
+    _fields_ = [("temperature", c_float), ("top_k", c_int32), ("top_p", c_float)]
+
+
+def sampling_of(temperature, top_k=0, top_p=1.0):
+    return Sampling(float(temperature), int(top_k), float(top_p))
+
+
 class AcceptIO(ctypes.Structure):
     _fields_ = [("p_draft", c_void_p), ("uniforms", c_void_p), ("rng", Philox),
                 ("out_tokens", c_void_p), ("n_accepted", c_void_p)]
@@ -65,13 +74,13 @@ _sig("sps_kv_write", c_int32, [P, c_int32, c_int32, c_int32, c_int32, P, P, P])
 _sig("sps_kv_read", c_int32, [P, c_int32, c_int32, c_int32, c_int32, P, P, P])
 _sig("sps_workspace_bytes", c_size_t, [ctypes.POINTER(Config), c_int32, c_int32, c_int32])
 _sig("sps_forward", c_int32, [P, P, P, c_int32, c_int32, c_int32, c_int32, P, P, c_size_t, P])
-_sig("sps_verify_step", c_int32, [P, P, P, c_int32, c_int32, c_float, P, P, ctypes.POINTER(AcceptIO), P,
+_sig("sps_verify_step", c_int32, [P, P, P, c_int32, c_int32, Sampling, P, P, ctypes.POINTER(AcceptIO), P,
                                   c_size_t, P])
 _sig("sps_accept_resample", c_int32, [P, P, P, P, Philox, c_int32, c_int32, c_int32, P, P, P])
-_sig("sps_draft_step", c_int32, [P, P, P, c_int32, c_int32, c_float, Philox, P, P, P, c_size_t, P])
+_sig("sps_draft_step", c_int32, [P, P, P, c_int32, c_int32, Sampling, Philox, P, P, P, c_size_t, P])
 _sig("sps_commit", c_int32, [P, P, P, P, c_int32, c_int32, P, P, P, c_int32, P])
 _sig("sps_philox_uniforms", c_int32, [Philox, c_int32, c_int32, c_int32, P, P])
-_sig("sps_softmax", c_int32, [P, c_int32, c_int32, c_float, P, P])
+_sig("sps_softmax", c_int32, [P, c_int32, c_int32, Sampling, P, P])
 _sig("sps_device_error", c_int32, [P, c_int32, ctypes.POINTER(c_int32)])
 _sig("sps_profile_gemm_begin", c_int32, [c_int32])
 _sig("sps_profile_gemm_end", c_int32, [ctypes.POINTER(c_float), ctypes.POINTER(c_int32),
@@ -202,14 +211,14 @@ def forward(model, kv, tokens, M, pos_offset=0, logits=None, ws=None, tok_stride
 
 
 def verify_step(model, kv, tokens, K, temperature, ws, logits=None, q=None, p_draft=None, uniforms=None,
-                rng=(0, 0), out_tokens=None, n_accepted=None):
+                rng=(0, 0), out_tokens=None, n_accepted=None, top_k=0, top_p=1.0):
     acc = None
     if out_tokens is not None:
         acc = AcceptIO(_ptr(p_draft, torch.float32, "p_draft"), _ptr(uniforms, torch.float32, "uniforms"),
                        Philox(*rng), _ptr(out_tokens, torch.int32, "out_tokens"),
                        _ptr(n_accepted, torch.int32, "n_accepted"))
     check(lib.sps_verify_step(model.handle, kv.handle, _ptr(tokens, torch.int32, "tokens"), kv.B, K,
-                              float(temperature), _ptr(logits, torch.float32, "logits"),
+                              sampling_of(temperature, top_k, top_p), _ptr(logits, torch.float32, "logits"),
                               _ptr(q, torch.float32, "q"), ctypes.byref(acc) if acc else None, _ptr(ws),
                               ws.numel(), _stream()), "sps_verify_step")
 
@@ -231,8 +240,9 @@ def accept_resample(p_draft, q_target, draft_tokens, uniforms=None, rng=(0, 0), 
     return out_tokens, n_accepted
 
 
-def draft_step(model, kv, ctx, K, temperature, rng, tokens, p_out, ws):
-    check(lib.sps_draft_step(model.handle, kv.handle, _ptr(ctx, torch.int32, "ctx"), kv.B, K, float(temperature),
+def draft_step(model, kv, ctx, K, temperature, rng, tokens, p_out, ws, top_k=0, top_p=1.0):
+    check(lib.sps_draft_step(model.handle, kv.handle, _ptr(ctx, torch.int32, "ctx"), kv.B, K,
+                             sampling_of(temperature, top_k, top_p),
                              Philox(*rng), _ptr(tokens, torch.int32, "tokens"), _ptr(p_out, torch.float32, "p_out"),
                              _ptr(ws), ws.numel(), _stream()), "sps_draft_step")
 
@@ -249,10 +259,11 @@ def philox_uniforms(seed, loop, purpose, B, n, device="cuda"):
     return out
 
 
-def softmax(logits, temperature):
+def softmax(logits, temperature, top_k=0, top_p=1.0):
     rows, V = logits.reshape(-1, logits.shape[-1]).shape
     out = torch.empty_like(logits)
-    check(lib.sps_softmax(_ptr(logits, torch.float32, "logits"), rows, V, float(temperature), _ptr(out),
+    check(lib.sps_softmax(_ptr(logits, torch.float32, "logits"), rows, V, sampling_of(temperature, top_k, top_p),
+                          _ptr(out),
                           _stream()), "sps_softmax")
     return out
 
@@ -313,25 +324,26 @@ class Generator:
         self.lengths.fill_(Pn - 1)
         self.ctx.copy_(prompt[:, Pn - 2:Pn])
 
-    def loop(self, temperature, seed, loop_index, seq_out=None, n_out=None, cap=0):
+    def loop(self, temperature, seed, loop_index, seq_out=None, n_out=None, cap=0, top_k=0, top_p=1.0):
         K = self.K
         rng = (seed, loop_index)
         if self.draft is not None and K > 0:
-            draft_step(self.draft, self.kv_d, self.ctx, K, temperature, rng, self.tokens, self.p, self.ws_d)
+            draft_step(self.draft, self.kv_d, self.ctx, K, temperature, rng, self.tokens, self.p, self.ws_d,
+                       top_k, top_p)
         else:
             check(lib.sps_draft_step(self.target.handle, self.kv_t.handle, _ptr(self.ctx), self.B, 0,
-                                     float(temperature), Philox(*rng), _ptr(self.tokens), None, _ptr(self.ws_t),
-                                     self.ws_t.numel(), _stream()), "sps_draft_step(K=0)")
+                                     sampling_of(temperature, top_k, top_p), Philox(*rng), _ptr(self.tokens), None,
+                                     _ptr(self.ws_t), self.ws_t.numel(), _stream()), "sps_draft_step(K=0)")
         verify_step(self.target, self.kv_t, self.tokens, K, temperature, self.ws_t, p_draft=self.p if K else None,
-                    rng=rng, out_tokens=self.out, n_accepted=self.n_acc)
+                    rng=rng, out_tokens=self.out, n_accepted=self.n_acc, top_k=top_k, top_p=top_p)
         commit(self.kv_t, self.tokens, self.out, self.n_acc, K, self.ctx, seq_out, n_out, cap)
 
-    def generate(self, prompt, n_new, temperature, seed, accepted_log=None):
+    def generate(self, prompt, n_new, temperature, seed, accepted_log=None, top_k=0, top_p=1.0):
         """Prefill, then run(); returns [B][n_new] int32 tokens (device)."""
         self.prefill(prompt)
-        return self.run(n_new, temperature, seed, accepted_log)
+        return self.run(n_new, temperature, seed, accepted_log, top_k, top_p)
 
-    def run(self, n_new, temperature, seed, accepted_log=None):
+    def run(self, n_new, temperature, seed, accepted_log=None, top_k=0, top_p=1.0):
         """SpS loops until every sequence has n_new tokens. The host looks at
         the device-side output counts only between bursts of loops: every
         loop emits at most K + 1 tokens, so ceil(remaining / (K + 1)) loops
@@ -348,7 +360,7 @@ class Generator:
                 break
             for _ in range(max(1, -(-remaining // (self.K + 1)))):
                 done = (n_out >= n_new).clone() if accepted_log is not None else None
-                self.loop(temperature, seed, loop_index, seq, n_out, n_new)
+                self.loop(temperature, seed, loop_index, seq, n_out, n_new, top_k, top_p)
                 if accepted_log is not None:
                     accepted_log.append((self.n_acc.clone(), done))
                 loop_index += 1

@@ -37,7 +37,7 @@ def test_every_declared_function_is_exported(sps):
 def test_status_strings(sps):
     assert sps.lib.sps_status_string(0) == b"ok"
     assert sps.lib.sps_status_string(5) == b"HIP runtime error"
-    assert sps.lib.sps_abi_version() == 1
+    assert sps.lib.sps_abi_version() == 2
 
 
 def test_config_validation_and_sizes(sps):
@@ -68,13 +68,21 @@ def test_invalid_arguments_return_codes(sps):
     assert sps.lib.sps_accept_resample(None, one, one, None, Ph, 1, 2, 10, one, one, None) == 1
     # forward / verify / draft / commit with null handles
     assert sps.lib.sps_forward(None, None, one, 5, 1, 5, 0, None, one, 1 << 30, None) == 1
-    assert sps.lib.sps_verify_step(None, None, one, 1, 4, 1.0, None, None, None, one, 1 << 30, None) == 1
-    assert sps.lib.sps_verify_step(None, None, one, 1, -1, 1.0, None, None, None, one, 1 << 30, None) == 1
-    assert sps.lib.sps_draft_step(None, None, one, 1, 4, -1.0, Ph, one, one, one, 1 << 30, None) == 1
+    S = sps.sampling_of
+    assert sps.lib.sps_verify_step(None, None, one, 1, 4, S(1.0), None, None, None, one, 1 << 30, None) == 1
+    assert sps.lib.sps_verify_step(None, None, one, 1, -1, S(1.0), None, None, None, one, 1 << 30, None) == 1
+    assert sps.lib.sps_draft_step(None, None, one, 1, 4, S(-1.0), Ph, one, one, one, 1 << 30, None) == 1
     assert sps.lib.sps_commit(None, one, one, one, 1, 4, one, None, None, 0, None) == 1
     assert sps.lib.sps_pack_weight(None, 0, 0, one, one, None) == 2
     assert sps.lib.sps_philox_uniforms(Ph, 0, 1, 1, None, None) == 1
-    assert sps.lib.sps_softmax(one, 1, 1, 1.0, one, None) == 1
+    assert sps.lib.sps_softmax(one, 1, 1, S(1.0), one, None) == 1
+    # sampling parameters: negative top_k, top_p outside [0, 1] or NaN; modifiers beyond the supported vocabulary
+    assert sps.lib.sps_softmax(one, 1, 1000, S(1.0, -1, 1.0), one, None) == 1
+    assert sps.lib.sps_softmax(one, 1, 1000, S(1.0, 0, 1.5), one, None) == 1
+    assert sps.lib.sps_softmax(one, 1, 1000, S(1.0, 0, float("nan")), one, None) == 1
+    assert sps.lib.sps_softmax(one, 1, 1000, S(float("inf")), one, None) == 1
+    assert sps.lib.sps_softmax(one, 1, 40000, S(1.0, 5, 1.0), one, None) == 4
+    assert sps.lib.sps_softmax(one, 1, 40000, S(1.0, 0, 0.9), one, None) == 4
     assert sps.lib.sps_device_error(None, 0, None) == 1
 
 
