@@ -259,6 +259,9 @@ def main():
     ap.add_argument("--no-e2e", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--temperature", type=float, default=1.0)
+    ap.add_argument("--top-k", type=int, default=0, help="top-k modifier of p and q (0: off)")
+    ap.add_argument("--top-p", type=float, default=1.0, help="nucleus modifier of p and q (1: off)")
     ap.add_argument("--sweep", action="store_true", help="70B verify over K, B, ctx (+ accept-stage projection)")
     ap.add_argument("--accept-grid", action="store_true", help="accept/resample alone over the B x K grid")
     ap.add_argument("--no-roofline-pass", action="store_true",
@@ -309,9 +312,11 @@ def main():
     out = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
     nacc = torch.empty(B, dtype=torch.int32, device="cuda")
 
+    T, top_k, top_p = args.temperature, args.top_k, args.top_p
+
     def step(i):
-        sps.verify_step(target, kv, tokens, K, 1.0, ws, p_draft=p, rng=(args.seed, i), out_tokens=out,
-                        n_accepted=nacc)
+        sps.verify_step(target, kv, tokens, K, T, ws, p_draft=p, rng=(args.seed, i), out_tokens=out,
+                        n_accepted=nacc, top_k=top_k, top_p=top_p)
 
     for i in range(args.warmup):
         step(i)
@@ -360,7 +365,7 @@ def main():
             torch.cuda.synchronize()
             acc_log = []
             t0 = time.perf_counter()
-            g.run(args.n_new, 1.0, args.seed, accepted_log=acc_log)
+            g.run(args.n_new, T, args.seed, accepted_log=acc_log, top_k=top_k, top_p=top_p)
             torch.cuda.synchronize()
             dt = time.perf_counter() - t0
             accs = [int(a[0]) for a, done in acc_log if not bool(done[0])]
@@ -379,7 +384,8 @@ def main():
         "data": "synthetic: random-init weights N(0,0.02), random bf16 prior KV, random tokens and draft "
                 "distributions",
         "config": {"workload": "%s-shaped target verify step + softmax + fused accept/resample" % shape.name,
-                   "K": K, "batch": B, "ctx": ctx, "bytes_per_step": nbytes,
+                   "K": K, "batch": B, "ctx": ctx, "temperature": T, "top_k": top_k, "top_p": top_p,
+                   "bytes_per_step": nbytes,
                    "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)},
         "verify_ms": round(ms, 4),
     }
@@ -388,7 +394,8 @@ def main():
     if e2e:
         result["sps_tokens_per_s"] = round(e2e["sps"]["tokens_per_s"], 2)
         result["ars_tokens_per_s"] = round(e2e["ars"]["tokens_per_s"], 2)
-        result["e2e"] = {"draft": dshape.name, "prompt": ctx, "n_new": args.n_new, "K": K, "temperature": 1.0,
+        result["e2e"] = {"draft": dshape.name, "prompt": ctx, "n_new": args.n_new, "K": K, "temperature": T,
+                         "top_k": top_k, "top_p": top_p,
                          "sps_mean_accepted": round(e2e["sps"]["mean_accepted"], 3),
                          "sps_loops": e2e["sps"]["loops"], "ars_loops": e2e["ars"]["loops"],
                          "paper_context": "Chinchilla 70B on 16 TPU v4: ArS 14.1 ms/token, SpS 1.92-2.46x "

@@ -238,15 +238,31 @@ __device__ __forceinline__ uint64_t radix_select(const RowKeys& rk, uint64_t lo,
     zero = wave_sum_u64(zero);
     if ((tid & 63) == 0 && zero) atomicAdd(reinterpret_cast<unsigned long long*>(&sc.hist[0]), zero);
     __syncthreads();
-    if (tid == 0) {
-      uint64_t c = 0;
-      int b = 255;
-      for (; b > 0; --b) {
-        if (c + sc.hist[b] >= need) break;
-        c += sc.hist[b];
+    if (tid < 64) {
+      // Bins from the top: lane l owns bins 255 - 4l .. 252 - 4l. The first
+      // lane whose inclusive total reaches `need` walks its four bins.
+      uint64_t h[4], tot = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        h[j] = sc.hist[255 - 4 * tid - j];
+        tot += h[j];
       }
-      sc.prefix = P | (static_cast<uint64_t>(b) << sh);
-      sc.need = need - c;
+      const uint64_t inc = wave_incl_scan_u64(tot);
+      const uint64_t hit = __ballot(inc >= need);
+      if (tid == __ffsll(static_cast<long long>(hit)) - 1) {
+        uint64_t c = inc - tot;
+        int b = 255 - 4 * tid - 3;
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+          if (c + h[j] >= need) {
+            b = 255 - 4 * tid - j;
+            break;
+          }
+          c += h[j];
+        }
+        sc.prefix = P | (static_cast<uint64_t>(b) << sh);
+        sc.need = need - c;
+      }
     }
     __syncthreads();
     P = sc.prefix;
