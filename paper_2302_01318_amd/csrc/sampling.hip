@@ -86,14 +86,18 @@ __device__ __forceinline__ uint64_t rank_key(uint64_t w, int i) {
   return (w << 24) | static_cast<uint64_t>(0xFFFFFF - i);
 }
 
-// The probability the sampling stages use: prob_of, then the modifiers'
-// cut and renormalisation x / s (branch-free).
+// The probability the sampling stages use: prob_of, then (MOD: the row has
+// a top-k / nucleus cut, st.s > 0) the cut and the renormalisation x / s.
+// Branch-free; callers pick MOD once per row (a uniform branch outside
+// their loops).
+template <bool MOD>
 __device__ __forceinline__ float prob_final(float z, const RowStat& st, float inv_t, int i) {
   const float x = prob_of(z, st, inv_t, i);
+  if (!MOD) return x;
   const bool keep = rank_key(fixed_weight(x), i) >= st.tau;
-  const float y = __fdiv_rn(x, st.s);
-  return st.s > 0.f ? (keep ? y : 0.f) : x;
+  return keep ? __fdiv_rn(x, st.s) : 0.f;
 }
+__device__ __forceinline__ bool row_modified(const RowStat& st) { return st.s > 0.f; }
 
 // red: __shared__ float[32], ired: __shared__ int[16].
 __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, float temperature, float* red,
@@ -323,8 +327,9 @@ __device__ __forceinline__ bool modifiers_active(float temperature, int top_k, f
 }
 
 // pr[i] = prob_final(z[i]) for the whole row, 8 loads per thread in flight.
-__device__ __forceinline__ void write_probs(const float* __restrict__ z, int V, const RowStat& st, float inv_t,
-                                            float* __restrict__ pr) {
+template <bool MOD>
+__device__ __forceinline__ void write_probs_t(const float* __restrict__ z, int V, const RowStat& st, float inv_t,
+                                              float* __restrict__ pr) {
   const int bd = blockDim.x;
   for (int base = 0; base < V; base += 8 * bd) {
     float zz[8];
@@ -333,9 +338,14 @@ __device__ __forceinline__ void write_probs(const float* __restrict__ z, int V, 
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const int i = base + k * bd + threadIdx.x;
-      if (i < V) pr[i] = prob_final(zz[k], st, inv_t, i);
+      if (i < V) pr[i] = prob_final<MOD>(zz[k], st, inv_t, i);
     }
   }
+}
+__device__ __forceinline__ void write_probs(const float* __restrict__ z, int V, const RowStat& st, float inv_t,
+                                            float* __restrict__ pr) {
+  if (row_modified(st)) write_probs_t<true>(z, V, st, inv_t, pr);
+  else write_probs_t<false>(z, V, st, inv_t, pr);
 }
 
 __global__ __launch_bounds__(kSampleThreads) void row_softmax_kernel(const float* __restrict__ logits, int V,
@@ -452,6 +462,8 @@ struct QProbs {
   int V;
   struct Row {
     const float* q;
+    __device__ bool modified() const { return false; }
+    template <bool MOD> __device__ float get(int i) const { return q[i]; }
     __device__ float operator()(int i) const { return q[i]; }
   };
   __device__ Row row(int r) const { return Row{q + static_cast<size_t>(r) * V}; }
@@ -466,10 +478,31 @@ struct QLogits {
     const float* z;
     RowStat st;
     float inv_t;
-    __device__ float operator()(int i) const { return prob_final(z[i], st, inv_t, i); }
+    __device__ bool modified() const { return row_modified(st); }
+    template <bool MOD> __device__ float get(int i) const { return prob_final<MOD>(z[i], st, inv_t, i); }
+    __device__ float operator()(int i) const {
+      return modified() ? get<true>(i) : get<false>(i);
+    }
   };
   __device__ Row row(int r) const { return Row{z + static_cast<size_t>(r) * V, st[r], inv_t}; }
 };
+
+// The final draw of one sequence: from (q - p)_+ if resid (falling back to
+// q when its weights sum to 0), else from q. -1 if q's weights are all 0.
+template <bool MOD, class Row>
+__device__ __forceinline__ int accept_draw(const Row& qr, const float* __restrict__ prow, bool resid, int V,
+                                           float u, uint64_t* wsum, int* s_y) {
+  const Segment sg = wave_segment(V);
+  auto wq = [&](int i) -> uint64_t { return fixed_weight(qr.template get<MOD>(i)); };
+  auto wr = [&](int i) -> uint64_t {
+    const uint64_t x = fixed_weight(qr.template get<MOD>(i)), y = fixed_weight(prow[i]);
+    return x > y ? x - y : 0;
+  };
+  int y = -1;
+  if (resid) y = block_draw(wr, sg, segment_total(wr, sg), u, wsum, s_y);
+  if (y < 0) y = block_draw(wq, sg, segment_total(wq, sg), u, wsum, s_y);
+  return y;
+}
 
 // One block per sequence. drafts[b * dstride + doff + t] is x~_{t+1}.
 template <class QS>
@@ -511,17 +544,10 @@ __global__ __launch_bounds__(kSampleThreads) void accept_kernel(QS qs, const flo
   const float* prow = p + (static_cast<size_t>(b) * K + (resid ? a : 0)) * V;
 
   // 2. draw from (q - p)_+ (or q for the bonus / the zero-residual fallback)
-  const Segment sg = wave_segment(V);
   const typename QS::Row qr = qs.row(row);
-  auto wq = [&](int i) -> uint64_t { return fixed_weight(qr(i)); };
-  auto wr = [&](int i) -> uint64_t {
-    const uint64_t x = fixed_weight(qr(i)), y = fixed_weight(prow[i]);
-    return x > y ? x - y : 0;
-  };
   const float u = unif ? unif[b * (K + 1) + K] : philox_uniform(seed, loop, 2, b, 0);
-  int y = -1;
-  if (resid) y = block_draw(wr, sg, segment_total(wr, sg), u, wsum, &s_y);
-  if (y < 0) y = block_draw(wq, sg, segment_total(wq, sg), u, wsum, &s_y);
+  int y = qr.modified() ? accept_draw<true>(qr, prow, resid, V, u, wsum, &s_y)
+                        : accept_draw<false>(qr, prow, resid, V, u, wsum, &s_y);
   if (y < 0) {
     y = 0;
     if (tid == 0) atomicOr(err, kErrEmpty);
@@ -550,9 +576,13 @@ __global__ __launch_bounds__(kSampleThreads) void draft_sample_kernel(
     const RowStat base = st;
     row_cutoff([&](int i) { return prob_of(z[i], base, inv_t, i); }, V, top_k, top_p, st, sc, s_rowkeys);
   }
-  write_probs(z, V, st, inv_t, p_out + (static_cast<size_t>(b) * K + t) * V);
+  // p_t once into p_out, then the draw from the stored values (visible to
+  // the whole block after the barrier).
+  float* pr = p_out + (static_cast<size_t>(b) * K + t) * V;
+  write_probs(z, V, st, inv_t, pr);
+  __syncthreads();
   const Segment sg = wave_segment(V);
-  auto wp = [&](int i) -> uint64_t { return fixed_weight(prob_final(z[i], st, inv_t, i)); };
+  auto wp = [&](int i) -> uint64_t { return fixed_weight(pr[i]); };
   int y = block_draw(wp, sg, segment_total(wp, sg), philox_uniform(seed, loop, 0, b, t), wsum, &s_y);
   if (y < 0) {
     y = 0;
