@@ -178,9 +178,8 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
 
 // Launch shape for one launch: n-tiles per wave, waves per work-group, k-tiles
 // per chunk. A single M tile (every verify and draft step) streams two n-tiles
-// per wave with 8-wave work-groups when there are enough output tiles to fill
-// the GPU, else one n-tile per wave with 16-wave work-groups; either way about
-// 24-32 waves per CU keep 8 KiB each in flight.
+// per wave with 8-wave work-groups on large matrices (single_tile_ntw), else
+// one n-tile per wave with 16-wave work-groups.
 template <typename T, int MT, int NTW, int WAVES, int U>
 static hipError_t gemm_launch(const GemmParams& p, hipStream_t st) {
   const dim3 grid((p.NT + NTW - 1) / NTW), block(WAVES * 64);
@@ -194,7 +193,13 @@ static hipError_t gemm_launch(const GemmParams& p, hipStream_t st) {
   return hipGetLastError();
 }
 
-static int single_tile_ntw(int NT) { return (NT % 2 == 0 && NT / 2 >= 512) ? 2 : 1; }
+// Two output tiles per wave (half the activation loads per weight byte, 8
+// waves per work-group) once the matrix is large enough (>= 512 tiles wide,
+// >= ~120 MB of bf16 weights) for 256+ work-groups to stream long enough;
+// smaller matrices keep one tile per wave and 16 waves.
+static int single_tile_ntw(int NT, int KT) {
+  return (NT % 2 == 0 && NT >= 512 && static_cast<long>(NT) * KT >= 120000) ? 2 : 1;
+}
 
 // fp32 models (16-row M tiles) at any row count, bf16 models at <= 8 rows.
 // bf16 launches over more rows go to the wide kernel (gemm_wide.hip).
@@ -202,7 +207,7 @@ static hipError_t gemm_dispatch_f32(const GemmParams& p, hipStream_t st) {
   using T = float;
   const int MT = (p.M + ActRows<T>::kRows - 1) / ActRows<T>::kRows;
   if (MT == 1) {
-    if (p.Mtot <= ActRows<T>::kRows && single_tile_ntw(p.NT) == 2) return gemm_launch<T, 1, 2, 8, 4>(p, st);
+    if (p.Mtot <= ActRows<T>::kRows && single_tile_ntw(p.NT, p.KT) == 2) return gemm_launch<T, 1, 2, 8, 4>(p, st);
     return gemm_launch<T, 1, 1, 16, 4>(p, st);
   }
   switch (MT) {
@@ -221,7 +226,7 @@ static hipError_t gemm_dispatch_bf16(const GemmParams& p, hipStream_t st) {
   using T = bf16;
   if (gemm_is_wide(1, p.Mtot)) return launch_gemm_wide(p, wide_plan(p.NT, p.KT, p.M), st);
   if (p.M > ActRows<T>::kRows) return hipErrorInvalidValue;
-  if (single_tile_ntw(p.NT) == 2) return gemm_launch<T, 1, 2, 8, 4>(p, st);
+  if (single_tile_ntw(p.NT, p.KT) == 2) return gemm_launch<T, 1, 2, 8, 4>(p, st);
   return gemm_launch<T, 1, 1, 16, 4>(p, st);
 }
 
@@ -230,10 +235,10 @@ int gemm_max_rows(int dtype) { return dtype == 1 ? 20 * ActRows<bf16>::kRows : 1
 
 bool gemm_is_wide(int dtype, int Mtot) { return dtype == 1 && Mtot > ActRows<bf16>::kRows; }
 
-int gemm_groups(int dtype, int NT, int Mtot) {
+int gemm_groups(int dtype, int NT, int KT, int Mtot) {
   if (gemm_is_wide(dtype, Mtot)) return wide_groups(NT);
   const int rows = dtype == 1 ? ActRows<bf16>::kRows : ActRows<float>::kRows;
-  const int ntw = (Mtot <= rows) ? single_tile_ntw(NT) : 1;
+  const int ntw = (Mtot <= rows) ? single_tile_ntw(NT, KT) : 1;
   return (NT + ntw - 1) / ntw;
 }
 

@@ -39,7 +39,7 @@ struct GemmParams {
 };
 hipError_t launch_gemm(int dtype, const GemmParams& p, hipStream_t st);
 int gemm_max_rows(int dtype);                 // rows one launch handles
-int gemm_groups(int dtype, int NT, int Mtot); // column groups (ss_out groups) of a GEMM over Mtot rows
+int gemm_groups(int dtype, int NT, int KT, int Mtot); // column groups (ss_out groups) of a GEMM
 
 // Wide GEMM (bf16, more than 8 rows; gemm_wide.hip): M tiles, k-tiles per
 // chunk, column groups, k splits and chunks of one launch.

@@ -270,7 +270,7 @@ sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t*
     p.u = x; p.ldu = L.d; p.uplane = uplane; p.ss_out = ss_nxt; p.epi = sps::kEpiResid;
     s = gemm(dt, p, st);
     if (s != SPS_OK) return s;
-    const int ng_o = sps::gemm_groups(dt, L.d / 16, M);
+    const int ng_o = sps::gemm_groups(dt, L.d / 16, KThd, M);
 
     p = base;                                // W_1: norm scale, GELU / SwiGLU
     p.X = x; p.ldx = L.d; p.xplane = uplane;
@@ -290,7 +290,7 @@ sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t*
     p.u = x; p.ldu = L.d; p.uplane = uplane; p.ss_out = ss_cur; p.epi = sps::kEpiResid;
     s = gemm(dt, p, st);
     if (s != SPS_OK) return s;
-    ng = sps::gemm_groups(dt, L.d / 16, M);
+    ng = sps::gemm_groups(dt, L.d / 16, KTf, M);
   }
   if (logits) {
     GemmParams p = base;                     // final norm scale + unembedding
