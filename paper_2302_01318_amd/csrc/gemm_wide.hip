@@ -42,12 +42,17 @@ template <int MT> constexpr int wide_part_floats() { return kWideNtw * MT * 128;
 template <int MT> constexpr int wide_waves_per_simd() { return MT <= 6 ? 3 : MT <= 12 ? 2 : 1; }
 
 // Accumulate chunks [c0, c1) of column group g into acc, then fold the
-// lo-plane rows (lanes 32-63) into their hi rows (lanes 0-31).
+// lo-plane rows (lanes 32-63) into their hi rows (lanes 0-31). Double
+// buffered: while a chunk's MFMAs run, the next chunk's activation
+// fragments are already on their way into the other LDS buffer (s_a holds
+// 2 * MT * KC fragments) and its weight fragments into the other register
+// set; one barrier per chunk.
 template <int MT, int KC>
 __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0, int c1, bf16x8 (*s_a)[64],
                                               f32x4 (&acc)[kWideNtw][MT]) {
   using T = bf16;
   constexpr int kTile = 512;                       // elements per 16 x 32 tile
+  constexpr int kBuf = MT * KC;                    // fragments per LDS buffer
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ntw = g * kWideNg + wave * kWideNtw;   // first n-tile of this wave
   const int r16 = lane & 15, grp = lane >> 4;
@@ -71,41 +76,66 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int c = c0; c < c1; ++c) {
+  // Activation fragments of chunk c into LDS buffer bb, fragment f = mt * KC + u.
+  auto issue_a = [&](int c, int bb) {
     const int kb = c * KC;
-    // Activation fragments of the chunk into LDS, fragment f = mt * KC + u.
-    for (int f = wave; f < MT * KC; f += kWideWaves) {
+    for (int f = wave; f < kBuf; f += kWideWaves) {
       const int mt = f / KC, u = f % KC;
       if (kb + u < KT) {
         const int m = mt * 8 + arow;
         const T* src = xbase + static_cast<size_t>(p.m0 + (m < M ? m : 0)) * p.ldx + (kb + u) * 32;
-        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src), reinterpret_cast<void*>(&s_a[f][0]),
-                                         16, 0, 0);
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src),
+                                         reinterpret_cast<void*>(&s_a[bb * kBuf + f][0]), 16, 0, 0);
       }
     }
-    Frag<T> b[kWideNtw][KC];
+  };
+  auto load_b = [&](int c, Frag<T> (&b)[kWideNtw][KC]) {
+    const int kb = c * KC;
 #pragma unroll
     for (int j = 0; j < kWideNtw; ++j)
 #pragma unroll
       for (int u = 0; u < KC; ++u)
         b[j][u] = wv[j] && kb + u < KT ? load_frag_stream(wp[j] + static_cast<size_t>(kb + u) * kTile)
                                        : Frag<T>::zero();
-    __builtin_amdgcn_s_waitcnt(0);                 // the LDS copies have landed
-    __syncthreads();
+  };
+  auto compute = [&](int c, int bb, const Frag<T> (&b)[kWideNtw][KC]) {
+    const int kb = c * KC;
 #pragma unroll
     for (int u = 0; u < KC; ++u) {
       if (kb + u < KT) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
           Frag<T> a;
-          a.v = s_a[mt * KC + u][lane];
+          a.v = s_a[bb * kBuf + mt * KC + u][lane];
 #pragma unroll
           for (int j = 0; j < kWideNtw; ++j) acc[j][mt] = mma8(acc[j][mt], a, b[j][u]);
         }
       }
     }
-    __syncthreads();                               // chunk consumed before the next overwrites it
+  };
+  // One chunk: wait for its loads (the only ones outstanding), start the
+  // next chunk's, then multiply. Buffer bb ^ 1 is free: every wave passed
+  // this barrier only after finishing the previous chunk, which used it.
+  auto step = [&](int c, int bb, const Frag<T> (&bcur)[kWideNtw][KC], Frag<T> (&bnext)[kWideNtw][KC]) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (c + 1 < c1) {
+      issue_a(c + 1, bb ^ 1);
+      load_b(c + 1, bnext);
+    }
+    compute(c, bb, bcur);
+  };
+
+  Frag<T> b0[kWideNtw][KC], b1[kWideNtw][KC];
+  if (c0 < c1) {
+    issue_a(c0, 0);
+    load_b(c0, b0);
   }
+  for (int c = c0; c < c1; c += 2) {
+    step(c, 0, b0, b1);
+    if (c + 1 < c1) step(c + 1, 1, b1, b0);
+  }
+  __syncthreads();                                 // LDS free for the caller (epilogue tile)
 #pragma unroll
   for (int j = 0; j < kWideNtw; ++j)
 #pragma unroll
@@ -170,13 +200,15 @@ __device__ __forceinline__ void wide_epilogue(const GemmParams& p, int g, const 
 template <int MT, int KC, int EPI>
 __global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT>())))
 void gemm_wide_kernel(const GemmParams p, int chunks) {
-  __shared__ bf16x8 s_a[MT * KC][64];              // one chunk of activation fragments
-  __shared__ float s_rs[MT * 8];
-  // The epilogue's output tile reuses the chunk buffer, dead after the loop.
-  static_assert(kWideNg * MT * 128 * sizeof(float) <= sizeof(s_a), "output tile must fit the chunk buffer");
+  __shared__ bf16x8 s_a[2 * MT * KC][64];          // two chunks of activation fragments
+  // The epilogue's output tile and row scales reuse the chunk buffers, dead
+  // after the loop.
+  constexpr int kTile = kWideNg * MT * 128;        // floats
+  static_assert((kTile + MT * 8) * sizeof(float) <= sizeof(s_a), "epilogue buffers must fit the chunk buffers");
   f32x4 acc[kWideNtw][MT];
   wide_mainloop<MT, KC>(p, blockIdx.x, 0, chunks, s_a, acc);
-  wide_epilogue<MT, EPI>(p, blockIdx.x, acc, reinterpret_cast<float*>(&s_a[0][0]), s_rs);
+  float* ep = reinterpret_cast<float*>(&s_a[0][0]);
+  wide_epilogue<MT, EPI>(p, blockIdx.x, acc, ep, ep + kTile);
 }
 
 // Split s of column group g (work-group g + s G): chunks [s C / S, (s+1) C / S)
@@ -184,7 +216,7 @@ void gemm_wide_kernel(const GemmParams p, int chunks) {
 template <int MT, int KC>
 __global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT>())))
 void gemm_wide_split_kernel(const GemmParams p, int S, int chunks) {
-  __shared__ bf16x8 s_a[MT * KC][64];
+  __shared__ bf16x8 s_a[2 * MT * KC][64];
   const int G = (p.NT + kWideNg - 1) / kWideNg;
   const int g = blockIdx.x % G, s = blockIdx.x / G;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -234,9 +266,10 @@ __global__ __launch_bounds__(kWideWaves * 64) void gemm_wide_reduce_kernel(const
 // ---------------------------------------------------------------------------
 static const int kWideMT[] = {2, 3, 4, 5, 6, 8, 10, 12, 14, 16, 18, 20};
 
-// k-tiles per chunk: the chunk's MT x KC KiB of LDS leaves room for two to
-// three work-groups per CU and holds the output tile (4 MT KiB).
-static constexpr int wide_kc(int MT) { return MT <= 6 ? 8 : 4; }
+// k-tiles per chunk: the two chunk buffers (2 MT KC KiB of LDS) leave room
+// for two to three work-groups per CU up to 10 M tiles (one above 12, where
+// registers allow one wave per SIMD) and hold the output tile (4 MT KiB).
+static constexpr int wide_kc(int MT) { return MT <= 10 ? 4 : MT == 12 || MT == 20 ? 3 : 4; }
 
 WidePlan wide_plan(int NT, int KT, int M) {
   WidePlan w{};
