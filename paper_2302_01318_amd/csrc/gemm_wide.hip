@@ -144,16 +144,54 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
       for (int r = 0; r < 4; ++r) acc[j][mt][r] += __shfl_xor(acc[j][mt][r], 32);
 }
 
-// Epilogue of column group g from the folded tile in acc. ep is LDS for the
-// group's output tile [8 n-tiles][MT][8 rows][16 columns], s_rs for MT*8
-// row scales.
+// Epilogue of M tiles mt0 .. mt0 + NMT - 1 of column group g. ep holds their
+// output tile in LDS as [8 n-tiles][NMT][8 rows][16 columns]; s_rs is LDS for
+// NMT * 8 row scales.
+template <int NMT, int EPI>
+__device__ __forceinline__ void wide_epilogue_tile(const GemmParams& p, int g, int mt0, float* ep, float* s_rs) {
+  using T = bf16;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int M = p.M, r0 = mt0 * 8;
+  // Row scales of the input RMSNorm.
+  for (int i = wave; i < NMT * 8; i += kWideWaves) {
+    const float v = norm_scale(p, r0 + i, lane);
+    if (lane == 0) s_rs[i] = v;
+  }
+  __syncthreads();
+
+  for (int e = threadIdx.x; e < kWideNg * NMT * 128; e += kWideWaves * 64) {
+    const int jj = e / (NMT * 128), mtl = (e >> 7) % NMT, i = (e >> 4) & 7, col = e & 15;
+    const int m = r0 + mtl * 8 + i, nt = g * kWideNg + jj;
+    if (m >= M || nt >= p.NT) {
+      if (EPI == kEpiResid) ep[e] = 0.f;
+      continue;
+    }
+    const float rs = s_rs[mtl * 8 + i];
+    const float v = ep[e] * rs;
+    const float v2 = (EPI == kEpiSwiglu || EPI == kEpiQkv) && col < 8 ? ep[e + 8] * rs : 0.f;
+    const float sq = epilogue_element<T, EPI>(p, p.m0 + m, nt, col, v, v2);
+    if (EPI == kEpiResid) ep[e] = sq;              // only this thread reads element e here
+  }
+  if (EPI == kEpiResid) {
+    // Sums of squares of the group's 128 columns per row, in a fixed order.
+    __syncthreads();
+    for (int r = threadIdx.x; r < NMT * 8; r += kWideWaves * 64) {
+      const int m = r0 + r;
+      if (m >= M) continue;
+      const int mtl = r >> 3, i = r & 7;
+      float sum = 0.f;
+      for (int jj = 0; jj < kWideNg; ++jj)
+        for (int c = 0; c < 16; ++c) sum += ep[((jj * NMT + mtl) * 8 + i) * 16 + c];
+      p.ss_out[static_cast<size_t>(g) * p.Mtot + p.m0 + m] = sum;
+    }
+  }
+}
+
+// Epilogue of column group g from the folded tile in acc (all MT M tiles).
 template <int MT, int EPI>
 __device__ __forceinline__ void wide_epilogue(const GemmParams& p, int g, const f32x4 (&acc)[kWideNtw][MT],
                                               float* ep, float* s_rs) {
-  using T = bf16;
-  constexpr int kMaxRows = MT * 8;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int M = p.M;
   if (lane < 32) {
 #pragma unroll
     for (int j = 0; j < kWideNtw; ++j)
@@ -163,37 +201,7 @@ __device__ __forceinline__ void wide_epilogue(const GemmParams& p, int g, const 
         for (int r = 0; r < 4; ++r)
           ep[(((wave * kWideNtw + j) * MT + mt) * 8 + (lane >> 4) * 4 + r) * 16 + (lane & 15)] = acc[j][mt][r];
   }
-  // Row scales of the input RMSNorm.
-  for (int m = wave; m < kMaxRows; m += kWideWaves) {
-    const float v = norm_scale(p, m, lane);
-    if (lane == 0) s_rs[m] = v;
-  }
-  __syncthreads();
-
-  for (int e = threadIdx.x; e < kWideNg * MT * 128; e += kWideWaves * 64) {
-    const int jj = e / (MT * 128), mt = (e >> 7) % MT, i = (e >> 4) & 7, col = e & 15;
-    const int m = mt * 8 + i, nt = g * kWideNg + jj;
-    if (m >= M || nt >= p.NT) {
-      if (EPI == kEpiResid) ep[e] = 0.f;
-      continue;
-    }
-    const float rs = s_rs[m];
-    const float v = ep[e] * rs;
-    const float v2 = (EPI == kEpiSwiglu || EPI == kEpiQkv) && col < 8 ? ep[e + 8] * rs : 0.f;
-    const float sq = epilogue_element<T, EPI>(p, p.m0 + m, nt, col, v, v2);
-    if (EPI == kEpiResid) ep[e] = sq;              // only this thread reads element e here
-  }
-  if (EPI == kEpiResid) {
-    // Sums of squares of the group's 128 columns per row, in a fixed order.
-    __syncthreads();
-    for (int m = threadIdx.x; m < M; m += kWideWaves * 64) {
-      const int mt = m >> 3, i = m & 7;
-      float sum = 0.f;
-      for (int jj = 0; jj < kWideNg; ++jj)
-        for (int c = 0; c < 16; ++c) sum += ep[((jj * MT + mt) * 8 + i) * 16 + c];
-      p.ss_out[static_cast<size_t>(g) * p.Mtot + p.m0 + m] = sum;
-    }
-  }
+  wide_epilogue_tile<MT, EPI>(p, g, 0, ep, s_rs);
 }
 
 // One work-group per column group over the whole k range, epilogue fused.
@@ -234,31 +242,26 @@ void gemm_wide_split_kernel(const GemmParams p, int S, int chunks) {
   }
 }
 
-// Sum of the S partials of column group g = blockIdx.x, in split order, then
-// the epilogue.
+// Sum of the S partials of column group g = blockIdx.x, M tile mt =
+// blockIdx.y, in split order, then the epilogue of that tile. Thread t sums
+// lane t % 32 of n-tile t / 32 (wave t / 64 of the split kernel, its tile
+// t / 32 % 2): one coalesced 16 B load per split.
 template <int MT, int EPI>
 __global__ __launch_bounds__(kWideWaves * 64) void gemm_wide_reduce_kernel(const GemmParams p, int S) {
-  __shared__ float ep[kWideNg * MT * 128];
-  __shared__ float s_rs[MT * 8];
+  __shared__ float ep[kWideNg * 128];
+  __shared__ float s_rs[8];
   const int G = (p.NT + kWideNg - 1) / kWideNg;
-  const int g = blockIdx.x;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  f32x4 acc[kWideNtw][MT];
+  const int g = blockIdx.x, mt = blockIdx.y;
+  const int t = threadIdx.x, jj = t >> 5, ln = t & 31;
+  const float* src = p.part + (static_cast<size_t>(g) * kWideWaves + (jj >> 1)) * wide_part_floats<MT>() +
+                     (((jj & 1) * MT + mt) * 32 + ln) * 4;
+  const size_t split = static_cast<size_t>(G) * kWideWaves * wide_part_floats<MT>();
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < S; ++s) acc += *reinterpret_cast<const f32x4*>(src + s * split);
 #pragma unroll
-  for (int j = 0; j < kWideNtw; ++j)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (lane < 32) {
-    for (int s = 0; s < S; ++s) {
-      const float* src = p.part + ((static_cast<size_t>(s) * G + g) * kWideWaves + wave) * wide_part_floats<MT>();
-#pragma unroll
-      for (int j = 0; j < kWideNtw; ++j)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-          acc[j][mt] += *reinterpret_cast<const f32x4*>(src + ((j * MT + mt) * 32 + lane) * 4);
-    }
-  }
-  wide_epilogue<MT, EPI>(p, g, acc, ep, s_rs);
+  for (int r = 0; r < 4; ++r) ep[(jj * 8 + (ln >> 4) * 4 + r) * 16 + (ln & 15)] = acc[r];
+  // (wide_epilogue_tile's first barrier orders these stores before the reads.)
+  wide_epilogue_tile<1, EPI>(p, g, mt, ep, s_rs);
 }
 
 // ---------------------------------------------------------------------------
@@ -304,11 +307,11 @@ static hipError_t wide_launch(const GemmParams& p, const WidePlan& w, hipStream_
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     switch (p.epi) {
-      case kEpiStore: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiStore>), dim3(w.G), block, 0, st, p, w.S); break;
-      case kEpiGelu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiGelu>), dim3(w.G), block, 0, st, p, w.S); break;
-      case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiSwiglu>), dim3(w.G), block, 0, st, p, w.S); break;
-      case kEpiResid: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiResid>), dim3(w.G), block, 0, st, p, w.S); break;
-      default: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiQkv>), dim3(w.G), block, 0, st, p, w.S); break;
+      case kEpiStore: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiStore>), dim3(w.G, MT), block, 0, st, p, w.S); break;
+      case kEpiGelu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiGelu>), dim3(w.G, MT), block, 0, st, p, w.S); break;
+      case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiSwiglu>), dim3(w.G, MT), block, 0, st, p, w.S); break;
+      case kEpiResid: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiResid>), dim3(w.G, MT), block, 0, st, p, w.S); break;
+      default: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiQkv>), dim3(w.G, MT), block, 0, st, p, w.S); break;
     }
     return hipGetLastError();
   }
