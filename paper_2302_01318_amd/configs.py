@@ -55,3 +55,9 @@ ACCEPT_GRID = {"V": 32000, "K": (1, 2, 4, 8), "B": (1, 8, 64), "sigma": 2.0, "si
 # 70B verify sweep.
 SWEEP = {"K": (1, 2, 3, 4, 6, 8), "B": (1, 4, 16), "ctx": (2048, 8192),
          "sigma_pert": (0.1, 0.5, 1.0)}
+
+# K trade-off study on a coupled 70B / draft pair: the draft's logits are the
+# target's plus N(0, code_pert^2) per entry (the sigma_pert of the accept-stage
+# pairs), the logit spread is 2 as there.
+K_STUDY = {"K": (1, 2, 3, 4, 6, 8), "layer_std": 0.002, "code_pert": (0.1, 0.5, 1.0), "logit_std": 2.0,
+           "rank": 64, "prompt": 256, "n_new": 128, "reps": 10, "pair_seed": 7}

@@ -17,6 +17,20 @@ Recipes:
                z_p = z_q + N(0, sigma_pert^2); p and q are the normalised
                exponentials of those logits, rounded to fp32; draft token t
                is drawn from p_t with numpy's generic categorical sampler.
+  coupled pair a target and a draft of different widths whose logits are
+               the accept_case recipe realised in weights: both share token
+               codes z_x ~ N(0, I_r) and output codes o_y ~ N(0, s^2 I_r)
+               (rank r, one generator seeded by the pair seed); a model may
+               perturb its copy, o'_y = o_y + code_pert n_y with
+               n_y ~ N(0, I_r) from its own seed. Each model has its own
+               orthonormal basis Q [d][r] (QR of an N(0, 1) matrix), embeds
+               E[x] = sqrt(d) Q z_x and unembeds with W_U[y] = Q o'_y / sqrt(d);
+               norm gains are 1. Through the skip path alone the final
+               RMSNorm of E[x] is sqrt(d) Q z_x / |z_x|, so the logits are
+               o'_y . z_x / |z_x|: N(0, s^2) per entry for the target and the
+               same plus N(0, code_pert^2) for the draft. Attention and FFN
+               weights are N(0, layer_std^2); at small layer_std they cost
+               their full time but move the logits little.
 """
 import numpy as np
 import torch
@@ -126,5 +140,36 @@ def device_weights(cfg, seed, std=0.02, gain_std=0.1, device="cuda"):
             t = torch.randn(shape, generator=gen, device=device, dtype=torch.float32).mul_(gain_std).add_(1.0)
         else:
             t = torch.randn(shape, generator=gen, device=device, dtype=dt).mul_(std)
+        yield key, t
+        del t
+
+
+def coupled_device_weights(cfg, pair_seed, model_seed, layer_std, code_pert=0.0, logit_std=2.0, rank=64,
+                           device="cuda"):
+    """Yield ((name, layer), tensor) for one model of a coupled pair (module
+    doc): embedding and unembedding from the shared codes in this model's
+    basis (output codes perturbed by code_pert), unit gains, N(0, layer_std^2)
+    layer weights."""
+    d, V = cfg.d_model, cfg.vocab
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    pair = torch.Generator(device=device)
+    pair.manual_seed(int(pair_seed))
+    z = torch.randn((V, rank), generator=pair, device=device)
+    o = torch.randn((V, rank), generator=pair, device=device) * logit_std
+    q, _ = np.linalg.qr(_rng(model_seed, 4, d).standard_normal((d, rank)))
+    Q = torch.from_numpy(q.astype(np.float32)).to(device)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(model_seed))
+    if code_pert:
+        o = o + torch.randn((V, rank), generator=gen, device=device) * code_pert
+    for key, shape in tensor_shapes(cfg).items():
+        if key[0] == "embed":
+            t = (z @ Q.t()).mul_(float(np.sqrt(d))).to(dt)
+        elif key[0] == "unembed":
+            t = (o @ Q.t()).mul_(float(1.0 / np.sqrt(d))).to(dt)
+        elif key[0].endswith("norm"):
+            t = torch.ones(shape, device=device, dtype=torch.float32)
+        else:
+            t = torch.randn(shape, generator=gen, device=device, dtype=dt).mul_(layer_std)
         yield key, t
         del t
