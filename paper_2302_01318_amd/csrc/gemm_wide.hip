@@ -7,9 +7,10 @@
 // weight byte through the vector caches, and above MT = 1 that traffic, not
 // HBM, sets the speed. Here:
 //
-//  * a work-group of 4 waves owns 8 consecutive n-tiles (128 output columns)
-//    and one contiguous range of the k-tiles; wave w multiplies n-tiles
-//    2w and 2w + 1 by all MT M tiles;
+//  * a work-group of 4 waves owns 4 NTW consecutive n-tiles (NTW = 2, or 4
+//    at 14 M tiles, where each fragment read from LDS then feeds four MFMAs
+//    instead of two) and one contiguous range of the k-tiles; wave w
+//    multiplies n-tiles NTW w .. NTW w + NTW - 1 by all MT M tiles;
 //  * per chunk of KC k-tiles the work-group copies the MT x KC activation
 //    fragments once into LDS with global_load_lds (16 B per lane, each
 //    wave instruction one fragment in register order), so the four waves
@@ -18,7 +19,9 @@
 //  * where N is too small to give every CU a work-group (the d_model-wide
 //    outputs), the k range is split S ways (split-K): each split writes its
 //    fp32 partial tile to the workspace and a second kernel sums the splits
-//    in split order and runs the epilogue. (A last-arriving-split fixup
+//    in split order and runs the epilogue, one work-group per norm group
+//    (8 n-tiles, 128 columns: the unit of the residual epilogue's sums of
+//    squares whatever NTW is) and M tile. (A last-arriving-split fixup
 //    inside one kernel would need device-scope fences, which on this GPU
 //    write back and invalidate the L2 and cost more than the launch.)
 #include <algorithm>
@@ -30,16 +33,23 @@
 namespace sps {
 
 constexpr int kWideWaves = 4;                      // waves per work-group
-constexpr int kWideNtw = 2;                        // n-tiles per wave
-constexpr int kWideNg = kWideWaves * kWideNtw;     // n-tiles per work-group (column group)
+constexpr int kNormTiles = 8;                      // n-tiles per norm group (128 columns)
 
-// Partial tile of one wave: kWideNtw x MT fragments of 32 lanes x 4 floats
-// (the hi rows after folding the lo rows in), in register order.
-template <int MT> constexpr int wide_part_floats() { return kWideNtw * MT * 128; }
+// n-tiles per wave: 4 at 14 M tiles (one wave per SIMD either way; W_1 and
+// W_2 of the 70B shape run 22-24 % faster than with 2). From 16 M tiles the
+// 4 x MT accumulators and the compiler's early LDS fragment reads no longer
+// fit the register file, and the spilled kernel is no faster than NTW = 2.
+static constexpr int wide_ntw(int MT) { return MT == 14 ? 4 : 2; }
+
+// Partial tile of one wave: NTW x MT fragments of 32 lanes x 4 floats (the
+// hi rows after folding the lo rows in), in register order.
+template <int MT, int NTW> constexpr int wide_part_floats() { return NTW * MT * 128; }
 
 // Waves per SIMD the register allocation must allow (the compiler would
 // otherwise hoist every LDS fragment read of a chunk into registers).
-template <int MT> constexpr int wide_waves_per_simd() { return MT <= 6 ? 3 : MT <= 12 ? 2 : 1; }
+template <int MT, int NTW> constexpr int wide_waves_per_simd() {
+  return NTW == 4 || MT > 12 ? 1 : MT <= 6 ? 3 : 2;
+}
 
 // Accumulate chunks [c0, c1) of column group g into acc, then fold the
 // lo-plane rows (lanes 32-63) into their hi rows (lanes 0-31). Double
@@ -47,22 +57,22 @@ template <int MT> constexpr int wide_waves_per_simd() { return MT <= 6 ? 3 : MT 
 // fragments are already on their way into the other LDS buffer (s_a holds
 // 2 * MT * KC fragments) and its weight fragments into the other register
 // set; one barrier per chunk.
-template <int MT, int KC>
+template <int MT, int KC, int NTW>
 __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0, int c1, bf16x8 (*s_a)[64],
-                                              f32x4 (&acc)[kWideNtw][MT]) {
+                                              f32x4 (&acc)[NTW][MT]) {
   using T = bf16;
   constexpr int kTile = 512;                       // elements per 16 x 32 tile
   constexpr int kBuf = MT * KC;                    // fragments per LDS buffer
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int ntw = g * kWideNg + wave * kWideNtw;   // first n-tile of this wave
+  const int ntw = g * kWideWaves * NTW + wave * NTW;   // first n-tile of this wave
   const int r16 = lane & 15, grp = lane >> 4;
   const int KT = p.KT, M = p.M;
   const T* W = static_cast<const T*>(p.W);
 
-  const T* wp[kWideNtw];
-  bool wv[kWideNtw];
+  const T* wp[NTW];
+  bool wv[NTW];
 #pragma unroll
-  for (int j = 0; j < kWideNtw; ++j) {
+  for (int j = 0; j < NTW; ++j) {
     wv[j] = ntw + j < p.NT;
     wp[j] = W + static_cast<size_t>(wv[j] ? ntw + j : 0) * KT * kTile + lane * 8;
   }
@@ -72,7 +82,7 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
   const T* xbase = static_cast<const T*>(p.X) + (r16 >> 3) * p.xplane + grp * 8;
 
 #pragma unroll
-  for (int j = 0; j < kWideNtw; ++j)
+  for (int j = 0; j < NTW; ++j)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -89,16 +99,16 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
       }
     }
   };
-  auto load_b = [&](int c, Frag<T> (&b)[kWideNtw][KC]) {
+  auto load_b = [&](int c, Frag<T> (&b)[NTW][KC]) {
     const int kb = c * KC;
 #pragma unroll
-    for (int j = 0; j < kWideNtw; ++j)
+    for (int j = 0; j < NTW; ++j)
 #pragma unroll
       for (int u = 0; u < KC; ++u)
         b[j][u] = wv[j] && kb + u < KT ? load_frag_stream(wp[j] + static_cast<size_t>(kb + u) * kTile)
                                        : Frag<T>::zero();
   };
-  auto compute = [&](int c, int bb, const Frag<T> (&b)[kWideNtw][KC]) {
+  auto compute = [&](int c, int bb, const Frag<T> (&b)[NTW][KC]) {
     const int kb = c * KC;
 #pragma unroll
     for (int u = 0; u < KC; ++u) {
@@ -108,7 +118,7 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
           Frag<T> a;
           a.v = s_a[bb * kBuf + mt * KC + u][lane];
 #pragma unroll
-          for (int j = 0; j < kWideNtw; ++j) acc[j][mt] = mma8(acc[j][mt], a, b[j][u]);
+          for (int j = 0; j < NTW; ++j) acc[j][mt] = mma8(acc[j][mt], a, b[j][u]);
         }
       }
     }
@@ -116,7 +126,7 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
   // One chunk: wait for its loads (the only ones outstanding), start the
   // next chunk's, then multiply. Buffer bb ^ 1 is free: every wave passed
   // this barrier only after finishing the previous chunk, which used it.
-  auto step = [&](int c, int bb, const Frag<T> (&bcur)[kWideNtw][KC], Frag<T> (&bnext)[kWideNtw][KC]) {
+  auto step = [&](int c, int bb, const Frag<T> (&bcur)[NTW][KC], Frag<T> (&bnext)[NTW][KC]) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (c + 1 < c1) {
@@ -126,7 +136,7 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
     compute(c, bb, bcur);
   };
 
-  Frag<T> b0[kWideNtw][KC], b1[kWideNtw][KC];
+  Frag<T> b0[NTW][KC], b1[NTW][KC];
   if (c0 < c1) {
     issue_a(c0, 0);
     load_b(c0, b0);
@@ -137,31 +147,36 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
   }
   __syncthreads();                                 // LDS free for the caller (epilogue tile)
 #pragma unroll
-  for (int j = 0; j < kWideNtw; ++j)
+  for (int j = 0; j < NTW; ++j)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[j][mt][r] += __shfl_xor(acc[j][mt][r], 32);
 }
 
-// Epilogue of M tiles mt0 .. mt0 + NMT - 1 of column group g. ep holds their
-// output tile in LDS as [8 n-tiles][NMT][8 rows][16 columns]; s_rs is LDS for
-// NMT * 8 row scales.
-template <int NMT, int EPI>
-__device__ __forceinline__ void wide_epilogue_tile(const GemmParams& p, int g, int mt0, float* ep, float* s_rs) {
-  using T = bf16;
+// Row scales of the input RMSNorm for rows mt0 * 8 .. (mt0 + NMT) * 8 - 1
+// into s_rs (the caller synchronises before use).
+template <int NMT>
+__device__ __forceinline__ void wide_row_scales(const GemmParams& p, int mt0, float* s_rs) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int M = p.M, r0 = mt0 * 8;
-  // Row scales of the input RMSNorm.
   for (int i = wave; i < NMT * 8; i += kWideWaves) {
-    const float v = norm_scale(p, r0 + i, lane);
+    const float v = norm_scale(p, mt0 * 8 + i, lane);
     if (lane == 0) s_rs[i] = v;
   }
-  __syncthreads();
+}
 
-  for (int e = threadIdx.x; e < kWideNg * NMT * 128; e += kWideWaves * 64) {
+// Epilogue of norm group gs (n-tiles 8 gs .. 8 gs + 7) for M tiles mt0 ..
+// mt0 + NMT - 1. ep holds their output tile in LDS as [8 n-tiles][NMT][8
+// rows][16 columns] and s_rs their row scales, both visible to every thread.
+template <int NMT, int EPI>
+__device__ __forceinline__ void wide_epilogue_group(const GemmParams& p, int gs, int mt0, float* ep,
+                                                    const float* s_rs) {
+  using T = bf16;
+  const int M = p.M, r0 = mt0 * 8;
+  if (gs * kNormTiles >= p.NT) return;             // whole group past the last n-tile
+  for (int e = threadIdx.x; e < kNormTiles * NMT * 128; e += kWideWaves * 64) {
     const int jj = e / (NMT * 128), mtl = (e >> 7) % NMT, i = (e >> 4) & 7, col = e & 15;
-    const int m = r0 + mtl * 8 + i, nt = g * kWideNg + jj;
+    const int m = r0 + mtl * 8 + i, nt = gs * kNormTiles + jj;
     if (m >= M || nt >= p.NT) {
       if (EPI == kEpiResid) ep[e] = 0.f;
       continue;
@@ -180,88 +195,98 @@ __device__ __forceinline__ void wide_epilogue_tile(const GemmParams& p, int g, i
       if (m >= M) continue;
       const int mtl = r >> 3, i = r & 7;
       float sum = 0.f;
-      for (int jj = 0; jj < kWideNg; ++jj)
+      for (int jj = 0; jj < kNormTiles; ++jj)
         for (int c = 0; c < 16; ++c) sum += ep[((jj * NMT + mtl) * 8 + i) * 16 + c];
-      p.ss_out[static_cast<size_t>(g) * p.Mtot + p.m0 + m] = sum;
+      p.ss_out[static_cast<size_t>(gs) * p.Mtot + p.m0 + m] = sum;
     }
   }
 }
 
-// Epilogue of column group g from the folded tile in acc (all MT M tiles).
-template <int MT, int EPI>
-__device__ __forceinline__ void wide_epilogue(const GemmParams& p, int g, const f32x4 (&acc)[kWideNtw][MT],
-                                              float* ep, float* s_rs) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (lane < 32) {
-#pragma unroll
-    for (int j = 0; j < kWideNtw; ++j)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          ep[(((wave * kWideNtw + j) * MT + mt) * 8 + (lane >> 4) * 4 + r) * 16 + (lane & 15)] = acc[j][mt][r];
-  }
-  wide_epilogue_tile<MT, EPI>(p, g, 0, ep, s_rs);
-}
-
-// One work-group per column group over the whole k range, epilogue fused.
-template <int MT, int KC, int EPI>
-__global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT>())))
+// One work-group per column group (4 NTW n-tiles) over the whole k range,
+// epilogue fused: the folded tile goes to LDS one norm group at a time.
+template <int MT, int KC, int NTW, int EPI>
+__global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, NTW>())))
 void gemm_wide_kernel(const GemmParams p, int chunks) {
   __shared__ bf16x8 s_a[2 * MT * KC][64];          // two chunks of activation fragments
-  // The epilogue's output tile and row scales reuse the chunk buffers, dead
-  // after the loop.
-  constexpr int kTile = kWideNg * MT * 128;        // floats
-  static_assert((kTile + MT * 8) * sizeof(float) <= sizeof(s_a), "epilogue buffers must fit the chunk buffers");
-  f32x4 acc[kWideNtw][MT];
-  wide_mainloop<MT, KC>(p, blockIdx.x, 0, chunks, s_a, acc);
+  // One norm group's output tile reuses the chunk buffers, dead after the
+  // loop, and so do the row scales where they fit behind it.
+  constexpr int kTile = kNormTiles * MT * 128;     // floats
+  static_assert(kTile * sizeof(float) <= sizeof(s_a), "epilogue tile must fit the chunk buffers");
+  constexpr bool kRsInA = (kTile + MT * 8) * sizeof(float) <= sizeof(s_a);
+  __shared__ float s_rs_own[kRsInA ? 1 : MT * 8];
+  constexpr int kGroups = kWideWaves * NTW / kNormTiles;   // norm groups per work-group
+  constexpr int kWavesPerGroup = kWideWaves / kGroups;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  f32x4 acc[NTW][MT];
+  wide_mainloop<MT, KC, NTW>(p, blockIdx.x, 0, chunks, s_a, acc);
   float* ep = reinterpret_cast<float*>(&s_a[0][0]);
-  wide_epilogue<MT, EPI>(p, blockIdx.x, acc, ep, ep + kTile);
+  float* s_rs = kRsInA ? ep + kTile : s_rs_own;
+#pragma unroll
+  for (int h = 0; h < kGroups; ++h) {
+    if (wave / kWavesPerGroup == h && lane < 32) {
+      const int jw = (wave % kWavesPerGroup) * NTW;
+#pragma unroll
+      for (int j = 0; j < NTW; ++j)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            ep[(((jw + j) * MT + mt) * 8 + (lane >> 4) * 4 + r) * 16 + (lane & 15)] = acc[j][mt][r];
+    }
+    if (h == 0) wide_row_scales<MT>(p, 0, s_rs);   // after the first dump: fewer live registers
+    __syncthreads();
+    wide_epilogue_group<MT, EPI>(p, blockIdx.x * kGroups + h, 0, ep, s_rs);
+    if (h + 1 < kGroups) __syncthreads();          // ep is rewritten for the next group
+  }
 }
 
 // Split s of column group g (work-group g + s G): chunks [s C / S, (s+1) C / S)
 // into the partial buffer.
-template <int MT, int KC>
-__global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT>())))
+template <int MT, int KC, int NTW>
+__global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, NTW>())))
 void gemm_wide_split_kernel(const GemmParams p, int S, int chunks) {
   __shared__ bf16x8 s_a[2 * MT * KC][64];
-  const int G = (p.NT + kWideNg - 1) / kWideNg;
+  const int G = (p.NT + kWideWaves * NTW - 1) / (kWideWaves * NTW);
   const int g = blockIdx.x % G, s = blockIdx.x / G;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c0 = static_cast<int>(static_cast<long>(s) * chunks / S);
   const int c1 = static_cast<int>(static_cast<long>(s + 1) * chunks / S);
-  f32x4 acc[kWideNtw][MT];
-  wide_mainloop<MT, KC>(p, g, c0, c1, s_a, acc);
+  f32x4 acc[NTW][MT];
+  wide_mainloop<MT, KC, NTW>(p, g, c0, c1, s_a, acc);
   if (lane < 32) {
-    float* mine = p.part + ((static_cast<size_t>(s) * G + g) * kWideWaves + wave) * wide_part_floats<MT>();
+    float* mine = p.part + ((static_cast<size_t>(s) * G + g) * kWideWaves + wave) * wide_part_floats<MT, NTW>();
 #pragma unroll
-    for (int j = 0; j < kWideNtw; ++j)
+    for (int j = 0; j < NTW; ++j)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
         *reinterpret_cast<f32x4*>(mine + ((j * MT + mt) * 32 + lane) * 4) = acc[j][mt];
   }
 }
 
-// Sum of the S partials of column group g = blockIdx.x, M tile mt =
+// Sum of the S partials of norm group gs = blockIdx.x, M tile mt =
 // blockIdx.y, in split order, then the epilogue of that tile. Thread t sums
-// lane t % 32 of n-tile t / 32 (wave t / 64 of the split kernel, its tile
-// t / 32 % 2): one coalesced 16 B load per split.
-template <int MT, int EPI>
+// lane t % 32 of n-tile 8 gs + t / 32, which the split kernel's work-group
+// (8 gs + t / 32) / (4 NTW) holds in wave ((8 gs + t / 32) % (4 NTW)) / NTW:
+// one coalesced 16 B load per split.
+template <int MT, int NTW, int EPI>
 __global__ __launch_bounds__(kWideWaves * 64) void gemm_wide_reduce_kernel(const GemmParams p, int S) {
-  __shared__ float ep[kWideNg * 128];
+  __shared__ float ep[kNormTiles * 128];
   __shared__ float s_rs[8];
-  const int G = (p.NT + kWideNg - 1) / kWideNg;
-  const int g = blockIdx.x, mt = blockIdx.y;
+  constexpr int kNg = kWideWaves * NTW;
+  const int G = (p.NT + kNg - 1) / kNg;
+  const int gs = blockIdx.x, mt = blockIdx.y;
   const int t = threadIdx.x, jj = t >> 5, ln = t & 31;
-  const float* src = p.part + (static_cast<size_t>(g) * kWideWaves + (jj >> 1)) * wide_part_floats<MT>() +
-                     (((jj & 1) * MT + mt) * 32 + ln) * 4;
-  const size_t split = static_cast<size_t>(G) * kWideWaves * wide_part_floats<MT>();
+  const int nt = gs * kNormTiles + jj, g = nt / kNg, wave = (nt % kNg) / NTW, j = nt % NTW;
+  const float* src = p.part + (static_cast<size_t>(g) * kWideWaves + wave) * wide_part_floats<MT, NTW>() +
+                     ((j * MT + mt) * 32 + ln) * 4;
+  const size_t split = static_cast<size_t>(G) * kWideWaves * wide_part_floats<MT, NTW>();
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int s = 0; s < S; ++s) acc += *reinterpret_cast<const f32x4*>(src + s * split);
 #pragma unroll
   for (int r = 0; r < 4; ++r) ep[(jj * 8 + (ln >> 4) * 4 + r) * 16 + (ln & 15)] = acc[r];
-  // (wide_epilogue_tile's first barrier orders these stores before the reads.)
-  wide_epilogue_tile<1, EPI>(p, g, mt, ep, s_rs);
+  wide_row_scales<1>(p, mt, s_rs);
+  __syncthreads();
+  wide_epilogue_group<1, EPI>(p, gs, mt, ep, s_rs);
 }
 
 // ---------------------------------------------------------------------------
@@ -271,7 +296,8 @@ static const int kWideMT[] = {2, 3, 4, 5, 6, 8, 10, 12, 14, 16, 18, 20};
 
 // k-tiles per chunk: the two chunk buffers (2 MT KC KiB of LDS) leave room
 // for two to three work-groups per CU up to 10 M tiles (one above 12, where
-// registers allow one wave per SIMD) and hold the output tile (4 MT KiB).
+// registers allow one wave per SIMD) and hold a norm group's output tile
+// (4 MT KiB).
 static constexpr int wide_kc(int MT) { return MT <= 10 ? 4 : MT == 12 || MT == 20 ? 3 : 4; }
 
 WidePlan wide_plan(int NT, int KT, int M) {
@@ -281,7 +307,8 @@ WidePlan wide_plan(int NT, int KT, int M) {
   for (int v : kWideMT)
     if (v >= mt) { w.MT = v; break; }
   w.KC = wide_kc(w.MT);
-  w.G = (NT + kWideNg - 1) / kWideNg;
+  w.NTW = wide_ntw(w.MT);
+  w.G = (NT + kWideWaves * w.NTW - 1) / (kWideWaves * w.NTW);
   w.chunks = (KT + w.KC - 1) / w.KC;
   // Split until the launch holds about two work-groups per CU (one above
   // 12 M tiles, where registers allow one wave per SIMD).
@@ -294,34 +321,36 @@ WidePlan wide_plan(int NT, int KT, int M) {
 }
 
 size_t wide_part_bytes(const WidePlan& w) {
-  return w.S > 1 ? static_cast<size_t>(w.S) * w.G * kWideWaves * kWideNtw * w.MT * 128 * sizeof(float) : 0;
+  return w.S > 1 ? static_cast<size_t>(w.S) * w.G * kWideWaves * w.NTW * w.MT * 128 * sizeof(float) : 0;
 }
 
-int wide_groups(int NT) { return (NT + kWideNg - 1) / kWideNg; }
+int wide_groups(int NT) { return (NT + kNormTiles - 1) / kNormTiles; }
 
-template <int MT, int KC = wide_kc(MT)>
+template <int MT, int KC = wide_kc(MT), int NTW = wide_ntw(MT)>
 static hipError_t wide_launch(const GemmParams& p, const WidePlan& w, hipStream_t st) {
   const dim3 block(kWideWaves * 64);
+  if (w.NTW != NTW || w.KC != KC) return hipErrorInvalidValue;
   if (w.S > 1) {
-    hipLaunchKernelGGL((gemm_wide_split_kernel<MT, KC>), dim3(w.G * w.S), block, 0, st, p, w.S, w.chunks);
+    hipLaunchKernelGGL((gemm_wide_split_kernel<MT, KC, NTW>), dim3(w.G * w.S), block, 0, st, p, w.S, w.chunks);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    const dim3 rgrid(wide_groups(p.NT), MT);
     switch (p.epi) {
-      case kEpiStore: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiStore>), dim3(w.G, MT), block, 0, st, p, w.S); break;
-      case kEpiGelu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiGelu>), dim3(w.G, MT), block, 0, st, p, w.S); break;
-      case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiSwiglu>), dim3(w.G, MT), block, 0, st, p, w.S); break;
-      case kEpiResid: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiResid>), dim3(w.G, MT), block, 0, st, p, w.S); break;
-      default: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, kEpiQkv>), dim3(w.G, MT), block, 0, st, p, w.S); break;
+      case kEpiStore: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, kEpiStore>), rgrid, block, 0, st, p, w.S); break;
+      case kEpiGelu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, kEpiGelu>), rgrid, block, 0, st, p, w.S); break;
+      case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, kEpiSwiglu>), rgrid, block, 0, st, p, w.S); break;
+      case kEpiResid: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, kEpiResid>), rgrid, block, 0, st, p, w.S); break;
+      default: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, kEpiQkv>), rgrid, block, 0, st, p, w.S); break;
     }
     return hipGetLastError();
   }
   const dim3 grid(w.G);
   switch (p.epi) {
-    case kEpiStore: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, kEpiStore>), grid, block, 0, st, p, w.chunks); break;
-    case kEpiGelu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, kEpiGelu>), grid, block, 0, st, p, w.chunks); break;
-    case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, kEpiSwiglu>), grid, block, 0, st, p, w.chunks); break;
-    case kEpiResid: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, kEpiResid>), grid, block, 0, st, p, w.chunks); break;
-    default: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, kEpiQkv>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiStore: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiStore>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiGelu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiGelu>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiSwiglu>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiResid: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiResid>), grid, block, 0, st, p, w.chunks); break;
+    default: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiQkv>), grid, block, 0, st, p, w.chunks); break;
   }
   return hipGetLastError();
 }

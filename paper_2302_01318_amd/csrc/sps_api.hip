@@ -90,14 +90,18 @@ WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
   const size_t M = static_cast<size_t>(B) * Mps;
   const size_t NP = sps::attn_partials(T_cap);
   const size_t ng = (L.d + 15) / 16;   // column groups a residual GEMM can produce
-  // Split-K partials of the wide GEMM (bf16, more than 8 rows).
+  // Split-K partials of the wide GEMM (bf16, more than 8 rows), for every
+  // launch of the forward: full launches of gemm_max_rows rows and the
+  // remainder, which may split more ways.
   size_t part = 0;
   if (sps::gemm_is_wide(dt, static_cast<int>(M))) {
     int g[5][2];
     forward_gemms(L, g);
-    for (int i = 0; i < 5; ++i) {
-      const sps::WidePlan p = sps::wide_plan(g[i][0], g[i][1], static_cast<int>(M));
-      part = std::max(part, sps::wide_part_bytes(p));
+    const int cap = sps::gemm_max_rows(dt);
+    const int rows[2] = {static_cast<int>(std::min<size_t>(M, cap)), static_cast<int>(M % cap)};
+    for (int r : rows) {            // (every launch of a forward past 8 rows is wide)
+      if (r <= 0) continue;
+      for (int i = 0; i < 5; ++i) part = std::max(part, sps::wide_part_bytes(sps::wide_plan(g[i][0], g[i][1], r)));
     }
   }
   size_t o = 0;
