@@ -38,6 +38,8 @@ CALIBRATION_BYTES = 1 << 30      # plain device copy whose HBM counters calibrat
 # Sources of the single-tile GEMM kernel (the one the traffic counters were taken on).
 GEMM_SOURCES = [os.path.join(ROOT, "paper_2302_01318_amd", "csrc", f) for f in ("gemm.hip", "gemm_epi.h", "common.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
+MFMA_FILE = os.path.join(ROOT, "profiles", "gemm_mfma.json")
+STREAM_READ_BYTES = 8 << 30      # bytes of the packed weights read by the streaming-read ceiling
 
 
 def source_digest(paths):
@@ -60,6 +62,34 @@ def measured_traffic():
     if t.get("gemm_source_sha256_16") != source_digest(GEMM_SOURCES):
         return None
     return t.get("hbm_bytes_per_launch")
+
+
+def measured_mfma():
+    """MFMA utilisation of the GEMM launches from rocprofv3 counters (see the
+    profiles/ file), if they were taken on the current GEMM source."""
+    try:
+        with open(MFMA_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("gemm_source_sha256_16") != source_digest(GEMM_SOURCES):
+        return None
+    return {k: t[k] for k in ("mfma_busy_pct", "mfma_executed_tflops", "useful_tflops") if k in t}
+
+
+def stream_read_rate(sps, torch, buf, nbytes=STREAM_READ_BYTES, reps=10):
+    """GB/s of the library's plain streaming read over the first `nbytes` of
+    `buf` (the attainable HBM read rate on this device), median of `reps`."""
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    sps.stream_read(buf, nbytes, sink)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    ev[0].record()
+    for i in range(reps):
+        sps.stream_read(buf, nbytes, sink)
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    t = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(reps))
+    return nbytes / (t[reps // 2] * 1e-3) / 1e9
 
 
 def round_up(x, m):
@@ -403,6 +433,8 @@ def main():
     target = device_model(sps, synth, shape, args.seed)
     torch.cuda.synchronize()
     log("target packed: %.1f GB in %.1f s" % (target.packed.numel() / 1e9, time.time() - t0))
+    read_gbs = stream_read_rate(sps, torch, target.packed)
+    log("streaming read ceiling: %.1f GB/s" % read_gbs)
 
     # ---- verify step: timed region -------------------------------------------------
     T_cap = round_up(ctx + K + 1, 32)
@@ -457,7 +489,8 @@ def main():
                     "achieved": round(g_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(g_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                     "launches_per_step": g_n // args.steps, "avg_launch_us": round(g_avg_ms * 1e3, 2),
-                    "bytes_per_launch": g_bytes / g_n}
+                    "bytes_per_launch": g_bytes / g_n,
+                    "frac_of_stream_read": round(g_gbs / read_gbs, 4), "mfma": measured_mfma()}
     del kv, ws
 
     # ---- SpS and ArS tokens/s end to end ---------------------------------------------
@@ -515,6 +548,8 @@ def main():
                    "K": K, "batch": B, "ctx": ctx, "temperature": T, "top_k": top_k, "top_p": top_p,
                    "bytes_per_step": nbytes,
                    "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)},
+        "stream_read_gbs": round(read_gbs, 1),
+        "verify_frac_of_stream_read": round(gbs / read_gbs, 4),
         "verify_ms": round(ms, 4),
         "verify_ms_p10_median_p90": [round(pct(0.1), 4), round(pct(0.5), 4), round(pct(0.9), 4)],
     }

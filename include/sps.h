@@ -264,6 +264,15 @@ sps_status sps_profile_gemm_begin(int32_t repeats);
 sps_status sps_profile_gemm_end(float* total_ms /*host*/, int32_t* launches /*host*/,
                                 double* bytes /*host*/);
 
+/* Measurement helper: read `bytes` (a multiple of 16) of device memory at
+ * `src` (16-byte aligned) once, with the same nontemporal 16-byte loads the
+ * GEMMs stream their weights with, on `stream`. Nothing is written except,
+ * in practice never, one word of `sink` (a device uint32). Timing this call
+ * with events gives the attainable HBM read rate the verify step's kernels
+ * are compared with. SPS_E_INVALID on null pointers, a misaligned `src` or
+ * a size that is zero or not a multiple of 16. */
+sps_status sps_stream_read(const void* src, size_t bytes, uint32_t* sink, void* stream);
+
 /* Synchronise `stream`, return the current device's sticky error bits in
  * *flags (host) and clear them if `clear` != 0. */
 sps_status sps_device_error(void* stream, int32_t clear, int32_t* flags /*host*/);

@@ -94,6 +94,7 @@ hipError_t launch_commit(int32_t* lengths, const int32_t* tokens, const int32_t*
                          const int32_t* n_acc, int B, int K, int32_t* ctx, int32_t* seq_out,
                          int32_t* n_out, int cap, hipStream_t st);
 hipError_t launch_ctx_tokens(const int32_t* ctx, int B, int K, int32_t* tokens, hipStream_t st);
+hipError_t launch_stream_read(const void* src, size_t n16, uint32_t* sink, hipStream_t st);
 hipError_t launch_philox(uint64_t seed, uint64_t loop, int purpose, int B, int n, float* out,
                          hipStream_t st);
 

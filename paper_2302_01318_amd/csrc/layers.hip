@@ -108,3 +108,46 @@ hipError_t launch_kv_copy(int dtype, int to_cache, void* kc, void* vc, int H, in
 }
 
 }  // namespace sps
+
+namespace sps {
+
+// Streaming read of `n16` 16-byte words with the weight stream's nontemporal
+// loads: the device's attainable HBM read rate, against which the verify
+// step's kernels are measured. Each work-group reads one contiguous region,
+// four 16-byte loads in flight per thread (the best of a sweep over grid,
+// block, loads in flight and grid-stride vs contiguous regions: 512 x 256,
+// regions, 4 loads). The folded words are stored only on a value the data
+// cannot produce by chance in practice, which keeps every load live without
+// writing back.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void stream_read_kernel(const u32x4* __restrict__ src, size_t n16,
+                                                          uint32_t key, uint32_t* __restrict__ sink) {
+  constexpr int U = 4;
+  const size_t per = (n16 + gridDim.x - 1) / gridDim.x;
+  const size_t begin = static_cast<size_t>(blockIdx.x) * per;
+  const size_t end = begin + per < n16 ? begin + per : n16;
+  const size_t step = blockDim.x;
+  size_t i = begin + threadIdx.x;
+  uint32_t acc = 0;
+  for (; i + (U - 1) * step < end; i += U * step) {
+    u32x4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(src + i + u * step);
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  for (; i < end; i += step) {
+    const u32x4 v = __builtin_nontemporal_load(src + i);
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  if (acc == key) sink[0] = acc;
+}
+
+hipError_t launch_stream_read(const void* src, size_t n16, uint32_t* sink, hipStream_t st) {
+  hipLaunchKernelGGL(stream_read_kernel, dim3(512), dim3(256), 0, st, static_cast<const u32x4*>(src), n16,
+                     0x9e3779b9u, sink);
+  return hipGetLastError();
+}
+
+}  // namespace sps

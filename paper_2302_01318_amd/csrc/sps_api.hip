@@ -620,6 +620,13 @@ sps_status sps_profile_gemm_end(float* total_ms, int32_t* launches, double* byte
   return SPS_OK;
 }
 
+sps_status sps_stream_read(const void* src, size_t bytes, uint32_t* sink, void* stream) {
+  if (!src || !sink || bytes == 0 || bytes % 16 != 0 || reinterpret_cast<uintptr_t>(src) % 16 != 0)
+    return SPS_E_INVALID;
+  SPS_HIP(sps::launch_stream_read(src, bytes / 16, sink, as_stream(stream)));
+  return SPS_OK;
+}
+
 sps_status sps_device_error(void* stream, int32_t clear, int32_t* flags) {
   if (!flags) return SPS_E_INVALID;
   SPS_HIP(hipStreamSynchronize(as_stream(stream)));

@@ -83,6 +83,7 @@ _sig("sps_philox_uniforms", c_int32, [Philox, c_int32, c_int32, c_int32, P, P])
 _sig("sps_softmax", c_int32, [P, c_int32, c_int32, Sampling, P, P])
 _sig("sps_device_error", c_int32, [P, c_int32, ctypes.POINTER(c_int32)])
 _sig("sps_profile_gemm_begin", c_int32, [c_int32])
+_sig("sps_stream_read", c_int32, [P, c_size_t, P, P])
 _sig("sps_profile_gemm_end", c_int32, [ctypes.POINTER(c_float), ctypes.POINTER(c_int32),
                                        ctypes.POINTER(ctypes.c_double)])
 
@@ -90,7 +91,8 @@ EXPORTS = ["sps_status_string", "sps_abi_version", "sps_weight_bytes", "sps_pack
            "sps_model_create", "sps_model_destroy", "sps_kv_bytes", "sps_kv_create", "sps_kv_destroy",
            "sps_kv_write", "sps_kv_read", "sps_workspace_bytes", "sps_forward", "sps_verify_step",
            "sps_accept_resample", "sps_draft_step", "sps_commit", "sps_philox_uniforms", "sps_softmax",
-           "sps_device_error", "sps_profile_gemm_begin", "sps_profile_gemm_end"]
+           "sps_device_error", "sps_profile_gemm_begin", "sps_profile_gemm_end",
+           "sps_stream_read"]
 
 
 class SPSError(RuntimeError):
@@ -283,6 +285,14 @@ def profile_gemm_end():
     ms, n, b = c_float(0), c_int32(0), ctypes.c_double(0)
     check(lib.sps_profile_gemm_end(ctypes.byref(ms), ctypes.byref(n), ctypes.byref(b)), "sps_profile_gemm_end")
     return ms.value, n.value, b.value
+
+
+def stream_read(buf, nbytes, sink):
+    """One streaming read of the first `nbytes` of device tensor `buf`
+    (measurement helper: the attainable HBM read rate)."""
+    if nbytes > buf.numel() * buf.element_size():
+        raise ValueError("stream_read: %d bytes exceed the buffer" % nbytes)
+    check(lib.sps_stream_read(_ptr(buf), nbytes, _ptr(sink, torch.int32, "sink"), _stream()), "sps_stream_read")
 
 
 class Generator:

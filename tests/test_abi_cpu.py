@@ -84,6 +84,13 @@ def test_invalid_arguments_return_codes(sps):
     assert sps.lib.sps_softmax(one, 1, 40000, S(1.0, 5, 1.0), one, None) == 4
     assert sps.lib.sps_softmax(one, 1, 40000, S(1.0, 0, 0.9), one, None) == 4
     assert sps.lib.sps_device_error(None, 0, None) == 1
+    # streaming-read helper: zero, ragged or misaligned sizes, null pointers
+    sixteen = P(16)
+    assert sps.lib.sps_stream_read(sixteen, 0, sixteen, None) == 1
+    assert sps.lib.sps_stream_read(sixteen, 24, sixteen, None) == 1
+    assert sps.lib.sps_stream_read(P(8), 32, sixteen, None) == 1
+    assert sps.lib.sps_stream_read(None, 32, sixteen, None) == 1
+    assert sps.lib.sps_stream_read(sixteen, 32, None, None) == 1
 
 
 def test_handles_and_shape_checks(sps):

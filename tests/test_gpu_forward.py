@@ -159,3 +159,17 @@ def test_full_width_layer_batched(sps, shape, B, K):
     g = np.random.default_rng(100 * B + K)
     verify_parity(sps, shape.with_(n_layers=1), B, K, [int(x) for x in g.integers(200, 600, B)], 31 + B, 2e-2,
                   check_kv=False)
+
+
+@pytest.mark.gpu
+def test_stream_read_helper(sps):
+    """The streaming-read measurement helper reads without writing: the sink
+    keeps its value for a buffer whose folded words differ from the key."""
+    buf = torch.ones(1 << 20, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    sps.stream_read(buf, 4 << 20, sink)
+    sps.stream_read(buf, (4 << 20) - 48, sink)   # ragged tail past the unrolled loop
+    torch.cuda.synchronize()
+    assert int(sink.item()) == 0
+    with pytest.raises(ValueError):
+        sps.stream_read(buf, (4 << 20) + 16, sink)
