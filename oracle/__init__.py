@@ -19,9 +19,11 @@ Modules:
   model     decoder-only transformer forward, full recompute and KV-cached
             (Conditional Scoring section).
   generate  the SpS loop (Algorithm 2) and ArS (Algorithm 1).
+  fp8       weight-only FP8 (OCP E4M3, one fp32 scale per output row)
+            quantisation of the projection matrices.
 
 Every function is pinned by tests under ``tests/`` that check it against
 what the paper and mathematics fix. The one function without such a pin is
 listed in its module header as "parity unpinned".
 """
-from . import philox, sampling, accept, model, generate  # noqa: F401
+from . import philox, sampling, accept, model, generate, fp8  # noqa: F401
