@@ -37,8 +37,7 @@ GEMM_REPEATS = 8                 # back-to-back launches per event bracket in th
 CALIBRATION_BYTES = 1 << 30      # plain device copy whose HBM counters calibrate FETCH/WRITE_SIZE
 # Sources of the single-tile GEMM kernel (the one the traffic counters were taken on).
 GEMM_SOURCES = [os.path.join(ROOT, "paper_2302_01318_amd", "csrc", f) for f in ("gemm.hip", "gemm_epi.h", "common.h")]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
-MFMA_FILE = os.path.join(ROOT, "profiles", "gemm_mfma.json")
+PROFILES = os.path.join(ROOT, "profiles")
 STREAM_READ_BYTES = 8 << 30      # bytes of the packed weights read by the streaming-read ceiling
 
 
@@ -51,11 +50,16 @@ def source_digest(paths):
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
+def _profile_file(kind, weights):
+    """profiles/gemm_<kind>.json for bf16 weights, gemm_<kind>_fp8.json for FP8."""
+    return os.path.join(PROFILES, "gemm_%s%s.json" % (kind, "_fp8" if weights == "fp8" else ""))
+
+
+def measured_traffic(weights="bf16"):
     """HBM bytes per GEMM launch measured with rocprofv3 counters (see the
     profiles/ file), if they were taken on the current GEMM source."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(_profile_file("traffic", weights)) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
@@ -64,11 +68,11 @@ def measured_traffic():
     return t.get("hbm_bytes_per_launch")
 
 
-def measured_mfma():
+def measured_mfma(weights="bf16"):
     """MFMA utilisation of the GEMM launches from rocprofv3 counters (see the
     profiles/ file), if they were taken on the current GEMM source."""
     try:
-        with open(MFMA_FILE) as f:
+        with open(_profile_file("mfma", weights)) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
@@ -100,10 +104,10 @@ def verify_bytes(shape, B, K, ctx):
     """Algorithmic HBM bytes of one verify step: every weight once, the KV
     cache of every sequence once (prior context plus the K+1 new positions),
     the new keys/values written once, the logits written and read once."""
-    es = 2 if shape.dtype == "bf16" else 4
+    es = shape.act_bytes()
     M = B * (K + 1)
     HD = shape.n_heads * shape.head_dim
-    weights = shape.n_layers * shape.matrix_bytes_per_layer() + shape.vocab * shape.d_model * es
+    weights = shape.n_layers * shape.matrix_bytes_per_layer() + shape.matrix_bytes(shape.vocab, shape.d_model)
     gains = (2 * shape.n_layers + 1) * shape.d_model * 4
     embed_rows = M * shape.d_model * es
     kv_read = shape.n_layers * B * 2 * HD * (ctx + K + 1) * es
@@ -139,8 +143,8 @@ def cpu_baseline(shape, K, ctx):
     from oracle.model import ModelSpec
     from paper_2302_01318_amd import synth
     one = shape.with_(n_layers=1)
-    spec = ModelSpec(one.d_model, 1, one.n_heads, one.head_dim, one.d_ff, one.vocab, one.ffn, one.dtype,
-                     one.eps, one.rope_base)
+    spec = ModelSpec(one.d_model, 1, one.n_heads, one.head_dim, one.d_ff, one.vocab, one.ffn,
+                     "bf16" if one.dtype == "fp8" else one.dtype, one.eps, one.rope_base)
     f = lambda t: t.float().numpy()
     w = {k: synth.weight(one, k[0], k[1], 0) for k in synth.tensor_shapes(one)}
     W = {"embed": f(w[("embed", -1)]), "final_norm": f(w[("final_norm", -1)]), "unembed": f(w[("unembed", -1)]),
@@ -148,6 +152,9 @@ def cpu_baseline(shape, K, ctx):
                      "wv": f(w[("wv", 0)]), "wo": f(w[("wo", 0)]), "ffn_norm": f(w[("ffn_norm", 0)]),
                      "w1": f(w[("w1", 0)]), "w2": f(w[("w2", 0)])}]}
     del w
+    if one.dtype == "fp8":                   # the oracle's own quantisation, outside the timed region
+        from oracle import fp8
+        W = fp8.fp8_weights(W)
     cache = om.new_cache(spec, 1, ctx + K + 1)
     k, v = synth.kv_prior(one, 1, 0, 1, ctx)
     cache["k"][0, 0, :, :ctx] = k[0].double().numpy()
@@ -385,6 +392,8 @@ def main():
     ap.add_argument("--ctx", type=int, default=2048)
     ap.add_argument("--n-new", type=int, default=128)
     ap.add_argument("--shape", default="70b", choices=["70b", "7b"])
+    ap.add_argument("--weights", default="bf16", choices=["bf16", "fp8"],
+                    help="projection weights of target and draft: bf16, or weight-only FP8 (E4M3)")
     ap.add_argument("--no-e2e", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
@@ -418,6 +427,8 @@ def main():
 
     shape = configs.SEVENTY_B if args.shape == "70b" else configs.SEVEN_B
     dshape = configs.DRAFT_70B
+    if args.weights == "fp8":
+        shape, dshape = shape.with_(dtype="fp8"), dshape.with_(dtype="fp8")
     B, K, ctx = args.B, args.K, args.ctx
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
 
@@ -487,10 +498,10 @@ def main():
         log("gemm: %d launches, avg %.1f us, %.1f GB/s" % (g_n, g_avg_ms * 1e3, g_gbs))
         roofline = {"bound": "hbm", "kernel": "gemm_kernel (weight-streaming skinny GEMM, all linear layers)",
                     "achieved": round(g_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(g_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
+                    "frac": round(g_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(args.weights),
                     "launches_per_step": g_n // args.steps, "avg_launch_us": round(g_avg_ms * 1e3, 2),
                     "bytes_per_launch": g_bytes / g_n,
-                    "frac_of_stream_read": round(g_gbs / read_gbs, 4), "mfma": measured_mfma()}
+                    "frac_of_stream_read": round(g_gbs / read_gbs, 4), "mfma": measured_mfma(args.weights)}
     del kv, ws
 
     # ---- SpS and ArS tokens/s end to end ---------------------------------------------
@@ -542,6 +553,8 @@ def main():
         "metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16",
+        "weights": "fp8 e4m3, one fp32 scale per output row (exact bf16 conversion before the MFMA)"
+                   if args.weights == "fp8" else "bf16",
         "data": "synthetic: verify timing on random-init weights N(0,0.02), random bf16 prior KV, random tokens "
                 "and draft distributions; end to end on a seeded coupled target/draft pair (see e2e.pair)",
         "config": {"workload": "%s-shaped target verify step + softmax + fused accept/resample" % shape.name,

@@ -48,18 +48,26 @@ typedef enum {
 #define SPS_DEV_CAPACITY 4   /* KV write at a position >= T_cap (write skipped) */
 
 enum { SPS_FFN_GELU = 0, SPS_FFN_SWIGLU = 1 };
-enum { SPS_DTYPE_F32 = 0, SPS_DTYPE_BF16 = 1 };
+enum { SPS_DTYPE_F32 = 0, SPS_DTYPE_BF16 = 1, SPS_DTYPE_FP8 = 2 };
 
 /* Decoder-only transformer shape (Conditional Scoring section; Hyperparams
  * table). Pre-norm blocks, RMSNorm with learned gains, multi-head attention
  * with rotate-half rotary position encoding, FFN = GELU(tanh) with two
  * matrices or SwiGLU with three, untied embedding / unembedding, no biases.
  * Supported: d_model % 32 == 0, d_model <= 16384, head_dim in {64, 128},
- * (n_heads * head_dim) % 32 == 0, d_ff % 32 == 0, 2 <= vocab < 2^24. */
+ * (n_heads * head_dim) % 32 == 0, d_ff % 32 == 0, 2 <= vocab < 2^24.
+ *
+ * dtype SPS_DTYPE_FP8 is a weight-only FP8 model (the paper notes SpS is
+ * compatible with quantisation: Introduction; Modified Rejection Sampling
+ * section): the projection matrices (WQ, WK, WV, WO, W1, W3, W2, UNEMBED)
+ * are OCP FP8 E4M3 codes (bias 7, subnormals, no infinities, max 448) with
+ * one fp32 scale per output row; the embedding, the KV cache and the
+ * activations are those of a bf16 model, the gains fp32. It needs d_model,
+ * n_heads * head_dim and d_ff to be multiples of 64. */
 typedef struct {
   int32_t d_model, n_layers, n_heads, head_dim, d_ff, vocab;
   int32_t ffn_kind; /* SPS_FFN_GELU or SPS_FFN_SWIGLU                         */
-  int32_t dtype;    /* SPS_DTYPE_F32 or SPS_DTYPE_BF16: weights, KV, GEMM inputs */
+  int32_t dtype;    /* SPS_DTYPE_F32 / _BF16: weights, KV, GEMM inputs; _FP8 above */
   float rms_eps;    /* e.g. 1e-5                                                */
   float rope_base;  /* e.g. 10000                                               */
 } sps_config;
@@ -95,7 +103,8 @@ typedef struct {
 } sps_sampling;
 
 /* Weight tensors, in canonical row-major nn.Linear orientation [out][in] and
- * the model dtype, except the gains (always fp32):
+ * the model dtype (bf16 for every matrix of an FP8 model), except the gains
+ * (always fp32):
  *   EMBED [V][d], FINAL_NORM [d], UNEMBED [V][d],
  *   per layer: ATTN_NORM [d], WQ/WK/WV [H*Dh][d], WO [d][H*Dh], FFN_NORM [d],
  *   W1 [F][d] (GELU up, or SwiGLU gate), W3 [F][d] (SwiGLU up only),
@@ -116,15 +125,33 @@ int32_t sps_abi_version(void);
 
 /* Bytes of the packed weight buffer for cfg (0 if cfg is invalid). The packed
  * layout stores every projection as 16 x 32 tiles in the register order of
- * the gfx950 MFMA B operand, so each wavefront load is one contiguous KiB. */
+ * the gfx950 MFMA B operand, so each wavefront load is one contiguous KiB.
+ * FP8 models store 16 x 64 tiles of one-byte codes (lane l: row l % 16,
+ * columns 8 (l / 16) .. +7 of the tile's first 32 columns, then the same
+ * columns of its second 32), each projection followed by its fp32 row
+ * scales in packed row order. */
 size_t sps_weight_bytes(const sps_config* cfg);
 
 /* Pack one canonical tensor `src` (layout above) into its slot of the packed
  * buffer `packed` (sps_weight_bytes(cfg) bytes). `layer` is ignored for
  * EMBED, FINAL_NORM and UNEMBED. W3 is only valid for SwiGLU. Every tensor
- * of the model must be packed once before the model is used. */
+ * of the model must be packed once before the model is used.
+ * FP8 models quantise each bf16 matrix row n here: scale s_n = fp32(max_k
+ * |w[n][k]|) / 448 (1 for an all-zero row), code = the E4M3 value nearest to
+ * fp32(w[n][k]) / s_n (fp32 divisions, correctly rounded), ties to the even
+ * code, |quotient| clamped to 448 first; the model computes with
+ * s_n * value(code). */
 sps_status sps_pack_weight(const sps_config* cfg, int32_t tensor, int32_t layer,
                            const void* src, void* packed, void* stream);
+
+/* Where tensor `tensor` of layer `layer` lives in the packed buffer (host
+ * outputs): its slot's byte offset and size, and for the projections of an
+ * FP8 model the byte offset of their fp32 row scales (0 otherwise). WQ, WK
+ * and WV share the fused QKV slot (packed rows: q and k heads with rotary
+ * partners side by side, then v), W1 and W3 of a SwiGLU model the
+ * interleaved gate / up slot (8 gate rows, then the matching 8 up rows). */
+sps_status sps_weight_slot(const sps_config* cfg, int32_t tensor, int32_t layer, size_t* offset /*host*/,
+                           size_t* bytes /*host*/, size_t* scale_offset /*host*/);
 
 /* Create a host handle viewing `packed` (not copied, not owned). */
 sps_status sps_model_create(const sps_config* cfg, void* packed, sps_model_t* out /*host*/);
@@ -272,6 +299,12 @@ sps_status sps_profile_gemm_end(float* total_ms /*host*/, int32_t* launches /*ho
  * are compared with. SPS_E_INVALID on null pointers, a misaligned `src` or
  * a size that is zero or not a multiple of 16. */
 sps_status sps_stream_read(const void* src, size_t bytes, uint32_t* sink, void* stream);
+
+/* Decode n (a multiple of 16) OCP FP8 E4M3 codes at `codes` (16-byte
+ * aligned) into fp32 values `out`, with the conversion the FP8-weight GEMM
+ * applies to its weight codes. SPS_E_INVALID on null pointers, misalignment
+ * or a bad n. */
+sps_status sps_fp8_decode(const uint8_t* codes, int32_t n, float* out, void* stream);
 
 /* Synchronise `stream`, return the current device's sticky error bits in
  * *flags (host) and clear them if `clear` != 0. */

@@ -19,7 +19,7 @@ class ModelShape:
     d_ff: int
     vocab: int
     ffn: str = "gelu"          # "gelu" or "swiglu"
-    dtype: str = "bf16"        # "f32" or "bf16"
+    dtype: str = "bf16"        # "f32", "bf16" or "fp8" (FP8 E4M3 projections, bf16 activations / KV)
     eps: float = 1e-5
     rope_base: float = 10000.0
 
@@ -31,11 +31,25 @@ class ModelShape:
         ffn = (2 if self.ffn == "gelu" else 3) * d * F
         return self.n_layers * (4 * d * HD + ffn + 2 * d) + 2 * V * d + d
 
+    def act_bytes(self):
+        """Bytes per element of the embedding, the KV cache and q."""
+        return 4 if self.dtype == "f32" else 2
+
+    def weight_bytes(self):
+        """Bytes per element of a projection matrix."""
+        return {"f32": 4, "bf16": 2, "fp8": 1}[self.dtype]
+
+    def matrix_bytes(self, rows, cols):
+        """Bytes a forward streams for one [rows][cols] projection: the
+        elements, plus an fp32 scale per row for FP8."""
+        return rows * cols * self.weight_bytes() + (4 * rows if self.dtype == "fp8" else 0)
+
     def matrix_bytes_per_layer(self):
         """Bytes of the projection matrices of one block (what a forward streams)."""
         d, F, HD = self.d_model, self.d_ff, self.n_heads * self.head_dim
-        es = 2 if self.dtype == "bf16" else 4
-        return es * (4 * d * HD + (2 if self.ffn == "gelu" else 3) * d * F)
+        mb = self.matrix_bytes
+        ffn = 2 * mb(F, d) + mb(d, F) if self.ffn == "swiglu" else mb(F, d) + mb(d, F)
+        return mb(3 * HD, d) + mb(d, HD) + ffn
 
 
 # Tiny end-to-end pair (fp32): target and draft share the vocabulary.

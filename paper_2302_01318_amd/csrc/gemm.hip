@@ -26,6 +26,14 @@
 // round robin, each accumulating one 16 x 16 fp32 tile per (n-tile, M tile)
 // with MFMA; the waves' partials are summed in LDS in a fixed order.
 //
+// FP8 weights (weight-only FP8 models): codes are stored in 16 x 64 tiles,
+// one per pair of 32-deep k-tiles, ordered [nt][k-tile pair]. Lane l holds 16
+// bytes: row 16 nt + l % 16, columns 8 (l / 16) .. +7 of the pair's first
+// k-tile, then the same columns of its second, so one wave-wide 16 B load is
+// still one contiguous KiB and yields two B fragments after an exact
+// conversion to bf16 (fp8.h). The row scale multiplies the output in the
+// epilogue: Y[m][n] = scale[n] * sum_k X[m][k] value(code[n][k]).
+//
 // Epilogues fuse the per-token work around each matmul:
 //  * input RMSNorm: the producer of a normed activation writes u = h * gain
 //    and per-column-group sums of squares; the consumer multiplies its
@@ -37,13 +45,15 @@
 //    side in one 16-row tile) and the KV-cache append;
 //  * FFN: GELU or SwiGLU.
 #include "common.h"
+#include "fp8.h"
 #include "gemm_epi.h"
 #include "launch.h"
 
 namespace sps {
 
-template <typename T, int MT, int NTW, int WAVES, int U, int EPI>
+template <typename T, int MT, int NTW, int WAVES, int U, int EPI, bool W8>
 __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
+  static_assert(!W8 || (sizeof(T) == 2 && U % 2 == 0), "FP8 weights: bf16 activations, whole k-tile pairs");
   constexpr int kTile = 512;  // elements per 16 x 32 tile
   constexpr int kRows = ActRows<T>::kRows;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -75,6 +85,58 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  if constexpr (W8) {
+    // Code tile pair kp of n-tile j: 64 lanes x 16 B at wq[j] + 64 kp.
+    const u32x4* wq[NTW];
+#pragma unroll
+    for (int j = 0; j < NTW; ++j)
+      wq[j] = reinterpret_cast<const u32x4*>(static_cast<const uint8_t*>(p.W) +
+                                             static_cast<size_t>(wv[j] ? nt0 + j : 0) * KT * kTile) + lane;
+    // One pair: two activation fragments, one code load per n-tile.
+    auto pair = [&](int kt, const u32x4 (&raw)[NTW], const Frag<T> (&a0)[MT], const Frag<T> (&a1)[MT]) {
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) {
+        Frag<T> b0, b1;
+        e4m3x16_to_frags(raw[j], b0, b1);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          acc[j][mt] = mma8(acc[j][mt], a0[mt], b0);
+          acc[j][mt] = mma8(acc[j][mt], a1[mt], b1);
+        }
+      }
+    };
+    int kb = wave * U;
+    for (; kb + U <= KT; kb += WAVES * U) {
+      u32x4 raw[U / 2][NTW];
+      Frag<T> a[U][MT];
+#pragma unroll
+      for (int u = 0; u < U / 2; ++u)
+#pragma unroll
+        for (int j = 0; j < NTW; ++j)
+          raw[u][j] = wv[j] ? __builtin_nontemporal_load(wq[j] + static_cast<size_t>(kb / 2 + u) * 64)
+                            : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) a[u][mt] = xv[mt] ? load_frag(xp[mt] + (kb + u) * 32) : Frag<T>::zero();
+#pragma unroll
+      for (int u = 0; u < U / 2; ++u) pair(kb + 2 * u, raw[u], a[2 * u], a[2 * u + 1]);
+    }
+    // Ragged last chunk: KT is even, so pairs stay whole.
+    for (int kt = kb; kt < KT && kt < kb + U; kt += 2) {
+      u32x4 raw[NTW];
+      Frag<T> a0[MT], a1[MT];
+#pragma unroll
+      for (int j = 0; j < NTW; ++j)
+        raw[j] = wv[j] ? __builtin_nontemporal_load(wq[j] + static_cast<size_t>(kt / 2) * 64) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        a0[mt] = xv[mt] ? load_frag(xp[mt] + kt * 32) : Frag<T>::zero();
+        a1[mt] = xv[mt] ? load_frag(xp[mt] + (kt + 1) * 32) : Frag<T>::zero();
+      }
+      pair(kt, raw, a0, a1);
+    }
+  } else {
   int kb = wave * U;
   for (; kb + U <= KT; kb += WAVES * U) {
     Frag<T> b[NTW][U];
@@ -111,6 +173,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
         }
       }
     }
+  }
   }
 
   // Sum the waves' partials in LDS (fixed order), then the epilogue.
@@ -160,8 +223,11 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
     if (nt >= p.NT || m >= M) continue;
     const int gm = p.m0 + m;
     const float rs = s_rs[m];
-    const float v = out_value(j, mt, r, ln) * rs;
-    const float v2 = (EPI == kEpiSwiglu || EPI == kEpiQkv) && col < 8 ? out_value(j, mt, r, ln + 8) * rs : 0.f;
+    const float sc = W8 ? p.wscale[nt * 16 + col] : 1.f;
+    const float v = out_value(j, mt, r, ln) * rs * sc;
+    const float v2 = (EPI == kEpiSwiglu || EPI == kEpiQkv) && col < 8
+                         ? out_value(j, mt, r, ln + 8) * rs * (W8 ? p.wscale[nt * 16 + col + 8] : 1.f)
+                         : 0.f;
     const float sq = epilogue_element<T, EPI>(p, gm, nt, col, v, v2);
     if (EPI == kEpiResid && nt * 16 + col < p.n_valid) s_sq[m][j * 16 + col] = sq;
   }
@@ -180,15 +246,15 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
 // per chunk. A single M tile (every verify and draft step) streams two n-tiles
 // per wave with 8-wave work-groups on large matrices (single_tile_ntw), else
 // one n-tile per wave with 16-wave work-groups.
-template <typename T, int MT, int NTW, int WAVES, int U>
+template <typename T, int MT, int NTW, int WAVES, int U, bool W8 = false>
 static hipError_t gemm_launch(const GemmParams& p, hipStream_t st) {
   const dim3 grid((p.NT + NTW - 1) / NTW), block(WAVES * 64);
   switch (p.epi) {
-    case kEpiStore: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiStore>), grid, block, 0, st, p); break;
-    case kEpiGelu: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiGelu>), grid, block, 0, st, p); break;
-    case kEpiSwiglu: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiSwiglu>), grid, block, 0, st, p); break;
-    case kEpiResid: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiResid>), grid, block, 0, st, p); break;
-    default: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiQkv>), grid, block, 0, st, p); break;
+    case kEpiStore: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiStore, W8>), grid, block, 0, st, p); break;
+    case kEpiGelu: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiGelu, W8>), grid, block, 0, st, p); break;
+    case kEpiSwiglu: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiSwiglu, W8>), grid, block, 0, st, p); break;
+    case kEpiResid: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiResid, W8>), grid, block, 0, st, p); break;
+    default: hipLaunchKernelGGL((gemm_kernel<T, MT, NTW, WAVES, U, kEpiQkv, W8>), grid, block, 0, st, p); break;
   }
   return hipGetLastError();
 }
@@ -230,25 +296,55 @@ static hipError_t gemm_dispatch_bf16(const GemmParams& p, hipStream_t st) {
   return gemm_launch<T, 1, 1, 16, 4>(p, st);
 }
 
-// One launch covers up to 160 rows (20 M tiles of 8 bf16 rows, 10 of 16 fp32).
-int gemm_max_rows(int dtype) { return dtype == 1 ? 20 * ActRows<bf16>::kRows : 10 * ActRows<float>::kRows; }
+// FP8 weights, one M tile (8 rows; more rows take several launches), 8
+// k-tiles (4 code loads of 16 B per lane and n-tile) per chunk. From a
+// launch-shape sweep over the 70B, 7B and draft matrices at 1 and 5 rows:
+// two n-tiles per wave with 8-wave work-groups from 512 n-tiles (the
+// activation fragment feeds two MFMA pairs), else one n-tile and 16 waves
+// (enough work-groups for the 3072- and 4096-wide outputs).
+static int fp8_ntw(int NT, int) { return NT % 2 == 0 && NT >= 512 ? 2 : 1; }
+
+static hipError_t gemm_dispatch_fp8(const GemmParams& p, hipStream_t st) {
+  using T = bf16;
+  if (p.M > ActRows<T>::kRows || !p.wscale || p.KT % 2) return hipErrorInvalidValue;
+  if (fp8_ntw(p.NT, p.KT) == 2) return gemm_launch<T, 1, 2, 8, 8, true>(p, st);
+  return gemm_launch<T, 1, 1, 16, 8, true>(p, st);
+}
+
+// One launch covers up to 160 rows (20 M tiles of 8 bf16 rows, 10 of 16
+// fp32); FP8-weight launches one M tile of 8 rows.
+int gemm_max_rows(int dtype) {
+  return dtype == 1 ? 20 * ActRows<bf16>::kRows : dtype == 2 ? ActRows<bf16>::kRows : 10 * ActRows<float>::kRows;
+}
 
 bool gemm_is_wide(int dtype, int Mtot) { return dtype == 1 && Mtot > ActRows<bf16>::kRows; }
 
 int gemm_groups(int dtype, int NT, int KT, int Mtot) {
   if (gemm_is_wide(dtype, Mtot)) return wide_groups(NT);
+  if (dtype == 2) {
+    const int ntw = fp8_ntw(NT, KT);
+    return (NT + ntw - 1) / ntw;
+  }
   const int rows = dtype == 1 ? ActRows<bf16>::kRows : ActRows<float>::kRows;
   const int ntw = (Mtot <= rows) ? single_tile_ntw(NT, KT) : 1;
   return (NT + ntw - 1) / ntw;
 }
 
 hipError_t launch_gemm(int dtype, const GemmParams& p, hipStream_t st) {
-  return dtype == 1 ? gemm_dispatch_bf16(p, st) : gemm_dispatch_f32(p, st);
+  return dtype == 2 ? gemm_dispatch_fp8(p, st) : dtype == 1 ? gemm_dispatch_bf16(p, st) : gemm_dispatch_f32(p, st);
 }
 
 // ---------------------------------------------------------------------------
 // Packing canonical [n][k] rows into tile order.
 // ---------------------------------------------------------------------------
+// Packed row of canonical row n: kind 0 row_off + n; kind 1 SwiGLU gate /
+// up interleaving; kind 2 rotary partners side by side.
+__device__ __forceinline__ int packed_row(int n, int kind, int row_off, int dh) {
+  return kind == 0   ? row_off + n
+         : kind == 1 ? (n / 8) * 16 + row_off * 8 + (n % 8)
+                     : row_off + (n / dh) * dh + rope_pack_index(n % dh, dh);
+}
+
 template <typename T>
 __global__ void pack_kernel(const T* __restrict__ src, int n_src, int Kd, T* __restrict__ dst, int KT,
                             int kind, int row_off, int dh) {
@@ -256,9 +352,7 @@ __global__ void pack_kernel(const T* __restrict__ src, int n_src, int Kd, T* __r
   const long i = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i >= static_cast<long>(n_src) * groups) return;
   const int n = static_cast<int>(i / groups), k = static_cast<int>(i % groups) * 8;
-  const int nf = kind == 0   ? row_off + n
-                 : kind == 1 ? (n / 8) * 16 + row_off * 8 + (n % 8)
-                             : row_off + (n / dh) * dh + rope_pack_index(n % dh, dh);
+  const int nf = packed_row(n, kind, row_off, dh);
   const int nt = nf / 16, rr = nf % 16, kt = k / 32, grp = (k % 32) / 8;
   const size_t o = ((static_cast<size_t>(nt) * KT + kt) * 64 + rr + 16 * grp) * 8;
   const T* s = src + static_cast<size_t>(n) * Kd + k;
@@ -289,6 +383,77 @@ static hipError_t pack_t(const void* src, int n_src, int Kd, void* dst, int KT, 
   if (zwork > 0)
     hipLaunchKernelGGL(pack_zero_kernel<T>, dim3(static_cast<unsigned>((zwork + 255) / 256)), dim3(256), 0,
                        st, static_cast<T*>(dst), KT, zero_from, zero_to);
+  return hipGetLastError();
+}
+
+// Byte offset of code (packed row nf, column k) in an FP8 projection of KT
+// k-tiles (16 x 64 tiles of k-tile pairs, see the header comment).
+__device__ __forceinline__ size_t fp8_offset(int nf, int k, int KT) {
+  const int nt = nf / 16, rr = nf % 16, kp = k / 64, half = (k % 64) / 32, grp = (k % 32) / 8;
+  return ((static_cast<size_t>(nt) * (KT / 2) + kp) * 64 + rr + 16 * grp) * 16 + half * 8 + (k % 8);
+}
+
+// One work-group per canonical row: the row's largest |w| (exact in fp32),
+// its scale, then every code.
+__global__ __launch_bounds__(256) void pack_fp8_kernel(const bf16* __restrict__ src, int Kd,
+                                                       uint8_t* __restrict__ dst, float* __restrict__ scales,
+                                                       int KT, int kind, int row_off, int dh) {
+  __shared__ float red[16];
+  const int n = blockIdx.x;
+  const bf16* s = src + static_cast<size_t>(n) * Kd;
+  float amax = 0.f;
+  for (int k = threadIdx.x; k < Kd; k += blockDim.x) amax = fmaxf(amax, fabsf(static_cast<float>(s[k])));
+  amax = block_max(amax, red);
+  const float sc = amax > 0.f ? __fdiv_rn(amax, 448.0f) : 1.0f;
+  const int nf = packed_row(n, kind, row_off, dh);
+  if (threadIdx.x == 0) scales[nf] = sc;
+  for (int k = threadIdx.x; k < Kd; k += blockDim.x)
+    dst[fp8_offset(nf, k, KT)] = static_cast<uint8_t>(e4m3_encode(__fdiv_rn(static_cast<float>(s[k]), sc)));
+}
+
+// Padding rows [zero_from, zero_to): code 0, scale 1.
+__global__ void pack_zero_fp8_kernel(uint8_t* __restrict__ dst, float* __restrict__ scales, int KT, int zero_from,
+                                     int zero_to) {
+  const int Kd = KT * 32;
+  const long i = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= static_cast<long>(zero_to - zero_from) * Kd) return;
+  const int nf = zero_from + static_cast<int>(i / Kd), k = static_cast<int>(i % Kd);
+  dst[fp8_offset(nf, k, KT)] = 0;
+  if (k == 0) scales[nf] = 1.0f;
+}
+
+hipError_t launch_pack_fp8(const void* src, int n_src, int Kd, void* dst, float* scales, int KT, int kind,
+                           int row_off, int dh, int zero_from, int zero_to, hipStream_t st) {
+  if (KT % 2 || Kd != KT * 32) return hipErrorInvalidValue;
+  if (n_src > 0)
+    hipLaunchKernelGGL(pack_fp8_kernel, dim3(n_src), dim3(256), 0, st, static_cast<const bf16*>(src), Kd,
+                       static_cast<uint8_t*>(dst), scales, KT, kind, row_off, dh);
+  const long zwork = static_cast<long>(zero_to - zero_from) * Kd;
+  if (zwork > 0)
+    hipLaunchKernelGGL(pack_zero_fp8_kernel, dim3(static_cast<unsigned>((zwork + 255) / 256)), dim3(256), 0, st,
+                       static_cast<uint8_t*>(dst), scales, KT, zero_from, zero_to);
+  return hipGetLastError();
+}
+
+// E4M3 codes to fp32 with the GEMM's conversion: 16 codes per thread.
+__global__ void fp8_decode_kernel(const u32x4* __restrict__ codes, int n16, float* __restrict__ out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n16) return;
+  Frag<bf16> lo, hi;
+  e4m3x16_to_frags(codes[i], lo, hi);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    out[static_cast<size_t>(i) * 16 + e] = static_cast<float>(lo.v[e]);
+    out[static_cast<size_t>(i) * 16 + 8 + e] = static_cast<float>(hi.v[e]);
+  }
+}
+
+hipError_t launch_fp8_decode(const void* codes, int n, float* out, hipStream_t st) {
+  if (n % 16) return hipErrorInvalidValue;
+  const int n16 = n / 16;
+  if (n16 > 0)
+    hipLaunchKernelGGL(fp8_decode_kernel, dim3((n16 + 255) / 256), dim3(256), 0, st,
+                       static_cast<const u32x4*>(codes), n16, out);
   return hipGetLastError();
 }
 

@@ -7,7 +7,9 @@ namespace sps {
 
 enum Epilogue { kEpiStore = 0, kEpiGelu = 1, kEpiSwiglu = 2, kEpiResid = 3, kEpiQkv = 4 };
 
-// Y = X W^T for a packed weight W (see gemm.hip). dtype: 0 fp32, 1 bf16.
+// Y = X W^T for a packed weight W (see gemm.hip). dtype: 0 fp32, 1 bf16,
+// 2 FP8 (E4M3) weight codes with per-row fp32 scales `wscale` and bf16
+// activations: Y[m][n] = wscale[n] * sum_k X[m][k] value(W[n][k]).
 // X, act and u are in the activation format (common.h: fp32, or bf16 hi/lo
 // planes `*plane` elements apart). Rows are global rows m0 .. m0+M-1 of a
 // forward over Mtot rows.
@@ -28,6 +30,7 @@ struct GemmParams {
   const void* X; int ldx; size_t xplane;
   int M, m0, Mtot;
   const void* W; int NT, KT, n_valid;
+  const float* wscale;     // FP8 weights: scale of every packed row (else NULL)
   const float* ss_in; int ng_in; float inv_d, eps;
   float* out; int ldo;
   void* act; int lda; size_t aplane;
@@ -58,6 +61,14 @@ hipError_t launch_gemm_wide(const GemmParams& p, const WidePlan& w, hipStream_t 
 // [zero_from, zero_to) are cleared.
 hipError_t launch_pack(int dtype, const void* src, int n_src, int Kd, void* dst, int KT, int kind,
                        int row_off, int dh, int zero_from, int zero_to, hipStream_t st);
+// The same for an FP8 projection: bf16 rows src are quantised per row (scale
+// = max |row| / 448, code = nearest E4M3 of w / scale, ties to even, clamped
+// to +-448) into 16 x 64 code tiles (see gemm.hip); the scale of packed row
+// map(n) goes to scales[map(n)]. Padding rows get code 0 and scale 1.
+hipError_t launch_pack_fp8(const void* src, int n_src, int Kd, void* dst, float* scales, int KT, int kind,
+                           int row_off, int dh, int zero_from, int zero_to, hipStream_t st);
+// E4M3 codes -> fp32 values with the GEMM's conversion (n % 16 == 0).
+hipError_t launch_fp8_decode(const void* codes, int n, float* out, hipStream_t st);
 
 // Activations (x, attention output o, FFN hidden) are in the activation
 // format of common.h; `xplane` is the element distance of the lo plane.

@@ -32,41 +32,59 @@ bool valid_config(const sps_config* c) {
   if (c->d_ff < 32 || c->d_ff % 32) return false;
   if (c->vocab < 2 || c->vocab >= (1 << 24)) return false;
   if (c->ffn_kind != SPS_FFN_GELU && c->ffn_kind != SPS_FFN_SWIGLU) return false;
-  if (c->dtype != SPS_DTYPE_F32 && c->dtype != SPS_DTYPE_BF16) return false;
+  if (c->dtype != SPS_DTYPE_F32 && c->dtype != SPS_DTYPE_BF16 && c->dtype != SPS_DTYPE_FP8) return false;
+  // FP8 codes are packed in 64-deep k-tile pairs: every contraction depth of
+  // the forward (d_model, n_heads * head_dim, d_ff) must be a multiple of 64.
+  if (c->dtype == SPS_DTYPE_FP8 && (c->d_model % 64 || (c->n_heads * c->head_dim) % 64 || c->d_ff % 64))
+    return false;
   if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f)) return false;
   return true;
 }
 
-// Byte offsets of every tensor in the packed weight buffer.
+// Element type of the activations, the embedding and the KV cache: fp32
+// for fp32 models, bf16 for bf16 and FP8-weight models.
+int act_dtype(const sps_config& c) { return c.dtype == SPS_DTYPE_F32 ? 0 : 1; }
+
+// Byte offsets of every tensor in the packed weight buffer. For FP8 models
+// each projection's codes are followed by its fp32 row scales (`*_sc`).
 struct Layout {
-  int es, d, L, H, DH, HD, F, V, NU, N1;
-  bool swiglu;
-  size_t embed, final_norm, unembed, layer0, layer_stride;
-  size_t l_attn_norm, l_ffn_norm, l_qkv, l_o, l_w1, l_w2;
+  int es, wes, d, L, H, DH, HD, F, V, NU, N1;   // es: activation / KV element bytes; wes: weight
+  bool swiglu, fp8;
+  size_t embed, final_norm, unembed, unembed_sc, layer0, layer_stride;
+  size_t l_attn_norm, l_ffn_norm, l_qkv, l_o, l_w1, l_w2, l_qkv_sc, l_o_sc, l_w1_sc, l_w2_sc;
   size_t total;
 };
 
 Layout make_layout(const sps_config* c) {
   Layout L{};
-  L.es = c->dtype == SPS_DTYPE_BF16 ? 2 : 4;
+  L.es = c->dtype == SPS_DTYPE_F32 ? 4 : 2;
+  L.fp8 = c->dtype == SPS_DTYPE_FP8;
+  L.wes = L.fp8 ? 1 : L.es;
   L.d = c->d_model; L.L = c->n_layers; L.H = c->n_heads; L.DH = c->head_dim;
   L.HD = L.H * L.DH; L.F = c->d_ff; L.V = c->vocab;
   L.NU = (L.V + 15) / 16 * 16;
   L.swiglu = c->ffn_kind == SPS_FFN_SWIGLU;
   L.N1 = L.swiglu ? 2 * L.F : L.F;
-  const size_t es = L.es;
+  const size_t es = L.es, wes = L.wes;
+  // Row scales of a projection with n packed rows (FP8 models only).
+  auto scales = [&](size_t n) { return L.fp8 ? align256(n * 4) : 0; };
   size_t o = 0;
   L.embed = o; o = align256(o + static_cast<size_t>(L.V) * L.d * es);
   L.final_norm = o; o = align256(o + static_cast<size_t>(L.d) * 4);
-  L.unembed = o; o = align256(o + static_cast<size_t>(L.NU) * L.d * es);
+  L.unembed = o; o = align256(o + static_cast<size_t>(L.NU) * L.d * wes);
+  L.unembed_sc = o; o += scales(L.NU);
   L.layer0 = o;
   size_t lo = 0;
   L.l_attn_norm = lo; lo = align256(lo + static_cast<size_t>(L.d) * 4);
   L.l_ffn_norm = lo; lo = align256(lo + static_cast<size_t>(L.d) * 4);
-  L.l_qkv = lo; lo = align256(lo + static_cast<size_t>(3) * L.HD * L.d * es);
-  L.l_o = lo; lo = align256(lo + static_cast<size_t>(L.d) * L.HD * es);
-  L.l_w1 = lo; lo = align256(lo + static_cast<size_t>(L.N1) * L.d * es);
-  L.l_w2 = lo; lo = align256(lo + static_cast<size_t>(L.d) * L.F * es);
+  L.l_qkv = lo; lo = align256(lo + static_cast<size_t>(3) * L.HD * L.d * wes);
+  L.l_qkv_sc = lo; lo += scales(static_cast<size_t>(3) * L.HD);
+  L.l_o = lo; lo = align256(lo + static_cast<size_t>(L.d) * L.HD * wes);
+  L.l_o_sc = lo; lo += scales(L.d);
+  L.l_w1 = lo; lo = align256(lo + static_cast<size_t>(L.N1) * L.d * wes);
+  L.l_w1_sc = lo; lo += scales(L.N1);
+  L.l_w2 = lo; lo = align256(lo + static_cast<size_t>(L.d) * L.F * wes);
+  L.l_w2_sc = lo; lo += scales(L.d);
   L.layer_stride = lo;
   L.total = L.layer0 + L.layer_stride * L.L;
   return L;
@@ -86,7 +104,7 @@ void forward_gemms(const Layout& L, int out[5][2]) {
 
 WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
   WsLayout w{};
-  const int dt = L.es == 2 ? 1 : 0;
+  const int dt = L.fp8 ? SPS_DTYPE_FP8 : L.es == 2 ? SPS_DTYPE_BF16 : SPS_DTYPE_F32;   // GEMM dtype
   const size_t M = static_cast<size_t>(B) * Mps;
   const size_t NP = sps::attn_partials(T_cap);
   const size_t ng = (L.d + 15) / 16;   // column groups a residual GEMM can produce
@@ -165,6 +183,10 @@ namespace {
 char* layer_ptr(const sps_model_s* m, int l, size_t off) {
   return m->base + m->L.layer0 + m->L.layer_stride * l + off;
 }
+// Row scales of a projection of layer l (FP8 models), else NULL.
+const float* scale_ptr(const sps_model_s* m, int l, size_t off) {
+  return m->L.fp8 ? reinterpret_cast<const float*>(layer_ptr(m, l, off)) : nullptr;
+}
 void* kv_k(const sps_kv_s* kv, int l) { return kv->buf + kv->plane_bytes * (2 * static_cast<size_t>(l)); }
 void* kv_v(const sps_kv_s* kv, int l) { return kv->buf + kv->plane_bytes * (2 * static_cast<size_t>(l) + 1); }
 
@@ -204,9 +226,10 @@ sps_status gemm(int dtype, GemmParams p, hipStream_t st) {
       e0 = g_prof.ev[g_prof.used];
       e1 = g_prof.ev[g_prof.used + 1];
       g_prof.used += 2;
-      const double wes = dtype == 1 ? 2.0 : 4.0;
+      const double wes = dtype == SPS_DTYPE_FP8 ? 1.0 : dtype == SPS_DTYPE_BF16 ? 2.0 : 4.0;
       const double rows_w = p.epi == sps::kEpiSwiglu ? 2.0 * p.n_valid : static_cast<double>(p.n_valid);
-      g_prof.bytes.push_back(rows_w * p.KT * 32 * wes + 4.0 * p.M * p.KT * 32 + 4.0 * p.M * p.n_valid);
+      const double scale_bytes = dtype == SPS_DTYPE_FP8 ? 4.0 * rows_w : 0.0;
+      g_prof.bytes.push_back(rows_w * p.KT * 32 * wes + scale_bytes + 4.0 * p.M * p.KT * 32 + 4.0 * p.M * p.n_valid);
       SPS_HIP(hipEventRecord(e0, st));
     }
     // Repeats redo the launch's work (a residual epilogue adds its output
@@ -227,7 +250,8 @@ sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t*
                         int Mps, int pos_offset, float* logits, char* ws_base, const WsLayout& ws, int* err,
                         hipStream_t st) {
   const Layout& L = m->L;
-  const int dt = m->cfg.dtype;
+  const int dt = m->cfg.dtype;             // GEMM dtype (weight format)
+  const int adt = act_dtype(m->cfg);       // activations, embedding, KV cache
   const int M = B * Mps;
   float* h = reinterpret_cast<float*>(ws_base + ws.h);
   void* x = ws_base + ws.x;
@@ -249,7 +273,7 @@ sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t*
   base.eps = m->cfg.rms_eps;
   base.part = reinterpret_cast<float*>(ws_base + ws.gpart);
 
-  SPS_HIP(sps::launch_embed(dt, tokens, tok_stride, Mps, M, m->base + L.embed, L.V, L.d,
+  SPS_HIP(sps::launch_embed(adt, tokens, tok_stride, Mps, M, m->base + L.embed, L.V, L.d,
                             reinterpret_cast<const float*>(layer_ptr(m, 0, L.l_attn_norm)), h, x, uplane, ss_cur,
                             err, st));
   int ng = 1;
@@ -257,6 +281,7 @@ sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t*
     GemmParams p = base;                     // QKV: norm scale, rotary encoding, KV append
     p.X = x; p.ldx = L.d; p.xplane = uplane;
     p.W = layer_ptr(m, l, L.l_qkv); p.NT = 3 * L.HD / 16; p.KT = KTd; p.n_valid = 3 * L.HD;
+    p.wscale = scale_ptr(m, l, L.l_qkv_sc);
     p.ss_in = ss_cur; p.ng_in = ng;
     p.lengths = kv->lengths; p.pos_offset = pos_offset; p.Mps = Mps; p.H = L.H; p.DH = L.DH;
     p.rope_base = m->cfg.rope_base; p.T_cap = kv->T_cap; p.q = q; p.kc = kv_k(kv, l); p.vc = kv_v(kv, l);
@@ -264,12 +289,13 @@ sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t*
     sps_status s = gemm(dt, p, st);
     if (s != SPS_OK) return s;
 
-    SPS_HIP(sps::launch_attention(dt, q, kv_k(kv, l), kv_v(kv, l), kv->lengths, pos_offset, B, Mps, L.H, L.DH,
+    SPS_HIP(sps::launch_attention(adt, q, kv_k(kv, l), kv_v(kv, l), kv->lengths, pos_offset, B, Mps, L.H, L.DH,
                                   kv->T_cap, apart, o, oplane, st));
 
     p = base;                                // W_O: residual add, input of the FFN norm
     p.X = o; p.ldx = L.HD; p.xplane = oplane;
     p.W = layer_ptr(m, l, L.l_o); p.NT = L.d / 16; p.KT = KThd; p.n_valid = L.d;
+    p.wscale = scale_ptr(m, l, L.l_o_sc);
     p.h = h; p.gain = reinterpret_cast<const float*>(layer_ptr(m, l, L.l_ffn_norm));
     p.u = x; p.ldu = L.d; p.uplane = uplane; p.ss_out = ss_nxt; p.epi = sps::kEpiResid;
     s = gemm(dt, p, st);
@@ -279,6 +305,7 @@ sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t*
     p = base;                                // W_1: norm scale, GELU / SwiGLU
     p.X = x; p.ldx = L.d; p.xplane = uplane;
     p.W = layer_ptr(m, l, L.l_w1); p.NT = L.N1 / 16; p.KT = KTd; p.n_valid = L.F;
+    p.wscale = scale_ptr(m, l, L.l_w1_sc);
     p.ss_in = ss_nxt; p.ng_in = ng_o;
     p.act = act; p.lda = L.F; p.aplane = aplane;
     p.epi = L.swiglu ? sps::kEpiSwiglu : sps::kEpiGelu;
@@ -288,6 +315,7 @@ sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t*
     p = base;                                // W_2: residual add, input of the next norm
     p.X = act; p.ldx = L.F; p.xplane = aplane;
     p.W = layer_ptr(m, l, L.l_w2); p.NT = L.d / 16; p.KT = KTf; p.n_valid = L.d;
+    p.wscale = scale_ptr(m, l, L.l_w2_sc);
     p.h = h;
     p.gain = l + 1 < L.L ? reinterpret_cast<const float*>(layer_ptr(m, l + 1, L.l_attn_norm))
                          : reinterpret_cast<const float*>(m->base + L.final_norm);
@@ -300,6 +328,7 @@ sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t*
     GemmParams p = base;                     // final norm scale + unembedding
     p.X = x; p.ldx = L.d; p.xplane = uplane;
     p.W = m->base + L.unembed; p.NT = L.NU / 16; p.KT = KTd; p.n_valid = L.V;
+    p.wscale = L.fp8 ? reinterpret_cast<const float*>(m->base + L.unembed_sc) : nullptr;
     p.ss_in = ss_cur; p.ng_in = ng;
     p.out = logits; p.ldo = L.V; p.epi = sps::kEpiStore;
     sps_status s = gemm(dt, p, st);
@@ -316,7 +345,8 @@ sps_status check_forward_args(const sps_model_s* m, const sps_kv_s* kv, int B, i
   if (B != kv->B) return SPS_E_SHAPE;
   const sps_config& a = m->cfg;
   const sps_config& b = kv->cfg;
-  if (a.n_layers != b.n_layers || a.n_heads != b.n_heads || a.head_dim != b.head_dim || a.dtype != b.dtype)
+  if (a.n_layers != b.n_layers || a.n_heads != b.n_heads || a.head_dim != b.head_dim ||
+      act_dtype(a) != act_dtype(b))
     return SPS_E_SHAPE;
   *out = make_ws(m->L, B, Mps, kv->T_cap);
   if (ws_bytes < out->total) return SPS_E_CAPACITY;
@@ -339,7 +369,7 @@ const char* sps_status_string(int32_t status) {
   }
 }
 
-int32_t sps_abi_version(void) { return 2; }
+int32_t sps_abi_version(void) { return 3; }
 
 size_t sps_weight_bytes(const sps_config* cfg) { return valid_config(cfg) ? make_layout(cfg).total : 0; }
 
@@ -357,6 +387,14 @@ sps_status sps_pack_weight(const sps_config* cfg, int32_t tensor, int32_t layer,
   const hipStream_t st = as_stream(stream);
   const int dt = cfg->dtype;
   const size_t es = L.es;
+  // One projection: canonical rows src [n_src][Kd] to packed rows (see
+  // launch_pack); FP8 models quantise bf16 rows and write the row scales at
+  // `sc`. Rows [zf, zt) are padding.
+  auto pack = [&](int n_src, int Kd, char* dst, char* sc, int kind, int row_off, int dh, int zf, int zt) {
+    return L.fp8 ? sps::launch_pack_fp8(src, n_src, Kd, dst, reinterpret_cast<float*>(sc), Kd / 32, kind, row_off,
+                                        dh, zf, zt, st)
+                 : sps::launch_pack(dt, src, n_src, Kd, dst, Kd / 32, kind, row_off, dh, zf, zt, st);
+  };
   switch (tensor) {
     case SPS_W_EMBED:
       SPS_HIP(hipMemcpyAsync(base + L.embed, src, static_cast<size_t>(L.V) * L.d * es, hipMemcpyDeviceToDevice, st));
@@ -371,31 +409,64 @@ sps_status sps_pack_weight(const sps_config* cfg, int32_t tensor, int32_t layer,
       SPS_HIP(hipMemcpyAsync(lp + L.l_ffn_norm, src, static_cast<size_t>(L.d) * 4, hipMemcpyDeviceToDevice, st));
       return SPS_OK;
     case SPS_W_UNEMBED:
-      SPS_HIP(sps::launch_pack(dt, src, L.V, L.d, base + L.unembed, L.d / 32, 0, 0, 0, L.V, L.NU, st));
+      SPS_HIP(pack(L.V, L.d, base + L.unembed, base + L.unembed_sc, 0, 0, 0, L.V, L.NU));
       return SPS_OK;
     case SPS_W_Q:   // rotary partners side by side (kind 2)
     case SPS_W_K:
-      SPS_HIP(sps::launch_pack(dt, src, L.HD, L.d, lp + L.l_qkv, L.d / 32, 2, (tensor - SPS_W_Q) * L.HD, L.DH, 0,
-                               0, st));
+      SPS_HIP(pack(L.HD, L.d, lp + L.l_qkv, lp + L.l_qkv_sc, 2, (tensor - SPS_W_Q) * L.HD, L.DH, 0, 0));
       return SPS_OK;
     case SPS_W_V:
-      SPS_HIP(sps::launch_pack(dt, src, L.HD, L.d, lp + L.l_qkv, L.d / 32, 0, 2 * L.HD, 0, 0, 0, st));
+      SPS_HIP(pack(L.HD, L.d, lp + L.l_qkv, lp + L.l_qkv_sc, 0, 2 * L.HD, 0, 0, 0));
       return SPS_OK;
     case SPS_W_O:
-      SPS_HIP(sps::launch_pack(dt, src, L.d, L.HD, lp + L.l_o, L.HD / 32, 0, 0, 0, 0, 0, st));
+      SPS_HIP(pack(L.d, L.HD, lp + L.l_o, lp + L.l_o_sc, 0, 0, 0, 0, 0));
       return SPS_OK;
     case SPS_W_1:
-      SPS_HIP(sps::launch_pack(dt, src, L.F, L.d, lp + L.l_w1, L.d / 32, L.swiglu ? 1 : 0, 0, 0, 0, 0, st));
+      SPS_HIP(pack(L.F, L.d, lp + L.l_w1, lp + L.l_w1_sc, L.swiglu ? 1 : 0, 0, 0, 0, 0));
       return SPS_OK;
     case SPS_W_3:
-      SPS_HIP(sps::launch_pack(dt, src, L.F, L.d, lp + L.l_w1, L.d / 32, 1, 1, 0, 0, 0, st));
+      SPS_HIP(pack(L.F, L.d, lp + L.l_w1, lp + L.l_w1_sc, 1, 1, 0, 0, 0));
       return SPS_OK;
     case SPS_W_2:
-      SPS_HIP(sps::launch_pack(dt, src, L.d, L.F, lp + L.l_w2, L.F / 32, 0, 0, 0, 0, 0, st));
+      SPS_HIP(pack(L.d, L.F, lp + L.l_w2, lp + L.l_w2_sc, 0, 0, 0, 0, 0));
       return SPS_OK;
     default:
       return SPS_E_INVALID;
   }
+}
+
+sps_status sps_weight_slot(const sps_config* cfg, int32_t tensor, int32_t layer, size_t* offset, size_t* bytes,
+                           size_t* scale_offset) {
+  if (!offset || !bytes || !scale_offset) return SPS_E_INVALID;
+  if (!valid_config(cfg)) return SPS_E_SHAPE;
+  const Layout L = make_layout(cfg);
+  const bool per_layer = tensor >= SPS_W_ATTN_NORM;
+  if (tensor < SPS_W_EMBED || tensor > SPS_W_2) return SPS_E_INVALID;
+  if (per_layer && (layer < 0 || layer >= L.L)) return SPS_E_INVALID;
+  if (tensor == SPS_W_3 && !L.swiglu) return SPS_E_INVALID;
+  const size_t lbase = L.layer0 + L.layer_stride * (per_layer ? layer : 0);
+  const size_t wes = L.wes;
+  size_t off = 0, n = 0, sc = 0;
+  switch (tensor) {
+    case SPS_W_EMBED: off = L.embed; n = static_cast<size_t>(L.V) * L.d * L.es; break;
+    case SPS_W_FINAL_NORM: off = L.final_norm; n = static_cast<size_t>(L.d) * 4; break;
+    case SPS_W_UNEMBED: off = L.unembed; n = static_cast<size_t>(L.NU) * L.d * wes; sc = L.unembed_sc; break;
+    case SPS_W_ATTN_NORM: off = lbase + L.l_attn_norm; n = static_cast<size_t>(L.d) * 4; break;
+    case SPS_W_FFN_NORM: off = lbase + L.l_ffn_norm; n = static_cast<size_t>(L.d) * 4; break;
+    case SPS_W_Q:
+    case SPS_W_K:
+    case SPS_W_V:
+      off = lbase + L.l_qkv; n = static_cast<size_t>(3) * L.HD * L.d * wes; sc = lbase + L.l_qkv_sc; break;
+    case SPS_W_O: off = lbase + L.l_o; n = static_cast<size_t>(L.d) * L.HD * wes; sc = lbase + L.l_o_sc; break;
+    case SPS_W_1:
+    case SPS_W_3:
+      off = lbase + L.l_w1; n = static_cast<size_t>(L.N1) * L.d * wes; sc = lbase + L.l_w1_sc; break;
+    default: off = lbase + L.l_w2; n = static_cast<size_t>(L.d) * L.F * wes; sc = lbase + L.l_w2_sc; break;
+  }
+  *offset = off;
+  *bytes = n;
+  *scale_offset = L.fp8 ? sc : 0;
+  return SPS_OK;
 }
 
 sps_status sps_model_create(const sps_config* cfg, void* packed, sps_model_t* out) {
@@ -450,7 +521,7 @@ static sps_status kv_copy(sps_kv_t kv, int32_t layer, int32_t b, int32_t pos0, i
   const size_t seq = static_cast<size_t>(b) * kv->L.H * kv->T_cap * kv->L.DH * kv->L.es;
   char* kc = static_cast<char*>(kv_k(kv, layer)) + seq;
   char* vc = static_cast<char*>(kv_v(kv, layer)) + seq;
-  SPS_HIP(sps::launch_kv_copy(kv->cfg.dtype, to_cache, kc, vc, kv->L.H, kv->L.DH, kv->T_cap, pos0, n, k, v,
+  SPS_HIP(sps::launch_kv_copy(act_dtype(kv->cfg), to_cache, kc, vc, kv->L.H, kv->L.DH, kv->T_cap, pos0, n, k, v,
                               as_stream(stream)));
   return SPS_OK;
 }
@@ -617,6 +688,12 @@ sps_status sps_profile_gemm_end(float* total_ms, int32_t* launches, double* byte
   *bytes = b;
   g_prof.used = 0;
   g_prof.bytes.clear();
+  return SPS_OK;
+}
+
+sps_status sps_fp8_decode(const uint8_t* codes, int32_t n, float* out, void* stream) {
+  if (!codes || !out || n < 0 || n % 16 != 0 || reinterpret_cast<uintptr_t>(codes) % 16 != 0) return SPS_E_INVALID;
+  SPS_HIP(sps::launch_fp8_decode(codes, n, out, as_stream(stream)));
   return SPS_OK;
 }
 

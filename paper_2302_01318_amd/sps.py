@@ -20,8 +20,10 @@ c_int32, c_uint64, c_float, c_size_t, c_void_p = (ctypes.c_int32, ctypes.c_uint6
                                                    ctypes.c_size_t, ctypes.c_void_p)
 
 FFN = {"gelu": 0, "swiglu": 1}
-DTYPE = {"f32": 0, "bf16": 1}
-TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
+DTYPE = {"f32": 0, "bf16": 1, "fp8": 2}
+# Tensor type of the canonical matrices handed to the packer and of the KV
+# cache: an FP8 model is packed from bf16 matrices and keeps a bf16 cache.
+TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16, "fp8": torch.bfloat16}
 TENSOR_ID = {"embed": 0, "final_norm": 1, "unembed": 2, "attn_norm": 3, "wq": 4, "wk": 5, "wv": 6,
              "wo": 7, "ffn_norm": 8, "w1": 9, "w3": 10, "w2": 11}
 PURPOSE_DRAFT, PURPOSE_ACCEPT, PURPOSE_RESAMPLE = 0, 1, 2
@@ -84,6 +86,9 @@ _sig("sps_softmax", c_int32, [P, c_int32, c_int32, Sampling, P, P])
 _sig("sps_device_error", c_int32, [P, c_int32, ctypes.POINTER(c_int32)])
 _sig("sps_profile_gemm_begin", c_int32, [c_int32])
 _sig("sps_stream_read", c_int32, [P, c_size_t, P, P])
+_sig("sps_fp8_decode", c_int32, [P, c_int32, P, P])
+_sig("sps_weight_slot", c_int32, [ctypes.POINTER(Config), c_int32, c_int32, ctypes.POINTER(c_size_t),
+                                  ctypes.POINTER(c_size_t), ctypes.POINTER(c_size_t)])
 _sig("sps_profile_gemm_end", c_int32, [ctypes.POINTER(c_float), ctypes.POINTER(c_int32),
                                        ctypes.POINTER(ctypes.c_double)])
 
@@ -92,7 +97,7 @@ EXPORTS = ["sps_status_string", "sps_abi_version", "sps_weight_bytes", "sps_pack
            "sps_kv_write", "sps_kv_read", "sps_workspace_bytes", "sps_forward", "sps_verify_step",
            "sps_accept_resample", "sps_draft_step", "sps_commit", "sps_philox_uniforms", "sps_softmax",
            "sps_device_error", "sps_profile_gemm_begin", "sps_profile_gemm_end",
-           "sps_stream_read"]
+           "sps_stream_read", "sps_fp8_decode", "sps_weight_slot"]
 
 
 class SPSError(RuntimeError):
@@ -293,6 +298,23 @@ def stream_read(buf, nbytes, sink):
     if nbytes > buf.numel() * buf.element_size():
         raise ValueError("stream_read: %d bytes exceed the buffer" % nbytes)
     check(lib.sps_stream_read(_ptr(buf), nbytes, _ptr(sink, torch.int32, "sink"), _stream()), "sps_stream_read")
+
+
+def weight_slot(shape, name, layer=0):
+    """(offset, bytes, scale offset) of a tensor's slot in the packed buffer."""
+    o, n, sc = c_size_t(0), c_size_t(0), c_size_t(0)
+    check(lib.sps_weight_slot(ctypes.byref(config_of(shape)), TENSOR_ID[name], layer, ctypes.byref(o),
+                              ctypes.byref(n), ctypes.byref(sc)), "sps_weight_slot")
+    return o.value, n.value, sc.value
+
+
+def fp8_decode(codes):
+    """fp32 values of E4M3 codes (uint8 device tensor, numel % 16 == 0) with
+    the FP8-weight GEMM's conversion."""
+    out = torch.empty(codes.numel(), dtype=torch.float32, device=codes.device)
+    check(lib.sps_fp8_decode(_ptr(codes, torch.uint8, "codes"), codes.numel(), _ptr(out), _stream()),
+          "sps_fp8_decode")
+    return out
 
 
 class Generator:

@@ -6,7 +6,8 @@ the CPU oracle consume its outputs, so neither depends on the other.
 
 Recipes:
   weights      N(0, std^2) per entry (std 0.02), stored in the model dtype
-               (bf16 by round-to-nearest-even through torch); RMSNorm gains
+               (bf16 by round-to-nearest-even through torch; bf16 also for
+               FP8 models, whose packer quantises them); RMSNorm gains
                1 + N(0, gain_std^2) in fp32. One numpy Generator per tensor,
                seeded by (seed, tensor id), so any single tensor can be
                regenerated on its own.
@@ -68,7 +69,7 @@ def weight(cfg, name, layer, seed, std=0.02, gain_std=0.1):
     if name.endswith("norm"):
         return torch.from_numpy(1.0 + gain_std * g.standard_normal(shape, dtype=np.float32))
     a = torch.from_numpy(g.standard_normal(shape, dtype=np.float32) * np.float32(std))
-    return a.to(torch.bfloat16) if cfg.dtype == "bf16" else a
+    return a.to(torch.bfloat16) if cfg.dtype in ("bf16", "fp8") else a
 
 
 def weights(cfg, seed, std=0.02, gain_std=0.1):
@@ -86,7 +87,7 @@ def kv_prior(cfg, seed, layer, B, T):
     shape = (B, cfg.n_heads, T, cfg.head_dim)
     k = torch.from_numpy(g.standard_normal(shape, dtype=np.float32))
     v = torch.from_numpy(g.standard_normal(shape, dtype=np.float32))
-    if cfg.dtype == "bf16":
+    if cfg.dtype in ("bf16", "fp8"):
         k, v = k.to(torch.bfloat16), v.to(torch.bfloat16)
     return k, v
 
@@ -134,7 +135,7 @@ def device_weights(cfg, seed, std=0.02, gain_std=0.1, device="cuda"):
     to draw on the host, e.g. the 70B shape). One tensor is alive at a time."""
     gen = torch.Generator(device=device)
     gen.manual_seed(int(seed))
-    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    dt = torch.bfloat16 if cfg.dtype in ("bf16", "fp8") else torch.float32
     for key, shape in tensor_shapes(cfg).items():
         if key[0].endswith("norm"):
             t = torch.randn(shape, generator=gen, device=device, dtype=torch.float32).mul_(gain_std).add_(1.0)
@@ -151,7 +152,7 @@ def coupled_device_weights(cfg, pair_seed, model_seed, layer_std, code_pert=0.0,
     basis (output codes perturbed by code_pert), unit gains, N(0, layer_std^2)
     layer weights."""
     d, V = cfg.d_model, cfg.vocab
-    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    dt = torch.bfloat16 if cfg.dtype in ("bf16", "fp8") else torch.float32
     pair = torch.Generator(device=device)
     pair.manual_seed(int(pair_seed))
     z = torch.randn((V, rank), generator=pair, device=device)

@@ -9,13 +9,16 @@ def spec_of(shape, **kw):
     """oracle ModelSpec with the dimensions of a configs.ModelShape."""
     s = dict(d_model=shape.d_model, n_layers=shape.n_layers, n_heads=shape.n_heads,
              head_dim=shape.head_dim, d_ff=shape.d_ff, vocab=shape.vocab, ffn=shape.ffn,
-             dtype=shape.dtype, eps=shape.eps, rope_base=shape.rope_base)
+             dtype="bf16" if shape.dtype == "fp8" else shape.dtype, eps=shape.eps,
+             rope_base=shape.rope_base)
     s.update(kw)
     return ModelSpec(**s)
 
 
 def oracle_weights(shape, wdict):
-    """{(name, layer): torch tensor} -> the oracle's nested dict of fp32 arrays."""
+    """{(name, layer): torch tensor} -> the oracle's nested dict of fp32 arrays
+    (for an FP8 model: the projections quantised and dequantised by the
+    oracle's own FP8 quantiser)."""
     f = lambda t: t.float().numpy()
     W = {"embed": f(wdict[("embed", -1)]), "final_norm": f(wdict[("final_norm", -1)]),
          "unembed": f(wdict[("unembed", -1)]), "layers": []}
@@ -31,4 +34,7 @@ def oracle_weights(shape, wdict):
             lw["wu"] = f(wdict[("w3", l)])
             lw["wd"] = f(wdict[("w2", l)])
         W["layers"].append(lw)
+    if shape.dtype == "fp8":
+        from oracle import fp8
+        W = fp8.fp8_weights(W)
     return W

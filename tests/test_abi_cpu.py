@@ -37,7 +37,7 @@ def test_every_declared_function_is_exported(sps):
 def test_status_strings(sps):
     assert sps.lib.sps_status_string(0) == b"ok"
     assert sps.lib.sps_status_string(5) == b"HIP runtime error"
-    assert sps.lib.sps_abi_version() == 2
+    assert sps.lib.sps_abi_version() == 3
 
 
 def test_config_validation_and_sizes(sps):
@@ -54,6 +54,41 @@ def test_config_validation_and_sizes(sps):
     assert sps.lib.sps_kv_bytes(ctypes.byref(good), 1, 100) == 0          # T_cap % 32
     assert sps.lib.sps_kv_bytes(ctypes.byref(good), 1, 2304) == 80 * 2 * 64 * 2304 * 128 * 2
     assert sps.lib.sps_workspace_bytes(ctypes.byref(good), 0, 5, 2304) == 0
+
+
+def test_fp8_config_and_slots(sps):
+    from paper_2302_01318_amd import configs
+    s70 = configs.SEVENTY_B
+    b16 = sps.config_of(s70)
+    f8 = sps.config_of(s70.with_(dtype="fp8"))
+    nb, n8 = sps.lib.sps_weight_bytes(ctypes.byref(b16)), sps.lib.sps_weight_bytes(ctypes.byref(f8))
+    # projections halve; the bf16 embedding (V x d) and the scales stay
+    V, d = s70.vocab, s70.d_model
+    assert n8 < nb and abs((nb - V * d * 2) / 2 - (n8 - V * d * 2)) < 0.001 * nb
+    # FP8 needs 64-deep contractions: d_model, heads x head_dim and d_ff multiples of 64
+    for field, bad in [("d_model", 96), ("d_ff", 96)]:
+        c = sps.config_of(s70.with_(dtype="fp8"))
+        setattr(c, field, bad)
+        assert sps.lib.sps_weight_bytes(ctypes.byref(c)) == 0, field
+    c = sps.config_of(configs.ModelShape("x", 96, 1, 1, 64, 128, 100, "gelu", "bf16"))
+    assert sps.lib.sps_weight_bytes(ctypes.byref(c)) > 0
+    c.dtype = 2
+    assert sps.lib.sps_weight_bytes(ctypes.byref(c)) == 0
+    # slots: FP8 projections carry row scales right after their codes; bf16 ones none
+    o, n, sc = sps.weight_slot(s70.with_(dtype="fp8"), "w1", 3)
+    assert n == 32768 * 8192 and sc >= o + n and sc - (o + n) < 256
+    o2, n2, sc2 = sps.weight_slot(s70, "w1", 3)
+    assert n2 == 2 * n and sc2 == 0
+    assert sps.weight_slot(s70.with_(dtype="fp8"), "wq", 0)[0] == sps.weight_slot(s70.with_(dtype="fp8"), "wv", 0)[0]
+    for layer in (-1, 80):
+        with pytest.raises(sps.SPSError):
+            sps.weight_slot(s70, "wo", layer)
+    with pytest.raises(sps.SPSError):
+        sps.weight_slot(s70, "w3", 0)                  # GELU model: no W3
+    P = ctypes.c_void_p
+    assert sps.lib.sps_fp8_decode(P(16), 17, P(16), None) == 1
+    assert sps.lib.sps_fp8_decode(P(8), 16, P(16), None) == 1
+    assert sps.lib.sps_fp8_decode(None, 16, P(16), None) == 1
 
 
 def test_invalid_arguments_return_codes(sps):

@@ -58,7 +58,7 @@ def verify_parity(sps, shape, B, K, n_prior, seed, tol, T=1.0, check_kv=True):
     np.testing.assert_array_equal(out.cpu().numpy(), w_out)
     np.testing.assert_array_equal(nacc.cpu().numpy(), w_n)
     if check_kv:
-        kt = tol if shape.dtype == "bf16" else 1e-4
+        kt = tol if shape.dtype in ("bf16", "fp8") else 1e-4
         for l in range(shape.n_layers):
             for b in range(B):
                 k, v = kv.read(l, b, n_prior[b], K + 1)
