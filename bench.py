@@ -36,7 +36,8 @@ HBM_PEAK_GBS = 8000.0
 GEMM_REPEATS = 8                 # back-to-back launches per event bracket in the roofline pass
 CALIBRATION_BYTES = 1 << 30      # plain device copy whose HBM counters calibrate FETCH/WRITE_SIZE
 # Sources of the single-tile GEMM kernel (the one the traffic counters were taken on).
-GEMM_SOURCES = [os.path.join(ROOT, "paper_2302_01318_amd", "csrc", f) for f in ("gemm.hip", "gemm_epi.h", "common.h")]
+GEMM_SOURCES = [os.path.join(ROOT, "paper_2302_01318_amd", "csrc", f)
+                for f in ("gemm.hip", "gemm_epi.h", "common.h", "fp8.h")]
 PROFILES = os.path.join(ROOT, "profiles")
 STREAM_READ_BYTES = 8 << 30      # bytes of the packed weights read by the streaming-read ceiling
 
