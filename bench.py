@@ -39,6 +39,7 @@ CALIBRATION_BYTES = 1 << 30      # plain device copy whose HBM counters calibrat
 GEMM_SOURCES = [os.path.join(ROOT, "paper_2302_01318_amd", "csrc", f)
                 for f in ("gemm.hip", "gemm_epi.h", "common.h", "fp8.h")]
 PROFILES = os.path.join(ROOT, "profiles")
+CPU_BASELINE_SECONDS = 10.0     # CPU work the oracle baseline is timed over
 STREAM_READ_BYTES = 8 << 30      # bytes of the packed weights read by the streaming-read ceiling
 
 
@@ -161,10 +162,12 @@ def cpu_baseline(shape, K, ctx):
     cache["k"][0, 0, :, :ctx] = k[0].double().numpy()
     cache["v"][0, 0, :, :ctx] = v[0].double().numpy()
     toks = synth.tokens(2, 1, K + 1, one.vocab)
-    reps = 4
+    # Repeat the sample until ~10 s of CPU work (at least 4 runs).
+    reps = 0
     t0 = time.perf_counter()
-    for _ in range(reps):
+    while reps < 4 or time.perf_counter() - t0 < CPU_BASELINE_SECONDS:
         om.forward_cached(spec, W, cache, toks, np.array([ctx]))
+        reps += 1
     dt = (time.perf_counter() - t0) / reps
     nbytes = verify_bytes(one, 1, K, ctx)
     try:

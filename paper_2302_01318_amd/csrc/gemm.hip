@@ -296,18 +296,20 @@ static hipError_t gemm_dispatch_bf16(const GemmParams& p, hipStream_t st) {
   return gemm_launch<T, 1, 1, 16, 4>(p, st);
 }
 
-// FP8 weights, one M tile (8 rows; more rows take several launches), 8
-// k-tiles (4 code loads of 16 B per lane and n-tile) per chunk. From a
-// launch-shape sweep over the 70B, 7B and draft matrices at 1 and 5 rows:
-// two n-tiles per wave with 8-wave work-groups from 512 n-tiles (the
-// activation fragment feeds two MFMA pairs), else one n-tile and 16 waves
-// (enough work-groups for the 3072- and 4096-wide outputs).
+// FP8 weights, one M tile (8 rows; more rows take several launches). From a
+// launch-shape sweep over the 70B, 7B and draft matrices at 0, 1 and 5 rows:
+// from 512 n-tiles, two n-tiles per wave (each activation fragment feeds two
+// MFMA pairs), 8-wave work-groups and 4 k-tiles (2 code loads of 16 B per
+// lane and n-tile) per chunk; below, one n-tile, 16 waves and 8 k-tiles
+// (enough work-groups for the 3072- and 4096-wide outputs). At 5 rows the
+// activation fragments, read by every wave from L2, cost ~10 % of the 70B
+// launches against the same launch with no activation rows.
 static int fp8_ntw(int NT, int) { return NT % 2 == 0 && NT >= 512 ? 2 : 1; }
 
 static hipError_t gemm_dispatch_fp8(const GemmParams& p, hipStream_t st) {
   using T = bf16;
   if (p.M > ActRows<T>::kRows || !p.wscale || p.KT % 2) return hipErrorInvalidValue;
-  if (fp8_ntw(p.NT, p.KT) == 2) return gemm_launch<T, 1, 2, 8, 8, true>(p, st);
+  if (fp8_ntw(p.NT, p.KT) == 2) return gemm_launch<T, 1, 2, 8, 4, true>(p, st);
   return gemm_launch<T, 1, 1, 16, 8, true>(p, st);
 }
 
