@@ -17,8 +17,7 @@
 
 namespace sps {
 
-constexpr int kWavePos = 64;         // positions per wave: two 32-position blocks
-constexpr int kGroupPos = 4 * kWavePos;  // positions per work-group (4 waves)
+constexpr int kWavePos = 64;         // positions per wave (prefill chunks): two 32-position blocks
 
 // One 32-position block for one query tile: scores, masked online softmax,
 // and accumulation of O^T. For bf16 the softmax weights enter the P V MFMA
@@ -96,12 +95,12 @@ __device__ __forceinline__ void load_block(const T* __restrict__ kr, const T* __
   }
 }
 
-// Grid (ceil(T_cap / 256), H, B), 4 waves. Wave w of work-group g covers
-// positions 256 g + 64 w .. +63. With one query tile (QT == 1: up to 16 new
+// Grid (ceil(T_cap / (4 WP)), H, B), 4 waves. Wave w of work-group g covers
+// positions 4 WP g + WP w .. + WP - 1 (WP = 32 or 64: one or two blocks). With one query tile (QT == 1: up to 16 new
 // tokens per sequence, every verify and draft step) the four waves' partials
 // are merged in LDS and the work-group writes one partial per 256 positions;
 // with more query tiles (prefill chunks) every wave writes its own.
-template <typename T, int DH, int QT>
+template <typename T, int DH, int QT, int WP>
 __global__ __launch_bounds__(256) void attn_partial_kernel(const T* __restrict__ q, const T* __restrict__ kc,
                                                            const T* __restrict__ vc,
                                                            const int32_t* __restrict__ lengths, int pos_offset,
@@ -115,7 +114,8 @@ __global__ __launch_bounds__(256) void attn_partial_kernel(const T* __restrict__
   const int len = lengths[b] + pos_offset;        // position of query 0
   int nkv = len + Mps;
   if (nkv > T_cap) nkv = T_cap;
-  const int p0 = blockIdx.x * kGroupPos + wave * kWavePos;
+  static_assert(WP == 32 || WP == 64, "one or two 32-position blocks per wave");
+  const int p0 = blockIdx.x * 4 * WP + wave * WP;
   const int HD = H * DH;
   const size_t region = (static_cast<size_t>(b) * H + h) * static_cast<size_t>(T_cap) * DH;
   const T* kr = kc + region;
@@ -141,7 +141,7 @@ __global__ __launch_bounds__(256) void attn_partial_kernel(const T* __restrict__
   }
 
   int nblk = nkv > p0 ? (nkv - p0 + 31) / 32 : 0;
-  if (nblk > kWavePos / 32) nblk = kWavePos / 32;
+  if (nblk > WP / 32) nblk = WP / 32;
   for (int b0 = 0; b0 < nblk; b0 += kPre) {
     Frag<T> kf[kPre][2][DH / 32];
     Frag<T> vf[kPre][DH / 16];
@@ -258,35 +258,47 @@ __global__ __launch_bounds__(DH) void attn_combine_kernel(const float* __restric
 // Upper bound of partials per (sequence, head): one per wave (prefill).
 int attn_partials(int T_cap) { return (T_cap + kWavePos - 1) / kWavePos; }
 
+// Decode launches (up to 16 new tokens per sequence): WP positions per wave,
+// partials merged per work-group of 4 WP positions.
+template <typename T, int DH, int WP>
+static hipError_t attn_decode_t(const void* q, const void* kc, const void* vc, const int32_t* lengths,
+                                int pos_offset, int B, int Mps, int H, int T_cap, float* part, void* o,
+                                size_t oplane, hipStream_t st) {
+  const float c_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(DH));
+  const int groups = (T_cap + 4 * WP - 1) / (4 * WP);
+  hipLaunchKernelGGL((attn_partial_kernel<T, DH, 1, WP>), dim3(groups, H, B), dim3(256), 0, st,
+                     static_cast<const T*>(q), static_cast<const T*>(kc), static_cast<const T*>(vc), lengths,
+                     pos_offset, Mps, H, T_cap, groups, c_log2, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3(B * Mps, H), dim3(DH), 0, st, part, lengths, pos_offset,
+                     Mps, H, T_cap, groups, 4 * WP, c_log2, static_cast<T*>(o), oplane);
+  return hipGetLastError();
+}
+
 template <typename T, int DH>
 static hipError_t attn_t(const void* q, const void* kc, const void* vc, const int32_t* lengths, int pos_offset,
                          int B, int Mps, int H, int T_cap, float* part, void* o, size_t oplane, hipStream_t st) {
+  if (Mps <= 16)
+    return attn_decode_t<T, DH, 64>(q, kc, vc, lengths, pos_offset, B, Mps, H, T_cap, part, o, oplane, st);
+  // Prefill chunks: 2 or 4 query tiles, every wave writes its own partial.
   const float c_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(DH));
-  const int groups = (T_cap + kGroupPos - 1) / kGroupPos;
+  const int groups = (T_cap + 4 * kWavePos - 1) / (4 * kWavePos);
   const dim3 grid(groups, H, B);
   const T* qq = static_cast<const T*>(q);
   const T* kk = static_cast<const T*>(kc);
   const T* vv = static_cast<const T*>(vc);
-  int NP, pp;
-  if (Mps <= 16) {
-    NP = groups;
-    pp = kGroupPos;
-    hipLaunchKernelGGL((attn_partial_kernel<T, DH, 1>), grid, dim3(256), 0, st, qq, kk, vv, lengths, pos_offset,
-                       Mps, H, T_cap, NP, c_log2, part);
-  } else {
-    NP = attn_partials(T_cap);
-    pp = kWavePos;
-    if (Mps <= 32)
-      hipLaunchKernelGGL((attn_partial_kernel<T, DH, 2>), grid, dim3(256), 0, st, qq, kk, vv, lengths, pos_offset,
-                         Mps, H, T_cap, NP, c_log2, part);
-    else
-      hipLaunchKernelGGL((attn_partial_kernel<T, DH, 4>), grid, dim3(256), 0, st, qq, kk, vv, lengths, pos_offset,
-                         Mps, H, T_cap, NP, c_log2, part);
-  }
+  const int NP = attn_partials(T_cap);
+  if (Mps <= 32)
+    hipLaunchKernelGGL((attn_partial_kernel<T, DH, 2, kWavePos>), grid, dim3(256), 0, st, qq, kk, vv, lengths,
+                       pos_offset, Mps, H, T_cap, NP, c_log2, part);
+  else
+    hipLaunchKernelGGL((attn_partial_kernel<T, DH, 4, kWavePos>), grid, dim3(256), 0, st, qq, kk, vv, lengths,
+                       pos_offset, Mps, H, T_cap, NP, c_log2, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3(B * Mps, H), dim3(DH), 0, st, part, lengths, pos_offset,
-                     Mps, H, T_cap, NP, pp, c_log2, static_cast<T*>(o), oplane);
+                     Mps, H, T_cap, NP, kWavePos, c_log2, static_cast<T*>(o), oplane);
   return hipGetLastError();
 }
 

@@ -290,13 +290,13 @@ static hipError_t gemm_dispatch_f32(const GemmParams& p, hipStream_t st) {
 
 static hipError_t gemm_dispatch_bf16(const GemmParams& p, hipStream_t st) {
   using T = bf16;
-  if (gemm_is_wide(1, p.Mtot)) return launch_gemm_wide(p, wide_plan(p.NT, p.KT, p.M), st);
+  if (gemm_is_wide(1, p.Mtot)) return launch_gemm_wide(p, wide_plan(p.NT, p.KT, p.M, false), st);
   if (p.M > ActRows<T>::kRows) return hipErrorInvalidValue;
   if (single_tile_ntw(p.NT, p.KT) == 2) return gemm_launch<T, 1, 2, 8, 4>(p, st);
   return gemm_launch<T, 1, 1, 16, 4>(p, st);
 }
 
-// FP8 weights, one M tile (8 rows; more rows take several launches). From a
+// FP8 weights, one M tile (8 rows; more rows take the wide kernel). From a
 // launch-shape sweep over the 70B, 7B and draft matrices at 0, 1 and 5 rows:
 // from 512 n-tiles, two n-tiles per wave (each activation fragment feeds two
 // MFMA pairs), 8-wave work-groups and 4 k-tiles (2 code loads of 16 B per
@@ -308,18 +308,18 @@ static int fp8_ntw(int NT, int) { return NT % 2 == 0 && NT >= 512 ? 2 : 1; }
 
 static hipError_t gemm_dispatch_fp8(const GemmParams& p, hipStream_t st) {
   using T = bf16;
-  if (p.M > ActRows<T>::kRows || !p.wscale || p.KT % 2) return hipErrorInvalidValue;
+  if (!p.wscale || p.KT % 2) return hipErrorInvalidValue;
+  if (gemm_is_wide(2, p.Mtot)) return launch_gemm_wide(p, wide_plan(p.NT, p.KT, p.M, true), st);
+  if (p.M > ActRows<T>::kRows) return hipErrorInvalidValue;
   if (fp8_ntw(p.NT, p.KT) == 2) return gemm_launch<T, 1, 2, 8, 4, true>(p, st);
   return gemm_launch<T, 1, 1, 16, 8, true>(p, st);
 }
 
 // One launch covers up to 160 rows (20 M tiles of 8 bf16 rows, 10 of 16
-// fp32); FP8-weight launches one M tile of 8 rows.
-int gemm_max_rows(int dtype) {
-  return dtype == 1 ? 20 * ActRows<bf16>::kRows : dtype == 2 ? ActRows<bf16>::kRows : 10 * ActRows<float>::kRows;
-}
+// fp32); bf16 and FP8 weights take the wide kernel above 8 rows.
+int gemm_max_rows(int dtype) { return dtype == 0 ? 10 * ActRows<float>::kRows : 20 * ActRows<bf16>::kRows; }
 
-bool gemm_is_wide(int dtype, int Mtot) { return dtype == 1 && Mtot > ActRows<bf16>::kRows; }
+bool gemm_is_wide(int dtype, int Mtot) { return dtype != 0 && Mtot > ActRows<bf16>::kRows; }
 
 int gemm_groups(int dtype, int NT, int KT, int Mtot) {
   if (gemm_is_wide(dtype, Mtot)) return wide_groups(NT);

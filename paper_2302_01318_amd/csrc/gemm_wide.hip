@@ -24,9 +24,15 @@
 //    squares whatever NTW is) and M tile. (A last-arriving-split fixup
 //    inside one kernel would need device-scope fences, which on this GPU
 //    write back and invalidate the L2 and cost more than the launch.)
+//
+// FP8 weights (W8): the weight fragments come from the 16 x 64 code tiles of
+// gemm.hip, one 16-byte load per lane and n-tile for each pair of k-tiles of
+// a chunk (KC even), converted exactly to two bf16 B fragments before their
+// MFMAs; the row scale is applied in the epilogue.
 #include <algorithm>
 
 #include "common.h"
+#include "fp8.h"
 #include "gemm_epi.h"
 #include "launch.h"
 
@@ -51,15 +57,23 @@ template <int MT, int NTW> constexpr int wide_waves_per_simd() {
   return NTW == 4 || MT > 12 ? 1 : MT <= 6 ? 3 : 2;
 }
 
+// Weight registers of one chunk: bf16 fragments, or the raw FP8 code loads
+// (one per k-tile pair) that become fragments right before their MFMAs.
+template <bool W8, int NTW, int KC> struct WideB;
+template <int NTW, int KC> struct WideB<false, NTW, KC> { Frag<bf16> f[NTW][KC]; };
+template <int NTW, int KC> struct WideB<true, NTW, KC> { u32x4 r[NTW][KC / 2]; };
+
 // Accumulate chunks [c0, c1) of column group g into acc, then fold the
 // lo-plane rows (lanes 32-63) into their hi rows (lanes 0-31). Double
 // buffered: while a chunk's MFMAs run, the next chunk's activation
 // fragments are already on their way into the other LDS buffer (s_a holds
 // 2 * MT * KC fragments) and its weight fragments into the other register
 // set; one barrier per chunk.
-template <int MT, int KC, int NTW>
+template <int MT, int KC, int NTW, bool W8>
 __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0, int c1, bf16x8 (*s_a)[64],
                                               f32x4 (&acc)[NTW][MT]) {
+  static_assert(!W8 || KC % 2 == 0, "FP8 chunks hold whole k-tile pairs");
+  using B = WideB<W8, NTW, KC>;
   using T = bf16;
   constexpr int kTile = 512;                       // elements per 16 x 32 tile
   constexpr int kBuf = MT * KC;                    // fragments per LDS buffer
@@ -70,11 +84,14 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
   const T* W = static_cast<const T*>(p.W);
 
   const T* wp[NTW];
+  const u32x4* wq[NTW];                            // FP8: pair kp of n-tile j at wq[j] + 64 kp
   bool wv[NTW];
 #pragma unroll
   for (int j = 0; j < NTW; ++j) {
     wv[j] = ntw + j < p.NT;
     wp[j] = W + static_cast<size_t>(wv[j] ? ntw + j : 0) * KT * kTile + lane * 8;
+    wq[j] = reinterpret_cast<const u32x4*>(static_cast<const uint8_t*>(p.W) +
+                                           static_cast<size_t>(wv[j] ? ntw + j : 0) * KT * kTile) + lane;
   }
   // This lane's activation row in each M tile: row mt*8 + r16%8 of plane
   // r16/8. Rows past M read row 0; their outputs are never stored.
@@ -99,26 +116,57 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
       }
     }
   };
-  auto load_b = [&](int c, Frag<T> (&b)[NTW][KC]) {
+  auto load_b = [&](int c, B& b) {
     const int kb = c * KC;
+    if constexpr (W8) {
 #pragma unroll
-    for (int j = 0; j < NTW; ++j)
+      for (int j = 0; j < NTW; ++j)
 #pragma unroll
-      for (int u = 0; u < KC; ++u)
-        b[j][u] = wv[j] && kb + u < KT ? load_frag_stream(wp[j] + static_cast<size_t>(kb + u) * kTile)
-                                       : Frag<T>::zero();
+        for (int u = 0; u < KC / 2; ++u)     // KT is even: a pair is whole or absent
+          b.r[j][u] = wv[j] && kb + 2 * u < KT ? __builtin_nontemporal_load(wq[j] + static_cast<size_t>(kb / 2 + u) * 64)
+                                               : u32x4{0u, 0u, 0u, 0u};
+    } else {
+#pragma unroll
+      for (int j = 0; j < NTW; ++j)
+#pragma unroll
+        for (int u = 0; u < KC; ++u)
+          b.f[j][u] = wv[j] && kb + u < KT ? load_frag_stream(wp[j] + static_cast<size_t>(kb + u) * kTile)
+                                           : Frag<T>::zero();
+    }
   };
-  auto compute = [&](int c, int bb, const Frag<T> (&b)[NTW][KC]) {
+  auto compute = [&](int c, int bb, const B& b) {
     const int kb = c * KC;
+    if constexpr (W8) {
 #pragma unroll
-    for (int u = 0; u < KC; ++u) {
-      if (kb + u < KT) {
+      for (int u = 0; u < KC / 2; ++u) {
+        if (kb + 2 * u < KT) {
+          Frag<T> b0[NTW], b1[NTW];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          Frag<T> a;
-          a.v = s_a[bb * kBuf + mt * KC + u][lane];
+          for (int j = 0; j < NTW; ++j) e4m3x16_to_frags(b.r[j][u], b0[j], b1[j]);
 #pragma unroll
-          for (int j = 0; j < NTW; ++j) acc[j][mt] = mma8(acc[j][mt], a, b[j][u]);
+          for (int mt = 0; mt < MT; ++mt) {
+            Frag<T> a0, a1;
+            a0.v = s_a[bb * kBuf + mt * KC + 2 * u][lane];
+            a1.v = s_a[bb * kBuf + mt * KC + 2 * u + 1][lane];
+#pragma unroll
+            for (int j = 0; j < NTW; ++j) {
+              acc[j][mt] = mma8(acc[j][mt], a0, b0[j]);
+              acc[j][mt] = mma8(acc[j][mt], a1, b1[j]);
+            }
+          }
+        }
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < KC; ++u) {
+        if (kb + u < KT) {
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            Frag<T> a;
+            a.v = s_a[bb * kBuf + mt * KC + u][lane];
+#pragma unroll
+            for (int j = 0; j < NTW; ++j) acc[j][mt] = mma8(acc[j][mt], a, b.f[j][u]);
+          }
         }
       }
     }
@@ -126,7 +174,7 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
   // One chunk: wait for its loads (the only ones outstanding), start the
   // next chunk's, then multiply. Buffer bb ^ 1 is free: every wave passed
   // this barrier only after finishing the previous chunk, which used it.
-  auto step = [&](int c, int bb, const Frag<T> (&bcur)[NTW][KC], Frag<T> (&bnext)[NTW][KC]) {
+  auto step = [&](int c, int bb, const B& bcur, B& bnext) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (c + 1 < c1) {
@@ -136,7 +184,7 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
     compute(c, bb, bcur);
   };
 
-  Frag<T> b0[NTW][KC], b1[NTW][KC];
+  B b0, b1;
   if (c0 < c1) {
     issue_a(c0, 0);
     load_b(c0, b0);
@@ -182,8 +230,10 @@ __device__ __forceinline__ void wide_epilogue_group(const GemmParams& p, int gs,
       continue;
     }
     const float rs = s_rs[mtl * 8 + i];
-    const float v = ep[e] * rs;
-    const float v2 = (EPI == kEpiSwiglu || EPI == kEpiQkv) && col < 8 ? ep[e + 8] * rs : 0.f;
+    const float* sc = p.wscale;                    // FP8 row scales (NULL for bf16 weights)
+    const float v = ep[e] * rs * (sc ? sc[nt * 16 + col] : 1.f);
+    const float v2 = (EPI == kEpiSwiglu || EPI == kEpiQkv) && col < 8 ? ep[e + 8] * rs * (sc ? sc[nt * 16 + col + 8] : 1.f)
+                                                                      : 0.f;
     const float sq = epilogue_element<T, EPI>(p, p.m0 + m, nt, col, v, v2);
     if (EPI == kEpiResid) ep[e] = sq;              // only this thread reads element e here
   }
@@ -204,7 +254,7 @@ __device__ __forceinline__ void wide_epilogue_group(const GemmParams& p, int gs,
 
 // One work-group per column group (4 NTW n-tiles) over the whole k range,
 // epilogue fused: the folded tile goes to LDS one norm group at a time.
-template <int MT, int KC, int NTW, int EPI>
+template <int MT, int KC, int NTW, int EPI, bool W8>
 __global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, NTW>())))
 void gemm_wide_kernel(const GemmParams p, int chunks) {
   __shared__ bf16x8 s_a[2 * MT * KC][64];          // two chunks of activation fragments
@@ -218,7 +268,7 @@ void gemm_wide_kernel(const GemmParams p, int chunks) {
   constexpr int kWavesPerGroup = kWideWaves / kGroups;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   f32x4 acc[NTW][MT];
-  wide_mainloop<MT, KC, NTW>(p, blockIdx.x, 0, chunks, s_a, acc);
+  wide_mainloop<MT, KC, NTW, W8>(p, blockIdx.x, 0, chunks, s_a, acc);
   float* ep = reinterpret_cast<float*>(&s_a[0][0]);
   float* s_rs = kRsInA ? ep + kTile : s_rs_own;
 #pragma unroll
@@ -242,7 +292,7 @@ void gemm_wide_kernel(const GemmParams p, int chunks) {
 
 // Split s of column group g (work-group g + s G): chunks [s C / S, (s+1) C / S)
 // into the partial buffer.
-template <int MT, int KC, int NTW>
+template <int MT, int KC, int NTW, bool W8>
 __global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, NTW>())))
 void gemm_wide_split_kernel(const GemmParams p, int S, int chunks) {
   __shared__ bf16x8 s_a[2 * MT * KC][64];
@@ -252,7 +302,7 @@ void gemm_wide_split_kernel(const GemmParams p, int S, int chunks) {
   const int c0 = static_cast<int>(static_cast<long>(s) * chunks / S);
   const int c1 = static_cast<int>(static_cast<long>(s + 1) * chunks / S);
   f32x4 acc[NTW][MT];
-  wide_mainloop<MT, KC, NTW>(p, g, c0, c1, s_a, acc);
+  wide_mainloop<MT, KC, NTW, W8>(p, g, c0, c1, s_a, acc);
   if (lane < 32) {
     float* mine = p.part + ((static_cast<size_t>(s) * G + g) * kWideWaves + wave) * wide_part_floats<MT, NTW>();
 #pragma unroll
@@ -298,15 +348,18 @@ static const int kWideMT[] = {2, 3, 4, 5, 6, 8, 10, 12, 14, 16, 18, 20};
 // for two to three work-groups per CU up to 10 M tiles (one above 12, where
 // registers allow one wave per SIMD) and hold a norm group's output tile
 // (4 MT KiB).
+// FP8 chunks hold whole k-tile pairs: 2 where bf16 takes 3.
 static constexpr int wide_kc(int MT) { return MT <= 10 ? 4 : MT == 12 || MT == 20 ? 3 : 4; }
+static constexpr int wide_kc8(int MT) { return wide_kc(MT) == 3 ? 2 : wide_kc(MT); }
 
-WidePlan wide_plan(int NT, int KT, int M) {
+WidePlan wide_plan(int NT, int KT, int M, bool w8) {
   WidePlan w{};
   const int mt = (M + 7) / 8;
   w.MT = 20;
   for (int v : kWideMT)
     if (v >= mt) { w.MT = v; break; }
-  w.KC = wide_kc(w.MT);
+  w.w8 = w8;
+  w.KC = w8 ? wide_kc8(w.MT) : wide_kc(w.MT);
   w.NTW = wide_ntw(w.MT);
   w.G = (NT + kWideWaves * w.NTW - 1) / (kWideWaves * w.NTW);
   w.chunks = (KT + w.KC - 1) / w.KC;
@@ -326,12 +379,12 @@ size_t wide_part_bytes(const WidePlan& w) {
 
 int wide_groups(int NT) { return (NT + kNormTiles - 1) / kNormTiles; }
 
-template <int MT, int KC = wide_kc(MT), int NTW = wide_ntw(MT)>
+template <int MT, bool W8, int KC = W8 ? wide_kc8(MT) : wide_kc(MT), int NTW = wide_ntw(MT)>
 static hipError_t wide_launch(const GemmParams& p, const WidePlan& w, hipStream_t st) {
   const dim3 block(kWideWaves * 64);
-  if (w.NTW != NTW || w.KC != KC) return hipErrorInvalidValue;
+  if (w.NTW != NTW || w.KC != KC || w.w8 != W8) return hipErrorInvalidValue;
   if (w.S > 1) {
-    hipLaunchKernelGGL((gemm_wide_split_kernel<MT, KC, NTW>), dim3(w.G * w.S), block, 0, st, p, w.S, w.chunks);
+    hipLaunchKernelGGL((gemm_wide_split_kernel<MT, KC, NTW, W8>), dim3(w.G * w.S), block, 0, st, p, w.S, w.chunks);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const dim3 rgrid(wide_groups(p.NT), MT);
@@ -346,31 +399,37 @@ static hipError_t wide_launch(const GemmParams& p, const WidePlan& w, hipStream_
   }
   const dim3 grid(w.G);
   switch (p.epi) {
-    case kEpiStore: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiStore>), grid, block, 0, st, p, w.chunks); break;
-    case kEpiGelu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiGelu>), grid, block, 0, st, p, w.chunks); break;
-    case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiSwiglu>), grid, block, 0, st, p, w.chunks); break;
-    case kEpiResid: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiResid>), grid, block, 0, st, p, w.chunks); break;
-    default: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiQkv>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiStore: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiStore, W8>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiGelu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiGelu, W8>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiSwiglu, W8>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiResid: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiResid, W8>), grid, block, 0, st, p, w.chunks); break;
+    default: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiQkv, W8>), grid, block, 0, st, p, w.chunks); break;
   }
   return hipGetLastError();
 }
 
+template <bool W8>
+static hipError_t wide_dispatch(const GemmParams& p, const WidePlan& w, hipStream_t st) {
+  switch (w.MT) {
+    case 2: return wide_launch<2, W8>(p, w, st);
+    case 3: return wide_launch<3, W8>(p, w, st);
+    case 4: return wide_launch<4, W8>(p, w, st);
+    case 5: return wide_launch<5, W8>(p, w, st);
+    case 6: return wide_launch<6, W8>(p, w, st);
+    case 8: return wide_launch<8, W8>(p, w, st);
+    case 10: return wide_launch<10, W8>(p, w, st);
+    case 12: return wide_launch<12, W8>(p, w, st);
+    case 14: return wide_launch<14, W8>(p, w, st);
+    case 16: return wide_launch<16, W8>(p, w, st);
+    case 18: return wide_launch<18, W8>(p, w, st);
+    default: return wide_launch<20, W8>(p, w, st);
+  }
+}
+
 hipError_t launch_gemm_wide(const GemmParams& p, const WidePlan& w, hipStream_t st) {
   if (w.S > 1 && !p.part) return hipErrorInvalidValue;
-  switch (w.MT) {
-    case 2: return wide_launch<2>(p, w, st);
-    case 3: return wide_launch<3>(p, w, st);
-    case 4: return wide_launch<4>(p, w, st);
-    case 5: return wide_launch<5>(p, w, st);
-    case 6: return wide_launch<6>(p, w, st);
-    case 8: return wide_launch<8>(p, w, st);
-    case 10: return wide_launch<10>(p, w, st);
-    case 12: return wide_launch<12>(p, w, st);
-    case 14: return wide_launch<14>(p, w, st);
-    case 16: return wide_launch<16>(p, w, st);
-    case 18: return wide_launch<18>(p, w, st);
-    default: return wide_launch<20>(p, w, st);
-  }
+  if (w.w8 != (p.wscale != nullptr) || (w.w8 && p.KT % 2)) return hipErrorInvalidValue;
+  return w.w8 ? wide_dispatch<true>(p, w, st) : wide_dispatch<false>(p, w, st);
 }
 
 }  // namespace sps

@@ -44,12 +44,12 @@ hipError_t launch_gemm(int dtype, const GemmParams& p, hipStream_t st);
 int gemm_max_rows(int dtype);                 // rows one launch handles
 int gemm_groups(int dtype, int NT, int KT, int Mtot); // column groups (ss_out groups) of a GEMM
 
-// Wide GEMM (bf16, more than 8 rows; gemm_wide.hip): M tiles, k-tiles per
-// chunk, n-tiles per wave, column groups (4 NTW n-tiles each), k splits and
-// chunks of one launch.
-struct WidePlan { int MT, KC, NTW, G, S, chunks; };
+// Wide GEMM (bf16 activations, bf16 or FP8 weights, more than 8 rows;
+// gemm_wide.hip): M tiles, k-tiles per chunk, n-tiles per wave, column groups
+// (4 NTW n-tiles each), k splits and chunks of one launch.
+struct WidePlan { int MT, KC, NTW, G, S, chunks; bool w8; };
 bool gemm_is_wide(int dtype, int Mtot);
-WidePlan wide_plan(int NT, int KT, int M);
+WidePlan wide_plan(int NT, int KT, int M, bool w8);   // w8: FP8 weight codes
 size_t wide_part_bytes(const WidePlan& w);    // workspace for the split-K partials
 int wide_groups(int NT);                      // norm groups (8 n-tiles each)
 hipError_t launch_gemm_wide(const GemmParams& p, const WidePlan& w, hipStream_t st);

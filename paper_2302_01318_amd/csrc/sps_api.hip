@@ -119,7 +119,8 @@ WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
     const int rows[2] = {static_cast<int>(std::min<size_t>(M, cap)), static_cast<int>(M % cap)};
     for (int r : rows) {            // (every launch of a forward past 8 rows is wide)
       if (r <= 0) continue;
-      for (int i = 0; i < 5; ++i) part = std::max(part, sps::wide_part_bytes(sps::wide_plan(g[i][0], g[i][1], r)));
+      for (int i = 0; i < 5; ++i)
+        part = std::max(part, sps::wide_part_bytes(sps::wide_plan(g[i][0], g[i][1], r, L.fp8)));
     }
   }
   size_t o = 0;

@@ -9,9 +9,10 @@
 * verify step: logits within 2e-2 max-abs of the oracle forward run on the
   oracle's own dequantised weights, q the softmax of the logits, the fused
   accept / resample outputs bit-exact against the oracle on the GPU's q; the
-  appended keys and values within 2e-2. Cases: 5 rows (one M tile), 12 rows
-  (two launches per GEMM), a 64-token prefill chunk, and one full-width block
-  of the 70B and 7B shapes in the benchmark's launch shapes;
+  appended keys and values within 2e-2. Cases: 5 rows (one M tile, the
+  single-tile kernel), 12 to 144 rows (the wide kernel, with and without
+  split-K), a 64-token prefill chunk, and full-width blocks of the 70B and 7B
+  shapes in the benchmark's and the sweep's launch shapes;
 * end to end: with the draft equal to the target every draft is accepted,
   and greedy SpS emits the same tokens as greedy ArS.
 """
@@ -104,9 +105,16 @@ def test_fp8_verify_one_tile(sps):
 
 
 @pytest.mark.parametrize("ffn", ["gelu", "swiglu"])
-def test_fp8_verify_ragged_two_launches(sps, ffn):
-    # 3 sequences x 4 positions = 12 rows: two 8-row launches per GEMM
+def test_fp8_verify_ragged_wide(sps, ffn):
+    # 3 sequences x 4 positions = 12 rows: the wide kernel at 2 M tiles
     verify_parity(sps, SMALL8.with_(ffn=ffn), 3, 3, [5, 100, 257], 62, 2e-2)
+
+
+@pytest.mark.parametrize("B,K", [(12, 8), (16, 8)])
+def test_fp8_verify_large_batch(sps, B, K):
+    # 108 and 144 rows: 14 and 18 M tiles (4 and 2 n-tiles per wave)
+    g = np.random.default_rng(B + 500)
+    verify_parity(sps, SMALL8, B, K, [int(x) for x in g.integers(0, 200, B)], 70 + B, 2e-2, check_kv=False)
 
 
 def test_fp8_verify_greedy(sps):
@@ -135,6 +143,15 @@ def test_fp8_full_width_layer(sps, shape):
     """One full-width FP8 block + unembedding at K = 4, B = 1 against a
     2048-token prior: the per-layer kernels in the benchmark's launch shapes."""
     verify_parity(sps, shape.with_(n_layers=1, dtype="fp8"), 1, 4, [2048], 67, 2e-2)
+
+
+@pytest.mark.parametrize("B,K", [(4, 4), (16, 8)], ids=["B4K4", "B16K8"])
+def test_fp8_full_width_layer_batched(sps, B, K):
+    """Batched full-width FP8 blocks of the 70B shape: the wide kernel with
+    split-K on the 8192-wide outputs."""
+    g = np.random.default_rng(200 * B + K)
+    verify_parity(sps, configs.SEVENTY_B.with_(n_layers=1, dtype="fp8"), B, K,
+                  [int(x) for x in g.integers(200, 600, B)], 80 + B, 2e-2, check_kv=False)
 
 
 def test_fp8_e2e_properties(sps):
