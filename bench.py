@@ -118,6 +118,16 @@ def verify_bytes(shape, B, K, ctx):
     return weights + gains + embed_rows + kv_read + kv_write + logits
 
 
+def model_shapes(configs, args):
+    """Target (70B or 7B shape) and draft shapes, with FP8 projections when
+    --weights fp8."""
+    shape = configs.SEVENTY_B if args.shape == "70b" else configs.SEVEN_B
+    dshape = configs.DRAFT_70B
+    if args.weights == "fp8":
+        shape, dshape = shape.with_(dtype="fp8"), dshape.with_(dtype="fp8")
+    return shape, dshape
+
+
 def device_model(sps, synth, shape, seed):
     m = sps.Model(shape)
     for (name, layer), t in synth.device_weights(shape, seed):
@@ -213,7 +223,7 @@ def sweep(args):
     acceptance rates imply with the measured draft and verify times."""
     import torch
     from paper_2302_01318_amd import configs, sps, synth
-    shape, dshape = configs.SEVENTY_B, configs.DRAFT_70B
+    shape, dshape = model_shapes(configs, args)
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
     target = device_model(sps, synth, shape, args.seed)
     rows = []
@@ -293,7 +303,7 @@ def k_study(args):
     import torch
     from paper_2302_01318_amd import configs, sps, synth
     st = configs.K_STUDY
-    shape, dshape = configs.SEVENTY_B, configs.DRAFT_70B
+    shape, dshape = model_shapes(configs, args)
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
     Ks = [int(k) for k in args.k_study_K.split(",")] if args.k_study_K else list(st["K"])
     perts = [float(x) for x in args.k_study_pert.split(",")] if args.k_study_pert else list(st["code_pert"])
@@ -429,10 +439,7 @@ def main():
     import torch
     from paper_2302_01318_amd import configs, sps, synth
 
-    shape = configs.SEVENTY_B if args.shape == "70b" else configs.SEVEN_B
-    dshape = configs.DRAFT_70B
-    if args.weights == "fp8":
-        shape, dshape = shape.with_(dtype="fp8"), dshape.with_(dtype="fp8")
+    shape, dshape = model_shapes(configs, args)
     B, K, ctx = args.B, args.K, args.ctx
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
 
