@@ -173,3 +173,18 @@ def test_stream_read_helper(sps):
     assert int(sink.item()) == 0
     with pytest.raises(ValueError):
         sps.stream_read(buf, (4 << 20) + 16, sink)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_max_rows_one_launch(sps, dtype):
+    """160 rows (32 sequences x 5 positions), the most one GEMM launch takes
+    (20 M tiles), with ragged cache lengths."""
+    g = np.random.default_rng(160)
+    verify_parity(sps, SMALL.with_(dtype=dtype, ffn="swiglu", d_model=192, d_ff=320), 32, 4,
+                  [int(x) for x in g.integers(0, 90, 32)], 160, 2e-2, check_kv=False)
+
+
+def test_max_lookahead(sps):
+    """K = 63, the largest lookahead: 64 positions of one sequence (8 M tiles,
+    4 query tiles in attention)."""
+    verify_parity(sps, SMALL, 1, 63, [100], 163, 2e-2)

@@ -138,3 +138,33 @@ def test_accept_error_flags(sps):
     out, nacc = run_accept(sps, None, qz, None, np.array([[0.3]], np.float32))
     assert out[0, 0] == 0 and sps.device_error() & sps.DEV_EMPTY
     assert sps.device_error() == 0
+
+
+@pytest.mark.parametrize("V", [(1 << 20) + 7, (1 << 24) - 1])
+def test_accept_large_vocabulary(sps, V):
+    """Vocabularies far past 32000, up to the largest the ABI accepts
+    (2^24 - 1, ragged against every block size): bit-exact tokens and counts,
+    and a residual draw that lands past the first 2^20 entries."""
+    print("accept large V", V, flush=True)
+    B, K = 2, 3
+    g = np.random.default_rng(V % 1000)
+    zq = g.normal(0, 2, size=(B, K + 1, V))
+    zp = zq[:, :K] + g.normal(0, 0.5, size=(B, K, V))
+    q = np.exp(zq - zq.max(-1, keepdims=True))
+    q = (q / q.sum(-1, keepdims=True)).astype(np.float32)
+    p = np.exp(zp - zp.max(-1, keepdims=True))
+    p = (p / p.sum(-1, keepdims=True)).astype(np.float32)
+    draw = lambda w: min(V - 1, int(np.searchsorted(np.cumsum(w), g.random() * w.sum(), side="right")))
+    drafts = np.array([[draw(p[b, t].astype(np.float64)) for t in range(K)] for b in range(B)], dtype=np.int32)
+    # reject the first draft of sequence 0 (u = 1 - 2^-24 > min(1, q/p) unless q >= p there) so a
+    # residual draw happens, and force the draw's threshold high into the vocabulary
+    unif = np.float32([[1 - 2 ** -24, 0.5, 0.5, 0.97], [0.1, 0.2, 0.3, 0.999]])
+    out, nacc = run_accept(sps, p, q, drafts, unif)
+    w_out, w_n, w_flags = oacc.accept_resample(p, q, drafts, unif)
+    np.testing.assert_array_equal(out, w_out)
+    np.testing.assert_array_equal(nacc, w_n)
+    assert not w_flags.any()
+    for b in range(B):                               # emitted tokens: a accepted drafts + one draw
+        emitted = out[b, :nacc[b] + 1]
+        assert (emitted >= 0).all() and (emitted < V).all()
+    assert sps.device_error() == 0
