@@ -293,6 +293,9 @@ static hipError_t gemm_dispatch_bf16(const GemmParams& p, hipStream_t st) {
   if (gemm_is_wide(1, p.Mtot)) return launch_gemm_wide(p, wide_plan(p.NT, p.KT, p.M, false), st);
   if (p.M > ActRows<T>::kRows) return hipErrorInvalidValue;
   if (single_tile_ntw(p.NT, p.KT) == 2) return gemm_launch<T, 1, 2, 8, 4>(p, st);
+  // Narrow outputs over a long contraction (the 7B W_2 and the draft's W_2:
+  // 256 or fewer n-tiles, >= 256 k-tiles) stream faster from 8-wave groups.
+  if (p.KT >= 256) return gemm_launch<T, 1, 1, 8, 4>(p, st);
   return gemm_launch<T, 1, 1, 16, 4>(p, st);
 }
 
