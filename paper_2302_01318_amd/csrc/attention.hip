@@ -70,17 +70,19 @@ __device__ __forceinline__ void attn_block(const Frag<T> (&kf)[2][DH / 32], cons
   }
 }
 
-template <typename T, int DH>
+// NTL: nontemporal (streaming) loads of the key and value tiles.
+template <typename T, int DH, bool NTL>
 __device__ __forceinline__ void load_block(const T* __restrict__ kr, const T* __restrict__ vr, int pb, int lane,
                                            int grp, int nkv, Frag<T> (&kf)[2][DH / 32], Frag<T> (&vf)[DH / 16]) {
+  auto ld = [](const T* p) { return NTL ? load_frag_stream(p) : load_frag(p); };
 #pragma unroll
   for (int pt = 0; pt < 2; ++pt)
 #pragma unroll
     for (int dt = 0; dt < DH / 32; ++dt)
-      kf[pt][dt] = load_frag(kr + ((static_cast<size_t>(pb * 2 + pt) * (DH / 32) + dt) * 64 + lane) * 8);
+      kf[pt][dt] = ld(kr + ((static_cast<size_t>(pb * 2 + pt) * (DH / 32) + dt) * 64 + lane) * 8);
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt)
-    vf[dt] = load_frag(vr + ((static_cast<size_t>(pb) * (DH / 16) + dt) * 64 + lane) * 8);
+    vf[dt] = ld(vr + ((static_cast<size_t>(pb) * (DH / 16) + dt) * 64 + lane) * 8);
   if (pb * 32 + 32 > nkv) {
     // Positions past the last written one hold whatever the buffer held;
     // their softmax weight is 0, but 0 * NaN is not, so clear them.
@@ -96,18 +98,20 @@ __device__ __forceinline__ void load_block(const T* __restrict__ kr, const T* __
 }
 
 // Grid (ceil(T_cap / (4 WP)), H, B), 4 waves. Wave w of work-group g covers
-// positions 4 WP g + WP w .. + WP - 1 (WP = 32 or 64: one or two blocks). With one query tile (QT == 1: up to 16 new
-// tokens per sequence, every verify and draft step) the four waves' partials
-// are merged in LDS and the work-group writes one partial per 256 positions;
-// with more query tiles (prefill chunks) every wave writes its own.
-template <typename T, int DH, int QT, int WP>
+// positions 4 WP g + WP w .. + WP - 1 (WP = 32 or 64: one or two blocks),
+// issuing the loads of KP blocks together. With one query tile (QT == 1: up
+// to 16 new tokens per sequence, every verify and draft step) the four
+// waves' partials are merged in LDS and the work-group writes one partial
+// per 4 WP positions; with more query tiles (prefill chunks) every wave
+// writes its own.
+template <typename T, int DH, int QT, int WP, int KP = 1, bool NTL = false>
 __global__ __launch_bounds__(256) void attn_partial_kernel(const T* __restrict__ q, const T* __restrict__ kc,
                                                            const T* __restrict__ vc,
                                                            const int32_t* __restrict__ lengths, int pos_offset,
                                                            int Mps, int H, int T_cap, int NP, float c_log2,
                                                            float* __restrict__ part) {
   constexpr bool kMerge = QT == 1;
-  constexpr int kPre = 1;   // blocks whose loads are issued together
+  constexpr int kPre = KP;   // blocks whose loads are issued together
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int b = blockIdx.z, h = blockIdx.y;
   const int r16 = lane & 15, grp = lane >> 4;
@@ -147,7 +151,7 @@ __global__ __launch_bounds__(256) void attn_partial_kernel(const T* __restrict__
     Frag<T> vf[kPre][DH / 16];
 #pragma unroll
     for (int u = 0; u < kPre; ++u)
-      if (b0 + u < nblk) load_block<T, DH>(kr, vr, p0 / 32 + b0 + u, lane, grp, nkv, kf[u], vf[u]);
+      if (b0 + u < nblk) load_block<T, DH, NTL>(kr, vr, p0 / 32 + b0 + u, lane, grp, nkv, kf[u], vf[u]);
 #pragma unroll
     for (int u = 0; u < kPre; ++u) {
       if (b0 + u < nblk) {
@@ -260,13 +264,13 @@ int attn_partials(int T_cap) { return (T_cap + kWavePos - 1) / kWavePos; }
 
 // Decode launches (up to 16 new tokens per sequence): WP positions per wave,
 // partials merged per work-group of 4 WP positions.
-template <typename T, int DH, int WP>
+template <typename T, int DH, int WP, int KP = 1, bool NTL = false>
 static hipError_t attn_decode_t(const void* q, const void* kc, const void* vc, const int32_t* lengths,
                                 int pos_offset, int B, int Mps, int H, int T_cap, float* part, void* o,
                                 size_t oplane, hipStream_t st) {
   const float c_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(DH));
   const int groups = (T_cap + 4 * WP - 1) / (4 * WP);
-  hipLaunchKernelGGL((attn_partial_kernel<T, DH, 1, WP>), dim3(groups, H, B), dim3(256), 0, st,
+  hipLaunchKernelGGL((attn_partial_kernel<T, DH, 1, WP, KP, NTL>), dim3(groups, H, B), dim3(256), 0, st,
                      static_cast<const T*>(q), static_cast<const T*>(kc), static_cast<const T*>(vc), lengths,
                      pos_offset, Mps, H, T_cap, groups, c_log2, part);
   hipError_t e = hipGetLastError();
@@ -279,8 +283,16 @@ static hipError_t attn_decode_t(const void* q, const void* kc, const void* vc, c
 template <typename T, int DH>
 static hipError_t attn_t(const void* q, const void* kc, const void* vc, const int32_t* lengths, int pos_offset,
                          int B, int Mps, int H, int T_cap, float* part, void* o, size_t oplane, hipStream_t st) {
-  if (Mps <= 16)
+  if (Mps <= 16) {
+    // From a sweep over 24-64 heads, contexts 2048-8192 and 1-4 sequences:
+    // with >= 512 work-groups (two per CU) both blocks' loads in flight and
+    // nontemporal K/V loads (70B at ctx 2048: 19.3 vs 20.6 us, at ctx 8192:
+    // 56.9 vs 66.1 us); below, one block at a time with regular loads.
+    const long wgs = static_cast<long>((T_cap + 255) / 256) * H * B;
+    if (wgs >= 512)
+      return attn_decode_t<T, DH, 64, 2, true>(q, kc, vc, lengths, pos_offset, B, Mps, H, T_cap, part, o, oplane, st);
     return attn_decode_t<T, DH, 64>(q, kc, vc, lengths, pos_offset, B, Mps, H, T_cap, part, o, oplane, st);
+  }
   // Prefill chunks: 2 or 4 query tiles, every wave writes its own partial.
   const float c_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(DH));
   const int groups = (T_cap + 4 * kWavePos - 1) / (4 * kWavePos);
