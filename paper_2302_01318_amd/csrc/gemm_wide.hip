@@ -157,16 +157,25 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
         }
       }
     } else {
+      // Fragment f = u MT + mt. LDS reads run kLook fragments ahead of the
+      // MFMAs that consume them, so their latency hides behind the MFMAs of
+      // the fragments before (at large MT one wave per SIMD leaves nothing
+      // else to hide it).
+      constexpr int kNF = KC * MT;
+      constexpr int kLook = 4;
+      const int nu = KT - kb < KC ? KT - kb : KC;  // k-tiles of this chunk that exist
+      auto frag_at = [&](int f) { return s_a[bb * kBuf + (f % MT) * KC + f / MT][lane]; };
+      Frag<T> ring[kLook];
 #pragma unroll
-      for (int u = 0; u < KC; ++u) {
-        if (kb + u < KT) {
+      for (int f = 0; f < kLook && f < kNF; ++f) ring[f].v = frag_at(f);
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            Frag<T> a;
-            a.v = s_a[bb * kBuf + mt * KC + u][lane];
+      for (int f = 0; f < kNF; ++f) {
+        const int u = f / MT, mt = f % MT;
+        const Frag<T> a = ring[f % kLook];
+        if (f + kLook < kNF) ring[f % kLook].v = frag_at(f + kLook);
+        if (u < nu) {
 #pragma unroll
-            for (int j = 0; j < NTW; ++j) acc[j][mt] = mma8(acc[j][mt], a, b.f[j][u]);
-          }
+          for (int j = 0; j < NTW; ++j) acc[j][mt] = mma8(acc[j][mt], a, b.f[j][u]);
         }
       }
     }
