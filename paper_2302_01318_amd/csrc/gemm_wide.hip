@@ -47,6 +47,17 @@ constexpr int kNormTiles = 8;                      // n-tiles per norm group (12
 // fit the register file, and the spilled kernel is no faster than NTW = 2.
 static constexpr int wide_ntw(int MT) { return MT == 14 ? 4 : 2; }
 
+// From 16 M tiles the weights go through LDS too (wide_mainloop_staged):
+// with one wave per SIMD, register-held weights allow one chunk in flight;
+// an LDS ring of kWideStages chunks allows three.
+static constexpr bool wide_staged(int MT) { return MT >= 16; }
+constexpr int kWideStages = 4;
+
+// s_waitcnt operand that waits until at most n vector memory operations of
+// this wave are outstanding, ignoring the export and LDS/scalar counters
+// (gfx9 encoding: vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+constexpr int vmcnt_only(int n) { return (n & 15) | ((n >> 4) & 3) << 14 | 7 << 4 | 15 << 8; }
+
 // Partial tile of one wave: NTW x MT fragments of 32 lanes x 4 floats (the
 // hi rows after folding the lo rows in), in register order.
 template <int MT, int NTW> constexpr int wide_part_floats() { return NTW * MT * 128; }
@@ -211,6 +222,182 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
       for (int r = 0; r < 4; ++r) acc[j][mt][r] += __shfl_xor(acc[j][mt][r], 32);
 }
 
+// One global_load_lds copy (16 bytes per lane, lane l to LDS address
+// lds + 16 l), written as inline assembly so that the compiler's wait-count
+// insertion does not track it: for a tracked copy it makes every later LDS
+// read wait for all copies in flight, whatever buffer they fill. The caller
+// waits for the copies itself (s_waitcnt vmcnt) before reading what they
+// wrote; the kernel has no other vector memory operations in flight then.
+__device__ __forceinline__ void lds_copy16_untracked(const void* src, uint32_t lds) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds) : "memory");
+}
+
+// One activation fragment of zeros: the source of k-tiles past KT in the
+// staged main loop (zero activations times finite weights add exact zeros).
+__device__ const bf16x8 kZeroFrag[64] = {};
+
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));   // low half of the flat address
+}
+
+// The main loop with the weights, too, copied into LDS: activation chunks
+// double-buffered as in wide_mainloop, weight chunks in a ring of
+// kWideStages buffers filled kWideStages - 2 chunks ahead of the chunk whose
+// activations are copied. Step c copies the activations of chunk c + 1 and
+// then the weights of chunk c + kWideStages - 1 (each only if that chunk is
+// one of this work-group's), so when step c starts, the copies issued after
+// chunk c's activations are at most the weights of chunk c + kWideStages - 2:
+// waiting until only those are outstanding (vmcnt), then a barrier, makes
+// chunk c's activations and weights visible to every wave while later
+// weights stay in flight. A buffer is refilled only after the barrier that
+// follows the last reads of the chunk it held.
+template <int MT, int KC, int NTW, bool W8>
+__device__ __forceinline__ void wide_mainloop_staged(const GemmParams& p, int g, int c0, int c1,
+                                                     bf16x8 (*s_a)[64], bf16x8 (*s_w)[64],
+                                                     f32x4 (&acc)[NTW][MT]) {
+  using T = bf16;
+  constexpr int kS = kWideStages;
+  constexpr int kBuf = MT * KC;                              // activation fragments per chunk
+  constexpr int kWF = W8 ? KC / 2 : KC;                      // weight fragments per n-tile and chunk
+  constexpr int kWSlots = kWideWaves * NTW * kWF;            // weight fragments per stage
+  constexpr int kALoads = kBuf / kWideWaves;
+  constexpr int kWLoads = NTW * kWF;
+  constexpr uint32_t kFragBytes = 64 * 16;
+  static_assert(kBuf % kWideWaves == 0, "activation fragments split evenly over the waves");
+  static_assert(KC == 2, "activation blocks hold the two k-tiles of a chunk");
+  static_assert(kS >= 3 && kALoads + (kS - 1) * kWLoads <= 63, "copies in flight fit the vmcnt counter");
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int ntw = g * kWideWaves * NTW + wave * NTW;        // first n-tile of this wave
+  const int KT = p.KT, M = p.M;
+  // This lane's 16 bytes of weight fragment (n-tile j, unit k) at
+  // wbase[j] + 1 KiB k, a unit being a k-tile (bf16) or a k-tile pair (FP8
+  // codes). n-tiles past NT read n-tile 0; their outputs are never stored.
+  const char* wbase[NTW];
+#pragma unroll
+  for (int j = 0; j < NTW; ++j)
+    wbase[j] = static_cast<const char*>(p.W) +
+               static_cast<size_t>(ntw + j < p.NT ? ntw + j : 0) * KT * 512 * (W8 ? 1 : 2) + lane * 16;
+  const int kUnits = W8 ? KT / 2 : KT;
+  const uint32_t a_lds = lds_address(&s_a[0][0]), w_lds = lds_address(&s_w[0][0]);
+
+#pragma unroll
+  for (int j = 0; j < NTW; ++j)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // Activation chunk c into buffer bb as 2 MT blocks of 1 KiB: block
+  // 2 mt + h holds rows 4 h .. 4 h + 3 of M tile mt in both planes, each
+  // row's 128 bytes (both k-tiles of the chunk) whole, so every copy
+  // instruction reads 8 complete 128-byte lines (fragment-order copies read
+  // 16 half lines). Lane 8 rho + q of a block copies the 16-byte piece
+  // q ^ r ^ pl of row r = 4 h + rho % 4 of plane pl = rho / 4: the XOR
+  // swizzle makes the MFMA-order LDS reads below conflict-free. Pieces of
+  // k-tiles past KT read zeros, so every chunk runs all its MFMAs.
+  const int c_rho = lane >> 3, c_pl = c_rho >> 2;
+  const T* X = static_cast<const T*>(p.X) + c_pl * p.xplane;
+  auto issue_a = [&](int c, int bb) {
+    const int kb = c * KC;
+#pragma unroll
+    for (int i = 0; i < kALoads; ++i) {
+      const int f = wave + i * kWideWaves;               // block 2 mt + h
+      const int mt = f >> 1, r = (f & 1) * 4 + (c_rho & 3);
+      const int piece = (lane & 7) ^ r ^ c_pl;           // 16-byte piece of the row: k-tile piece / 4, group piece % 4
+      const int m = mt * 8 + r;
+      const void* src = kb + (piece >> 2) < KT
+                            ? static_cast<const void*>(X + static_cast<size_t>(p.m0 + (m < M ? m : 0)) * p.ldx +
+                                                       kb * 32 + piece * 8)
+                            : static_cast<const void*>(&kZeroFrag[lane]);
+      lds_copy16_untracked(src, a_lds + (bb * kBuf + f) * kFragBytes);
+    }
+  };
+  // The MFMA A operand of k-tile u, M tile mt: lane l takes row r = l % 8 of
+  // plane pl = (l / 8) % 2, k-group l / 16, from block 2 mt + r / 4 at the
+  // swizzled slot.
+  const int rd_r = lane & 7, rd_pl = (lane >> 3) & 1, rd_g = lane >> 4;
+  const int rd_blk = rd_r >> 2;
+  const int rd_slot0 = (rd_pl * 4 + (rd_r & 3)) * 8 + (rd_g ^ rd_r ^ rd_pl);
+  const int rd_slot1 = (rd_pl * 4 + (rd_r & 3)) * 8 + ((4 + rd_g) ^ rd_r ^ rd_pl);
+  // Weight fragments of chunk c into stage st: slot (wave NTW + j) kWF + u;
+  // units past the last re-read it (finite weights, times zero activations).
+  auto issue_w = [&](int c, int st) {
+    const int ub = c * kWF;
+#pragma unroll
+    for (int j = 0; j < NTW; ++j)
+#pragma unroll
+      for (int u = 0; u < kWF; ++u) {
+        const int k = ub + u < kUnits ? ub + u : kUnits - 1;
+        lds_copy16_untracked(wbase[j] + static_cast<size_t>(k) * kFragBytes,
+                             w_lds + (st * kWSlots + (wave * NTW + j) * kWF + u) * kFragBytes);
+      }
+  };
+  // MFMAs of a chunk (activation buffer bb, weight stage st), k-tile-major:
+  // activation fragment f = u MT + mt times the B fragments of k-tile u
+  // (FP8: converted from their pair's codes first). LDS reads run kLook
+  // fragments ahead of their MFMAs; the scheduling barriers keep the compiler
+  // from sinking each read back to just before its use, where with one wave
+  // per SIMD nothing hides its latency.
+  auto compute = [&](int bb, int st) {
+    const bf16x8* wst = &s_w[st * kWSlots + wave * NTW * kWF][0];
+    Frag<T> b[NTW][KC];
+#pragma unroll
+    for (int j = 0; j < NTW; ++j)
+#pragma unroll
+      for (int u = 0; u < kWF; ++u) {
+        const bf16x8 raw = wst[(j * kWF + u) * 64 + lane];
+        if constexpr (W8)
+          e4m3x16_to_frags(__builtin_bit_cast(u32x4, raw), b[j][2 * u], b[j][2 * u + 1]);
+        else
+          b[j][u].v = raw;
+      }
+    constexpr int kNF = KC * MT;
+    constexpr int kLook = 4;
+    auto frag_at = [&](int f) {
+      return s_a[bb * kBuf + (f % MT) * 2 + rd_blk][f / MT ? rd_slot1 : rd_slot0];
+    };
+    Frag<T> ring[kLook];
+#pragma unroll
+    for (int f = 0; f < kLook && f < kNF; ++f) ring[f].v = frag_at(f);
+#pragma unroll
+    for (int f = 0; f < kNF; ++f) {
+      const int u = f / MT, mt = f % MT;
+      const Frag<T> a = ring[f % kLook];
+      if (f + kLook < kNF) ring[f % kLook].v = frag_at(f + kLook);
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) acc[j][mt] = mma8(acc[j][mt], a, b[j][u]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  if (c0 < c1) {
+#pragma unroll
+    for (int i = 0; i < kS - 2; ++i)
+      if (c0 + i < c1) issue_w(c0 + i, i);
+    issue_a(c0, 0);
+    if (c0 + kS - 2 < c1) issue_w(c0 + kS - 2, kS - 2);
+    for (int c = c0; c < c1; ++c) {
+      const int bb = (c - c0) & 1, st = (c - c0) % kS;
+      if (c + kS - 2 < c1)
+        __builtin_amdgcn_s_waitcnt(vmcnt_only(kWLoads));   // chunk c + kS - 2's weights may stay in flight
+      else
+        __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+      // A bare barrier: __syncthreads() would also wait for every copy in
+      // flight. The clobber keeps the compiler from moving LDS accesses across.
+      asm volatile("s_barrier" ::: "memory");
+      if (c + 1 < c1) issue_a(c + 1, bb ^ 1);
+      if (c + kS - 1 < c1) issue_w(c + kS - 1, (c + kS - 1 - c0) % kS);
+      compute(bb, st);
+    }
+  }
+  __syncthreads();                                 // LDS free for the caller (epilogue tile)
+#pragma unroll
+  for (int j = 0; j < NTW; ++j)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[j][mt][r] += __shfl_xor(acc[j][mt][r], 32);
+}
+
 // Row scales of the input RMSNorm for rows mt0 * 8 .. (mt0 + NMT) * 8 - 1
 // into s_rs (the caller synchronises before use).
 template <int NMT>
@@ -267,6 +454,7 @@ template <int MT, int KC, int NTW, int EPI, bool W8>
 __global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, NTW>())))
 void gemm_wide_kernel(const GemmParams p, int chunks) {
   __shared__ bf16x8 s_a[2 * MT * KC][64];          // two chunks of activation fragments
+  __shared__ bf16x8 s_w[wide_staged(MT) ? kWideStages * kWideWaves * NTW * (W8 ? KC / 2 : KC) : 1][64];
   // One norm group's output tile reuses the chunk buffers, dead after the
   // loop, and so do the row scales where they fit behind it.
   constexpr int kTile = kNormTiles * MT * 128;     // floats
@@ -277,7 +465,10 @@ void gemm_wide_kernel(const GemmParams p, int chunks) {
   constexpr int kWavesPerGroup = kWideWaves / kGroups;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   f32x4 acc[NTW][MT];
-  wide_mainloop<MT, KC, NTW, W8>(p, blockIdx.x, 0, chunks, s_a, acc);
+  if constexpr (wide_staged(MT))
+    wide_mainloop_staged<MT, KC, NTW, W8>(p, blockIdx.x, 0, chunks, s_a, s_w, acc);
+  else
+    wide_mainloop<MT, KC, NTW, W8>(p, blockIdx.x, 0, chunks, s_a, acc);
   float* ep = reinterpret_cast<float*>(&s_a[0][0]);
   float* s_rs = kRsInA ? ep + kTile : s_rs_own;
 #pragma unroll
@@ -305,13 +496,17 @@ template <int MT, int KC, int NTW, bool W8>
 __global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, NTW>())))
 void gemm_wide_split_kernel(const GemmParams p, int S, int chunks) {
   __shared__ bf16x8 s_a[2 * MT * KC][64];
+  __shared__ bf16x8 s_w[wide_staged(MT) ? kWideStages * kWideWaves * NTW * (W8 ? KC / 2 : KC) : 1][64];
   const int G = (p.NT + kWideWaves * NTW - 1) / (kWideWaves * NTW);
   const int g = blockIdx.x % G, s = blockIdx.x / G;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c0 = static_cast<int>(static_cast<long>(s) * chunks / S);
   const int c1 = static_cast<int>(static_cast<long>(s + 1) * chunks / S);
   f32x4 acc[NTW][MT];
-  wide_mainloop<MT, KC, NTW, W8>(p, g, c0, c1, s_a, acc);
+  if constexpr (wide_staged(MT))
+    wide_mainloop_staged<MT, KC, NTW, W8>(p, g, c0, c1, s_a, s_w, acc);
+  else
+    wide_mainloop<MT, KC, NTW, W8>(p, g, c0, c1, s_a, acc);
   if (lane < 32) {
     float* mine = p.part + ((static_cast<size_t>(s) * G + g) * kWideWaves + wave) * wide_part_floats<MT, NTW>();
 #pragma unroll
@@ -358,7 +553,7 @@ static const int kWideMT[] = {2, 3, 4, 5, 6, 8, 10, 12, 14, 16, 18, 20};
 // registers allow one wave per SIMD) and hold a norm group's output tile
 // (4 MT KiB).
 // FP8 chunks hold whole k-tile pairs: 2 where bf16 takes 3.
-static constexpr int wide_kc(int MT) { return MT <= 10 ? 4 : MT == 12 || MT == 20 ? 3 : 4; }
+static constexpr int wide_kc(int MT) { return wide_staged(MT) ? 2 : MT <= 10 || MT == 14 ? 4 : 3; }
 static constexpr int wide_kc8(int MT) { return wide_kc(MT) == 3 ? 2 : wide_kc(MT); }
 
 WidePlan wide_plan(int NT, int KT, int M, bool w8) {

@@ -98,6 +98,16 @@ def test_small_bf16_large_batch(sps, B, K):
                   check_kv=False)
 
 
+@pytest.mark.parametrize("B,K", [(16, 8), (25, 4)])
+def test_small_bf16_odd_depth_wide(sps, B, K):
+    """Contraction depths of 5, 6 and 9 k-tiles (d_model 160, three 64-wide
+    heads, d_ff 288) at 144 and 125 rows (18 and 16 M tiles): two-k-tile
+    chunks of the wide GEMM whose last chunk holds a single k-tile."""
+    g = np.random.default_rng(B + 900)
+    verify_parity(sps, SMALL.with_(d_model=160, d_ff=288, ffn="swiglu"), B, K,
+                  [int(x) for x in g.integers(0, 150, B)], 90 + B, 2e-2, check_kv=False)
+
+
 def test_small_fp32_greedy(sps):
     verify_parity(sps, SMALL.with_(dtype="f32"), 2, 4, [20, 77], 5, 1e-4, T=0.0)
 
