@@ -11,11 +11,11 @@
 //    at 14 M tiles, where each fragment read from LDS then feeds four MFMAs
 //    instead of two) and one contiguous range of the k-tiles; wave w
 //    multiplies n-tiles NTW w .. NTW w + NTW - 1 by all MT M tiles;
-//  * per chunk of KC k-tiles the work-group copies the MT x KC activation
-//    fragments once into LDS with global_load_lds (16 B per lane, each
-//    wave instruction one fragment in register order), so the four waves
-//    share them, and every wave streams its own weight fragments from HBM
-//    into registers;
+//  * per chunk of KC k-tiles the work-group copies the chunk's activations
+//    once into LDS with global_load_lds (16 B per lane, whole 128-byte
+//    lines per instruction: act_piece_src), so the four waves share them,
+//    and every wave streams its own weight fragments from HBM into
+//    registers (from 16 M tiles through LDS as well: the staged loop);
 //  * where N is too small to give every CU a work-group (the d_model-wide
 //    outputs), the k range is split S ways (split-K): each split writes its
 //    fp32 partial tile to the workspace and a second kernel sums the splits
@@ -41,16 +41,16 @@ namespace sps {
 constexpr int kWideWaves = 4;                      // waves per work-group
 constexpr int kNormTiles = 8;                      // n-tiles per norm group (128 columns)
 
-// n-tiles per wave: 4 at 14 M tiles (one wave per SIMD either way; W_1 and
-// W_2 of the 70B shape run 22-24 % faster than with 2). From 16 M tiles the
-// 4 x MT accumulators and the compiler's early LDS fragment reads no longer
-// fit the register file, and the spilled kernel is no faster than NTW = 2.
-static constexpr int wide_ntw(int MT) { return MT == 14 ? 4 : 2; }
+// n-tiles per wave. (With register-held weights, 4 at 14 M tiles ran the
+// 70B W_1 and W_2 22-24 % faster than 2; the staged loop at 2 beats both.)
+static constexpr int wide_ntw(int) { return 2; }
 
-// From 16 M tiles the weights go through LDS too (wide_mainloop_staged):
-// with one wave per SIMD, register-held weights allow one chunk in flight;
-// an LDS ring of kWideStages chunks allows three.
-static constexpr bool wide_staged(int MT) { return MT >= 16; }
+// Where the weights go through LDS too (wide_mainloop_staged): from 14 M
+// tiles for bf16 weights, where one wave per SIMD with register-held weights
+// has one chunk in flight, and from 8 for FP8 codes, whose register path
+// keeps only 4 KiB per wave in flight. Below, the register path with two to
+// three work-groups per CU is faster.
+static constexpr bool wide_staged(int MT, bool w8) { return MT >= (w8 ? 8 : 14); }
 constexpr int kWideStages = 4;
 
 // s_waitcnt operand that waits until at most n vector memory operations of
@@ -65,7 +65,7 @@ template <int MT, int NTW> constexpr int wide_part_floats() { return NTW * MT * 
 // Waves per SIMD the register allocation must allow (the compiler would
 // otherwise hoist every LDS fragment read of a chunk into registers).
 template <int MT, int NTW> constexpr int wide_waves_per_simd() {
-  return NTW == 4 || MT > 12 ? 1 : MT <= 6 ? 3 : 2;
+  return MT > 12 ? 1 : MT <= 6 ? 3 : 2;
 }
 
 // Weight registers of one chunk: bf16 fragments, or the raw FP8 code loads
@@ -73,6 +73,55 @@ template <int MT, int NTW> constexpr int wide_waves_per_simd() {
 template <bool W8, int NTW, int KC> struct WideB;
 template <int NTW, int KC> struct WideB<false, NTW, KC> { Frag<bf16> f[NTW][KC]; };
 template <int NTW, int KC> struct WideB<true, NTW, KC> { u32x4 r[NTW][KC / 2]; };
+
+// One global_load_lds copy (16 bytes per lane, lane l to LDS address
+// lds + 16 l), written as inline assembly so that the compiler's wait-count
+// insertion does not track it: for a tracked copy it makes every later LDS
+// read wait for all copies in flight, whatever buffer they fill. The caller
+// waits for the copies itself (s_waitcnt vmcnt) before reading what they
+// wrote; the kernel has no other vector memory operations in flight then.
+__device__ __forceinline__ void lds_copy16_untracked(const void* src, uint32_t lds) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds) : "memory");
+}
+
+// One activation fragment of zeros: the source of activation pieces past
+// KT (zero activations times finite weights add exact zeros).
+__device__ const bf16x8 kZeroFrag[64] = {};
+
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));   // low half of the flat address
+}
+
+// Activation blocks. A chunk's activations go to LDS as blocks of 1 KiB, one
+// per (M tile mt, k-tile pair, half h): rows 4 h .. 4 h + 3 of the M tile in
+// both planes, each row's 128 bytes (the two k-tiles of the pair) whole, so
+// every copy instruction reads 8 complete 128-byte lines where a copy in
+// MFMA fragment order would read 16 half lines. Lane 8 rho + q of a block
+// copies the 16-byte piece q ^ r ^ pl of row r = 4 h + rho % 4 of plane
+// pl = rho / 4; the XOR swizzle makes the MFMA-order reads conflict-free
+// (every 8 and every 16 consecutive lanes of a ds_read_b128 hit distinct
+// 16-byte bank groups).
+//
+// Source of this lane's piece of block (mt, h) of the pair starting at
+// k-tile kb; pieces of k-tiles past KT read zeros.
+__device__ __forceinline__ const void* act_piece_src(const GemmParams& p, int lane, int mt, int h, int kb) {
+  const int rho = lane >> 3, pl = rho >> 2;
+  const int r = h * 4 + (rho & 3);
+  const int piece = (lane & 7) ^ r ^ pl;            // k-tile kb + piece / 4, k-group piece % 4
+  const int m = mt * 8 + r;
+  if (kb + (piece >> 2) >= p.KT) return &kZeroFrag[lane];
+  return static_cast<const bf16*>(p.X) + pl * p.xplane + static_cast<size_t>(p.m0 + (m < p.M ? m : 0)) * p.ldx +
+         kb * 32 + piece * 8;
+}
+
+// Where the MFMA A operand of a pair's k-tile u (0 or 1) sits for this
+// lane (row l % 8 of plane (l / 8) % 2, k-group l / 16): block half
+// act_half(lane), slot act_slot(lane, u).
+__device__ __forceinline__ int act_half(int lane) { return (lane & 7) >> 2; }
+__device__ __forceinline__ int act_slot(int lane, int u) {
+  const int r = lane & 7, pl = (lane >> 3) & 1, g = lane >> 4;
+  return (pl * 4 + (r & 3)) * 8 + ((u * 4 + g) ^ r ^ pl);
+}
 
 // Accumulate chunks [c0, c1) of column group g into acc, then fold the
 // lo-plane rows (lanes 32-63) into their hi rows (lanes 0-31). Double
@@ -83,15 +132,14 @@ template <int NTW, int KC> struct WideB<true, NTW, KC> { u32x4 r[NTW][KC / 2]; }
 template <int MT, int KC, int NTW, bool W8>
 __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0, int c1, bf16x8 (*s_a)[64],
                                               f32x4 (&acc)[NTW][MT]) {
-  static_assert(!W8 || KC % 2 == 0, "FP8 chunks hold whole k-tile pairs");
+  static_assert(KC % 2 == 0, "chunks hold whole k-tile pairs (activation blocks, FP8 codes)");
   using B = WideB<W8, NTW, KC>;
   using T = bf16;
   constexpr int kTile = 512;                       // elements per 16 x 32 tile
   constexpr int kBuf = MT * KC;                    // fragments per LDS buffer
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ntw = g * kWideWaves * NTW + wave * NTW;   // first n-tile of this wave
-  const int r16 = lane & 15, grp = lane >> 4;
-  const int KT = p.KT, M = p.M;
+  const int KT = p.KT;
   const T* W = static_cast<const T*>(p.W);
 
   const T* wp[NTW];
@@ -104,28 +152,27 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
     wq[j] = reinterpret_cast<const u32x4*>(static_cast<const uint8_t*>(p.W) +
                                            static_cast<size_t>(wv[j] ? ntw + j : 0) * KT * kTile) + lane;
   }
-  // This lane's activation row in each M tile: row mt*8 + r16%8 of plane
-  // r16/8. Rows past M read row 0; their outputs are never stored.
-  const int arow = r16 & 7;
-  const T* xbase = static_cast<const T*>(p.X) + (r16 >> 3) * p.xplane + grp * 8;
+  const int a_half = act_half(lane), a_slot0 = act_slot(lane, 0), a_slot1 = act_slot(lane, 1);
 
 #pragma unroll
   for (int j = 0; j < NTW; ++j)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // Activation fragments of chunk c into LDS buffer bb, fragment f = mt * KC + u.
+  // Activation blocks of chunk c into LDS buffer bb: block f = 2 (mt KC / 2
+  // + pair) + h; pairs wholly past KT are skipped (their MFMAs are).
   auto issue_a = [&](int c, int bb) {
     const int kb = c * KC;
     for (int f = wave; f < kBuf; f += kWideWaves) {
-      const int mt = f / KC, u = f % KC;
-      if (kb + u < KT) {
-        const int m = mt * 8 + arow;
-        const T* src = xbase + static_cast<size_t>(p.m0 + (m < M ? m : 0)) * p.ldx + (kb + u) * 32;
-        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src),
+      const int h = f & 1, pr = (f >> 1) % (KC / 2), mt = (f >> 1) / (KC / 2);
+      if (kb + 2 * pr < KT)
+        __builtin_amdgcn_global_load_lds(act_piece_src(p, lane, mt, h, kb + 2 * pr),
                                          reinterpret_cast<void*>(&s_a[bb * kBuf + f][0]), 16, 0, 0);
-      }
     }
+  };
+  // A operand of k-tile u of the chunk, M tile mt, from buffer bb.
+  auto frag_a = [&](int bb, int mt, int u) {
+    return s_a[bb * kBuf + (mt * (KC / 2) + u / 2) * 2 + a_half][u % 2 ? a_slot1 : a_slot0];
   };
   auto load_b = [&](int c, B& b) {
     const int kb = c * KC;
@@ -157,8 +204,8 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
             Frag<T> a0, a1;
-            a0.v = s_a[bb * kBuf + mt * KC + 2 * u][lane];
-            a1.v = s_a[bb * kBuf + mt * KC + 2 * u + 1][lane];
+            a0.v = frag_a(bb, mt, 2 * u);
+            a1.v = frag_a(bb, mt, 2 * u + 1);
 #pragma unroll
             for (int j = 0; j < NTW; ++j) {
               acc[j][mt] = mma8(acc[j][mt], a0, b0[j]);
@@ -175,7 +222,7 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
       constexpr int kNF = KC * MT;
       constexpr int kLook = 4;
       const int nu = KT - kb < KC ? KT - kb : KC;  // k-tiles of this chunk that exist
-      auto frag_at = [&](int f) { return s_a[bb * kBuf + (f % MT) * KC + f / MT][lane]; };
+      auto frag_at = [&](int f) { return frag_a(bb, f % MT, f / MT); };
       Frag<T> ring[kLook];
 #pragma unroll
       for (int f = 0; f < kLook && f < kNF; ++f) ring[f].v = frag_at(f);
@@ -222,24 +269,6 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
       for (int r = 0; r < 4; ++r) acc[j][mt][r] += __shfl_xor(acc[j][mt][r], 32);
 }
 
-// One global_load_lds copy (16 bytes per lane, lane l to LDS address
-// lds + 16 l), written as inline assembly so that the compiler's wait-count
-// insertion does not track it: for a tracked copy it makes every later LDS
-// read wait for all copies in flight, whatever buffer they fill. The caller
-// waits for the copies itself (s_waitcnt vmcnt) before reading what they
-// wrote; the kernel has no other vector memory operations in flight then.
-__device__ __forceinline__ void lds_copy16_untracked(const void* src, uint32_t lds) {
-  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds) : "memory");
-}
-
-// One activation fragment of zeros: the source of k-tiles past KT in the
-// staged main loop (zero activations times finite weights add exact zeros).
-__device__ const bf16x8 kZeroFrag[64] = {};
-
-__device__ __forceinline__ uint32_t lds_address(const void* p) {
-  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));   // low half of the flat address
-}
-
 // The main loop with the weights, too, copied into LDS: activation chunks
 // double-buffered as in wide_mainloop, weight chunks in a ring of
 // kWideStages buffers filled kWideStages - 2 chunks ahead of the chunk whose
@@ -260,16 +289,15 @@ __device__ __forceinline__ void wide_mainloop_staged(const GemmParams& p, int g,
   constexpr int kBuf = MT * KC;                              // activation fragments per chunk
   constexpr int kWF = W8 ? KC / 2 : KC;                      // weight fragments per n-tile and chunk
   constexpr int kWSlots = kWideWaves * NTW * kWF;            // weight fragments per stage
-  constexpr int kALoads = kBuf / kWideWaves;
+  constexpr int kALoads = (kBuf + kWideWaves - 1) / kWideWaves;
   constexpr int kWLoads = NTW * kWF;
   constexpr uint32_t kFragBytes = 64 * 16;
-  static_assert(kBuf % kWideWaves == 0, "activation fragments split evenly over the waves");
   static_assert(KC == 2, "activation blocks hold the two k-tiles of a chunk");
   static_assert(kS >= 3 && kALoads + (kS - 1) * kWLoads <= 63, "copies in flight fit the vmcnt counter");
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int ntw = g * kWideWaves * NTW + wave * NTW;        // first n-tile of this wave
-  const int KT = p.KT, M = p.M;
+  const int KT = p.KT;
   // This lane's 16 bytes of weight fragment (n-tile j, unit k) at
   // wbase[j] + 1 KiB k, a unit being a k-tile (bf16) or a k-tile pair (FP8
   // codes). n-tiles past NT read n-tile 0; their outputs are never stored.
@@ -286,38 +314,18 @@ __device__ __forceinline__ void wide_mainloop_staged(const GemmParams& p, int g,
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // Activation chunk c into buffer bb as 2 MT blocks of 1 KiB: block
-  // 2 mt + h holds rows 4 h .. 4 h + 3 of M tile mt in both planes, each
-  // row's 128 bytes (both k-tiles of the chunk) whole, so every copy
-  // instruction reads 8 complete 128-byte lines (fragment-order copies read
-  // 16 half lines). Lane 8 rho + q of a block copies the 16-byte piece
-  // q ^ r ^ pl of row r = 4 h + rho % 4 of plane pl = rho / 4: the XOR
-  // swizzle makes the MFMA-order LDS reads below conflict-free. Pieces of
-  // k-tiles past KT read zeros, so every chunk runs all its MFMAs.
-  const int c_rho = lane >> 3, c_pl = c_rho >> 2;
-  const T* X = static_cast<const T*>(p.X) + c_pl * p.xplane;
+  // Activation chunk c (one k-tile pair) into buffer bb as 2 MT blocks:
+  // block 2 mt + h. Pieces of k-tiles past KT read zeros, so every chunk
+  // runs all its MFMAs.
   auto issue_a = [&](int c, int bb) {
-    const int kb = c * KC;
 #pragma unroll
     for (int i = 0; i < kALoads; ++i) {
-      const int f = wave + i * kWideWaves;               // block 2 mt + h
-      const int mt = f >> 1, r = (f & 1) * 4 + (c_rho & 3);
-      const int piece = (lane & 7) ^ r ^ c_pl;           // 16-byte piece of the row: k-tile piece / 4, group piece % 4
-      const int m = mt * 8 + r;
-      const void* src = kb + (piece >> 2) < KT
-                            ? static_cast<const void*>(X + static_cast<size_t>(p.m0 + (m < M ? m : 0)) * p.ldx +
-                                                       kb * 32 + piece * 8)
-                            : static_cast<const void*>(&kZeroFrag[lane]);
-      lds_copy16_untracked(src, a_lds + (bb * kBuf + f) * kFragBytes);
+      const int f = wave + i * kWideWaves;
+      if (kBuf % kWideWaves && f >= kBuf) break;       // uneven split: this wave's count is one lower
+      lds_copy16_untracked(act_piece_src(p, lane, f >> 1, f & 1, c * KC), a_lds + (bb * kBuf + f) * kFragBytes);
     }
   };
-  // The MFMA A operand of k-tile u, M tile mt: lane l takes row r = l % 8 of
-  // plane pl = (l / 8) % 2, k-group l / 16, from block 2 mt + r / 4 at the
-  // swizzled slot.
-  const int rd_r = lane & 7, rd_pl = (lane >> 3) & 1, rd_g = lane >> 4;
-  const int rd_blk = rd_r >> 2;
-  const int rd_slot0 = (rd_pl * 4 + (rd_r & 3)) * 8 + (rd_g ^ rd_r ^ rd_pl);
-  const int rd_slot1 = (rd_pl * 4 + (rd_r & 3)) * 8 + ((4 + rd_g) ^ rd_r ^ rd_pl);
+  const int a_half = act_half(lane), a_slot0 = act_slot(lane, 0), a_slot1 = act_slot(lane, 1);
   // Weight fragments of chunk c into stage st: slot (wave NTW + j) kWF + u;
   // units past the last re-read it (finite weights, times zero activations).
   auto issue_w = [&](int c, int st) {
@@ -353,7 +361,7 @@ __device__ __forceinline__ void wide_mainloop_staged(const GemmParams& p, int g,
     constexpr int kNF = KC * MT;
     constexpr int kLook = 4;
     auto frag_at = [&](int f) {
-      return s_a[bb * kBuf + (f % MT) * 2 + rd_blk][f / MT ? rd_slot1 : rd_slot0];
+      return s_a[bb * kBuf + (f % MT) * 2 + a_half][f / MT ? a_slot1 : a_slot0];
     };
     Frag<T> ring[kLook];
 #pragma unroll
@@ -454,7 +462,7 @@ template <int MT, int KC, int NTW, int EPI, bool W8>
 __global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, NTW>())))
 void gemm_wide_kernel(const GemmParams p, int chunks) {
   __shared__ bf16x8 s_a[2 * MT * KC][64];          // two chunks of activation fragments
-  __shared__ bf16x8 s_w[wide_staged(MT) ? kWideStages * kWideWaves * NTW * (W8 ? KC / 2 : KC) : 1][64];
+  __shared__ bf16x8 s_w[wide_staged(MT, W8) ? kWideStages * kWideWaves * NTW * (W8 ? KC / 2 : KC) : 1][64];
   // One norm group's output tile reuses the chunk buffers, dead after the
   // loop, and so do the row scales where they fit behind it.
   constexpr int kTile = kNormTiles * MT * 128;     // floats
@@ -465,7 +473,7 @@ void gemm_wide_kernel(const GemmParams p, int chunks) {
   constexpr int kWavesPerGroup = kWideWaves / kGroups;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   f32x4 acc[NTW][MT];
-  if constexpr (wide_staged(MT))
+  if constexpr (wide_staged(MT, W8))
     wide_mainloop_staged<MT, KC, NTW, W8>(p, blockIdx.x, 0, chunks, s_a, s_w, acc);
   else
     wide_mainloop<MT, KC, NTW, W8>(p, blockIdx.x, 0, chunks, s_a, acc);
@@ -496,14 +504,14 @@ template <int MT, int KC, int NTW, bool W8>
 __global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, NTW>())))
 void gemm_wide_split_kernel(const GemmParams p, int S, int chunks) {
   __shared__ bf16x8 s_a[2 * MT * KC][64];
-  __shared__ bf16x8 s_w[wide_staged(MT) ? kWideStages * kWideWaves * NTW * (W8 ? KC / 2 : KC) : 1][64];
+  __shared__ bf16x8 s_w[wide_staged(MT, W8) ? kWideStages * kWideWaves * NTW * (W8 ? KC / 2 : KC) : 1][64];
   const int G = (p.NT + kWideWaves * NTW - 1) / (kWideWaves * NTW);
   const int g = blockIdx.x % G, s = blockIdx.x / G;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c0 = static_cast<int>(static_cast<long>(s) * chunks / S);
   const int c1 = static_cast<int>(static_cast<long>(s + 1) * chunks / S);
   f32x4 acc[NTW][MT];
-  if constexpr (wide_staged(MT))
+  if constexpr (wide_staged(MT, W8))
     wide_mainloop_staged<MT, KC, NTW, W8>(p, g, c0, c1, s_a, s_w, acc);
   else
     wide_mainloop<MT, KC, NTW, W8>(p, g, c0, c1, s_a, acc);
@@ -548,13 +556,12 @@ __global__ __launch_bounds__(kWideWaves * 64) void gemm_wide_reduce_kernel(const
 // ---------------------------------------------------------------------------
 static const int kWideMT[] = {2, 3, 4, 5, 6, 8, 10, 12, 14, 16, 18, 20};
 
-// k-tiles per chunk: the two chunk buffers (2 MT KC KiB of LDS) leave room
-// for two to three work-groups per CU up to 10 M tiles (one above 12, where
-// registers allow one wave per SIMD) and hold a norm group's output tile
-// (4 MT KiB).
-// FP8 chunks hold whole k-tile pairs: 2 where bf16 takes 3.
-static constexpr int wide_kc(int MT) { return wide_staged(MT) ? 2 : MT <= 10 || MT == 14 ? 4 : 3; }
-static constexpr int wide_kc8(int MT) { return wide_kc(MT) == 3 ? 2 : wide_kc(MT); }
+// k-tiles per chunk, whole pairs (activation blocks, FP8 codes): the two
+// chunk buffers (2 MT KC KiB of LDS) leave room for two to three
+// work-groups per CU up to 12 M tiles (one from 14, where registers allow
+// one wave per SIMD; from 16 the staged loop also needs LDS for its weight
+// ring) and hold a norm group's output tile (4 MT KiB).
+static constexpr int wide_kc(int MT, bool w8) { return wide_staged(MT, w8) ? 2 : MT <= 10 ? 4 : 2; }
 
 WidePlan wide_plan(int NT, int KT, int M, bool w8) {
   WidePlan w{};
@@ -563,7 +570,7 @@ WidePlan wide_plan(int NT, int KT, int M, bool w8) {
   for (int v : kWideMT)
     if (v >= mt) { w.MT = v; break; }
   w.w8 = w8;
-  w.KC = w8 ? wide_kc8(w.MT) : wide_kc(w.MT);
+  w.KC = wide_kc(w.MT, w8);
   w.NTW = wide_ntw(w.MT);
   w.G = (NT + kWideWaves * w.NTW - 1) / (kWideWaves * w.NTW);
   w.chunks = (KT + w.KC - 1) / w.KC;
@@ -583,7 +590,7 @@ size_t wide_part_bytes(const WidePlan& w) {
 
 int wide_groups(int NT) { return (NT + kNormTiles - 1) / kNormTiles; }
 
-template <int MT, bool W8, int KC = W8 ? wide_kc8(MT) : wide_kc(MT), int NTW = wide_ntw(MT)>
+template <int MT, bool W8, int KC = wide_kc(MT, W8), int NTW = wide_ntw(MT)>
 static hipError_t wide_launch(const GemmParams& p, const WidePlan& w, hipStream_t st) {
   const dim3 block(kWideWaves * 64);
   if (w.NTW != NTW || w.KC != KC || w.w8 != W8) return hipErrorInvalidValue;

@@ -98,11 +98,11 @@ def test_small_bf16_large_batch(sps, B, K):
                   check_kv=False)
 
 
-@pytest.mark.parametrize("B,K", [(16, 8), (25, 4)])
+@pytest.mark.parametrize("B,K", [(16, 8), (25, 4), (4, 8), (12, 7), (11, 9)])
 def test_small_bf16_odd_depth_wide(sps, B, K):
     """Contraction depths of 5, 6 and 9 k-tiles (d_model 160, three 64-wide
-    heads, d_ff 288) at 144 and 125 rows (18 and 16 M tiles): two-k-tile
-    chunks of the wide GEMM whose last chunk holds a single k-tile."""
+    heads, d_ff 288) at 144, 125, 36, 96 and 110 rows (18, 16, 5, 12 and 14
+    M tiles): wide-GEMM chunks whose last k-tile pair is half past the end."""
     g = np.random.default_rng(B + 900)
     verify_parity(sps, SMALL.with_(d_model=160, d_ff=288, ffn="swiglu"), B, K,
                   [int(x) for x in g.integers(0, 150, B)], 90 + B, 2e-2, check_kv=False)

@@ -10,8 +10,8 @@
   oracle's own dequantised weights, q the softmax of the logits, the fused
   accept / resample outputs bit-exact against the oracle on the GPU's q; the
   appended keys and values within 2e-2. Cases: 5 rows (one M tile, the
-  single-tile kernel), 12 to 144 rows (the wide kernel, with and without
-  split-K), a 64-token prefill chunk, and full-width blocks of the 70B and 7B
+  single-tile kernel), 12 to 144 rows (the wide kernel, register and LDS
+  staged weights, with and without split-K), a 64-token prefill chunk, and full-width blocks of the 70B and 7B
   shapes in the benchmark's and the sweep's launch shapes;
 * end to end: with the draft equal to the target every draft is accepted,
   and greedy SpS emits the same tokens as greedy ArS.
@@ -110,9 +110,9 @@ def test_fp8_verify_ragged_wide(sps, ffn):
     verify_parity(sps, SMALL8.with_(ffn=ffn), 3, 3, [5, 100, 257], 62, 2e-2)
 
 
-@pytest.mark.parametrize("B,K", [(12, 8), (16, 8)])
+@pytest.mark.parametrize("B,K", [(12, 8), (16, 8), (16, 4), (7, 8)])
 def test_fp8_verify_large_batch(sps, B, K):
-    # 108 and 144 rows: 14 and 18 M tiles (4 and 2 n-tiles per wave)
+    # 108, 144, 80 and 63 rows: 14, 18, 10 and 8 M tiles (the staged loop)
     g = np.random.default_rng(B + 500)
     verify_parity(sps, SMALL8, B, K, [int(x) for x in g.integers(0, 200, B)], 70 + B, 2e-2, check_kv=False)
 
