@@ -74,10 +74,8 @@ __device__ __forceinline__ float epilogue_element(const GemmParams& p, int gm, i
       if (col < 8) {
         const int hh = (n % HD) / p.DH, pi = n % p.DH;
         const int f = (pi / 16) * 8 + col;
-        const double inv = exp2(-2.0 * f / p.DH * log2(static_cast<double>(p.rope_base)));
-        double sn, cs;
-        sincos(static_cast<double>(pos) * inv, &sn, &cs);
-        const float c = static_cast<float>(cs), s = static_cast<float>(sn);
+        const float2 cs = p.rope[static_cast<size_t>(gm) * (p.DH / 2) + f];   // cos, sin (embed_kernel)
+        const float c = cs.x, s = cs.y;
         const float y1 = v * c - v2 * s, y2 = v2 * c + v * s;
         const int half = p.DH / 2;
         if (n < HD) {

@@ -35,7 +35,8 @@ struct GemmParams {
   float* out; int ldo;
   void* act; int lda; size_t aplane;
   float* h; const float* gain; void* u; int ldu; size_t uplane; float* ss_out;
-  const int32_t* lengths; int pos_offset, Mps, H, DH; float rope_base; int T_cap;
+  const int32_t* lengths; int pos_offset, Mps, H, DH; int T_cap;
+  const float2* rope;  // (cos, sin) of the rotary angle of row gm, frequency f: rope[gm DH / 2 + f]
   void* q; void* kc; void* vc; int* err;
   float* part;             // split-K partials (wide GEMM)
   int epi;
@@ -73,8 +74,11 @@ hipError_t launch_fp8_decode(const void* codes, int n, float* out, hipStream_t s
 // Activations (x, attention output o, FFN hidden) are in the activation
 // format of common.h; `xplane` is the element distance of the lo plane.
 // h[m] = E[token]; u[m] = h[m] * gain; ss[m] = sum h[m]^2 (one group).
+// Also fills the rotary table of the step: rope[row DH / 2 + f] = (cos,
+// sin) of angle pos * base^(-2 f / DH), pos = lengths[b] + pos_offset + j.
 hipError_t launch_embed(int dtype, const int32_t* tokens, int tok_stride, int Mps, int M, const void* E,
                         int V, int d, const float* gain, float* h, void* u, size_t uplane, float* ss,
+                        const int32_t* lengths, int pos_offset, int DH, float rope_base, float2* rope,
                         int* err, hipStream_t st);
 hipError_t launch_attention(int dtype, const void* q, const void* kc, const void* vc,
                             const int32_t* lengths, int pos_offset, int B, int Mps, int H, int DH,

@@ -27,10 +27,24 @@ __global__ __launch_bounds__(kEmbedThreads) void embed_kernel(const int32_t* __r
                                                               int Mps, const T* __restrict__ E, int V, int d,
                                                               const float* __restrict__ gain, float* __restrict__ h,
                                                               T* __restrict__ u, size_t uplane,
-                                                              float* __restrict__ ss, int* err) {
+                                                              float* __restrict__ ss,
+                                                              const int32_t* __restrict__ lengths, int pos_offset,
+                                                              int DH, float rope_base, float2* __restrict__ rope,
+                                                              int* err) {
   __shared__ float red[16];
   const int row = blockIdx.x;
   const int b = row / Mps, j = row % Mps;
+  // Rotary table of this row (position lengths[b] + pos_offset + j), used by
+  // the QKV epilogue of every layer: the angle and its cosine and sine in
+  // double precision, rounded once to fp32.
+  if (static_cast<int>(threadIdx.x) < DH / 2) {
+    const int f = threadIdx.x;
+    const int pos = lengths[b] + pos_offset + j;
+    const double inv = exp2(-2.0 * f / DH * log2(static_cast<double>(rope_base)));
+    double sn, cs;
+    sincos(static_cast<double>(pos) * inv, &sn, &cs);
+    rope[static_cast<size_t>(row) * (DH / 2) + f] = make_float2(static_cast<float>(cs), static_cast<float>(sn));
+  }
   int tok = tokens[static_cast<size_t>(b) * tok_stride + j];
   const bool ok = tok >= 0 && tok < V;
   if (!ok) {
@@ -80,14 +94,18 @@ __global__ void kv_copy_kernel(int to_cache, T* __restrict__ kc, T* __restrict__
 }
 
 hipError_t launch_embed(int dtype, const int32_t* tokens, int tok_stride, int Mps, int M, const void* E, int V,
-                        int d, const float* gain, float* h, void* u, size_t uplane, float* ss, int* err,
+                        int d, const float* gain, float* h, void* u, size_t uplane, float* ss,
+                        const int32_t* lengths, int pos_offset, int DH, float rope_base, float2* rope, int* err,
                         hipStream_t st) {
+  if (DH / 2 > kEmbedThreads) return hipErrorInvalidValue;
   if (dtype == 1)
     hipLaunchKernelGGL(embed_kernel<bf16>, dim3(M), dim3(kEmbedThreads), 0, st, tokens, tok_stride, Mps,
-                       static_cast<const bf16*>(E), V, d, gain, h, static_cast<bf16*>(u), uplane, ss, err);
+                       static_cast<const bf16*>(E), V, d, gain, h, static_cast<bf16*>(u), uplane, ss, lengths,
+                       pos_offset, DH, rope_base, rope, err);
   else
     hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(kEmbedThreads), 0, st, tokens, tok_stride, Mps,
-                       static_cast<const float*>(E), V, d, gain, h, static_cast<float*>(u), uplane, ss, err);
+                       static_cast<const float*>(E), V, d, gain, h, static_cast<float*>(u), uplane, ss, lengths,
+                       pos_offset, DH, rope_base, rope, err);
   return hipGetLastError();
 }
 

@@ -92,7 +92,7 @@ Layout make_layout(const sps_config* c) {
 
 // Offsets of the forward's scratch buffers.
 struct WsLayout {
-  size_t h, x, o, q, apart, act, ss_a, ss_b, logits, stats, gpart, total;
+  size_t h, x, o, q, rope, apart, act, ss_a, ss_b, logits, stats, gpart, total;
 };
 
 // The GEMMs of one forward as (n-tiles, k-tiles).
@@ -128,6 +128,7 @@ WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
   w.x = o; o = align256(o + M * L.d * 4);                 // u = h * gain (activation format)
   w.o = o; o = align256(o + M * L.HD * 4);                // attention output (activation format)
   w.q = o; o = align256(o + M * L.HD * L.es);             // rotated queries (model dtype)
+  w.rope = o; o = align256(o + M * (L.DH / 2) * 8);       // rotary (cos, sin) per row and frequency
   w.apart = o; o = align256(o + static_cast<size_t>(B) * L.H * NP * Mps * (L.DH + 2) * 4);
   w.act = o; o = align256(o + M * L.F * 4);               // FFN hidden (activation format)
   w.ss_a = o; o = align256(o + ng * M * 4);               // per-group sums of squares of h
@@ -274,9 +275,10 @@ sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t*
   base.eps = m->cfg.rms_eps;
   base.part = reinterpret_cast<float*>(ws_base + ws.gpart);
 
+  float2* rope = reinterpret_cast<float2*>(ws_base + ws.rope);
   SPS_HIP(sps::launch_embed(adt, tokens, tok_stride, Mps, M, m->base + L.embed, L.V, L.d,
                             reinterpret_cast<const float*>(layer_ptr(m, 0, L.l_attn_norm)), h, x, uplane, ss_cur,
-                            err, st));
+                            kv->lengths, pos_offset, L.DH, m->cfg.rope_base, rope, err, st));
   int ng = 1;
   for (int l = 0; l < L.L; ++l) {
     GemmParams p = base;                     // QKV: norm scale, rotary encoding, KV append
@@ -285,7 +287,8 @@ sps_status forward_impl(const sps_model_s* m, const sps_kv_s* kv, const int32_t*
     p.wscale = scale_ptr(m, l, L.l_qkv_sc);
     p.ss_in = ss_cur; p.ng_in = ng;
     p.lengths = kv->lengths; p.pos_offset = pos_offset; p.Mps = Mps; p.H = L.H; p.DH = L.DH;
-    p.rope_base = m->cfg.rope_base; p.T_cap = kv->T_cap; p.q = q; p.kc = kv_k(kv, l); p.vc = kv_v(kv, l);
+    p.T_cap = kv->T_cap; p.q = q; p.kc = kv_k(kv, l); p.vc = kv_v(kv, l);
+    p.rope = rope;
     p.err = err; p.epi = sps::kEpiQkv;
     sps_status s = gemm(dt, p, st);
     if (s != SPS_OK) return s;
