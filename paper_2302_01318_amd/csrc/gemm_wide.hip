@@ -39,6 +39,8 @@
 namespace sps {
 
 constexpr int kWideWaves = 4;                      // waves per work-group
+constexpr int kCUs = 256;                          // compute units of the GPU (MI355X)
+constexpr long kLdsBytes = 160 * 1024;             // LDS per CU
 constexpr int kNormTiles = 8;                      // n-tiles per norm group (128 columns)
 
 // n-tiles per wave. (With register-held weights, 4 at 14 M tiles ran the
@@ -64,9 +66,8 @@ template <int MT, int NTW> constexpr int wide_part_floats() { return NTW * MT * 
 
 // Waves per SIMD the register allocation must allow (the compiler would
 // otherwise hoist every LDS fragment read of a chunk into registers).
-template <int MT, int NTW> constexpr int wide_waves_per_simd() {
-  return MT > 12 ? 1 : MT <= 6 ? 3 : 2;
-}
+static constexpr int waves_per_simd(int MT) { return MT > 12 ? 1 : MT <= 6 ? 3 : 2; }
+template <int MT, int NTW> constexpr int wide_waves_per_simd() { return waves_per_simd(MT); }
 
 // Weight registers of one chunk: bf16 fragments, or the raw FP8 code loads
 // (one per k-tile pair) that become fragments right before their MFMAs.
@@ -574,13 +575,26 @@ WidePlan wide_plan(int NT, int KT, int M, bool w8) {
   w.NTW = wide_ntw(w.MT);
   w.G = (NT + kWideWaves * w.NTW - 1) / (kWideWaves * w.NTW);
   w.chunks = (KT + w.KC - 1) / w.KC;
-  // Split until the launch holds about two work-groups per CU (one above
-  // 12 M tiles, where registers allow one wave per SIMD).
-  const int target = w.MT <= 12 ? 512 : 256;
-  int S = (target + w.G - 1) / w.G;
-  S = std::min(S, 16);
-  S = std::min(S, std::max(1, w.chunks / 2));
-  w.S = std::max(S, 1);
+  // Split count: the work-groups a CU holds at once (LDS of the split
+  // kernel, waves per SIMD the registers allow) give the launch's slots; a
+  // launch of G S work-groups runs in ceil(G S / slots) rounds of ~chunks / S
+  // chunks plus a fixed cost per work-group (~8 chunks). Minimising that over
+  // the measured split counts picks full last rounds: 4 splits for 192
+  // column groups at one work-group per CU (768 = 3 x 256; 2 splits leave a
+  // half-empty second round, 16 % slower), 2 for 250 at two per CU.
+  const bool staged = wide_staged(w.MT, w8);
+  const long lds = 2L * w.MT * w.KC * 1024 +
+                   (staged ? static_cast<long>(kWideStages) * kWideWaves * w.NTW * (w8 ? w.KC / 2 : w.KC) * 1024 : 0);
+  const int occ = std::max(1, std::min(static_cast<int>(kLdsBytes / lds), waves_per_simd(w.MT)));
+  const long slots = static_cast<long>(kCUs) * occ;
+  long best = -1;
+  w.S = 1;
+  for (int S : {1, 2, 3, 4, 6, 8}) {
+    if (S > 1 && S > w.chunks / 2) break;
+    const long rounds = (static_cast<long>(w.G) * S + slots - 1) / slots;
+    const long cost = rounds * ((w.chunks + S - 1) / S + 8);
+    if (best < 0 || cost < best) { best = cost; w.S = S; }
+  }
   return w;
 }
 
