@@ -525,9 +525,9 @@ def main():
         prompt = torch.randint(0, shape.vocab, (B, ctx), generator=gen, device="cuda", dtype=torch.int32)
         Tc = round_up(ctx + args.n_new + 2 * (K + 1), 32)
 
-        def pair_run(tgt, dm, label):
+        def pair_run(tgt, dm, label, ars=True):
             out = {}
-            for name, d_, k in (("sps", dm, K), ("ars", None, 0)):
+            for name, d_, k in (("sps", dm, K), ("ars", None, 0))[:2 if ars else 1]:
                 g = sps.Generator(tgt, d_, B, Tc, k)
                 g.prefill(prompt)
                 torch.cuda.synchronize()
@@ -559,6 +559,15 @@ def main():
         e2e["coupled"] = pair_run(target, draft, "coupled pair")
         del draft
         torch.cuda.empty_cache()
+        if dshape.dtype != "fp8":
+            # The same coupled pair with the draft's projections in weight-only
+            # FP8: half the draft's bytes per token. The accepted tokens still
+            # follow the bf16 target exactly (any draft does); only the
+            # acceptance rate and the draft time change.
+            draft = coupled(dshape.with_(dtype="fp8"), args.seed + 2, E2E_CODE_PERT)
+            e2e["coupled_fp8_draft"] = pair_run(target, draft, "coupled pair, fp8 draft", ars=False)
+            del draft
+            torch.cuda.empty_cache()
 
     result = {
         "metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
@@ -590,6 +599,13 @@ def main():
                          "sps_mean_accepted": round(c["sps"]["mean_accepted"], 3),
                          "sps_loops": c["sps"]["loops"], "ars_loops": c["ars"]["loops"],
                          "speedup_vs_ars": round(c["sps"]["tokens_per_s"] / c["ars"]["tokens_per_s"], 3),
+                         "fp8_draft": None if "coupled_fp8_draft" not in e2e else {
+                             "sps_tokens_per_s": round(e2e["coupled_fp8_draft"]["sps"]["tokens_per_s"], 2),
+                             "sps_mean_accepted": round(e2e["coupled_fp8_draft"]["sps"]["mean_accepted"], 3),
+                             "sps_loops": e2e["coupled_fp8_draft"]["sps"]["loops"],
+                             "speedup_vs_ars": round(e2e["coupled_fp8_draft"]["sps"]["tokens_per_s"]
+                                                     / c["ars"]["tokens_per_s"], 3),
+                             "note": "same coupled pair, draft projections in weight-only FP8 (target bf16)"},
                          "unrelated_pair": {"sps_tokens_per_s": round(u["sps"]["tokens_per_s"], 2),
                                             "ars_tokens_per_s": round(u["ars"]["tokens_per_s"], 2),
                                             "sps_mean_accepted": round(u["sps"]["mean_accepted"], 3)},

@@ -169,3 +169,29 @@ def test_fp8_e2e_properties(sps):
     g0 = sps.Generator(gm, None, 2, 128, 0).generate(prompt, 32, 0.0, 1)
     torch.cuda.synchronize()
     assert torch.equal(g1, g0)
+
+
+def test_bf16_target_fp8_draft(sps):
+    """A bf16 target drafted by its own weights in weight-only FP8 (the pair
+    the end-to-end benchmark also runs): greedy SpS emits exactly the
+    target's greedy ArS tokens, since every emitted token is the target's
+    argmax whatever the draft proposes; at T = 1 the quantised draft is
+    accepted most of the time."""
+    shape = SMALL8.with_(n_layers=2, dtype="bf16")
+    w = synth.weights(shape, 71)
+    gt = sps.Model(shape, w)
+    gd = sps.Model(shape.with_(dtype="fp8"), w)
+    del w
+    prompt = torch.from_numpy(synth.tokens(72, 2, 16, shape.vocab)).cuda()
+    print("bf16 target, fp8 draft", flush=True)
+    g1 = sps.Generator(gt, gd, 2, 128, 4).generate(prompt, 32, 0.0, 1)
+    g0 = sps.Generator(gt, None, 2, 128, 0).generate(prompt, 32, 0.0, 1)
+    torch.cuda.synchronize()
+    assert sps.device_error() == 0
+    assert torch.equal(g1, g0)
+    log = []
+    sps.Generator(gt, gd, 2, 128, 4).generate(prompt, 40, 1.0, 5, accepted_log=log)
+    torch.cuda.synchronize()
+    assert sps.device_error() == 0
+    flat = [int(a[b]) for a, done in log for b in range(2) if not bool(done[b])]
+    assert sum(flat) >= 0.8 * 4 * len(flat)
