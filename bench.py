@@ -20,7 +20,7 @@ about as often as the paper's trained drafts (and on an unrelated random
 pair beside it), and the CPU oracle timed on a bounded sample.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--K 4] [--B 1] [--ctx 2048]
-    python bench.py --sweep | --accept-grid | --k-study
+    python bench.py --sweep | --accept-grid | --k-study | --draft-step
 """
 import argparse
 import json
@@ -293,6 +293,44 @@ def sweep(args):
                     "the GPU accept kernel measures on synthetic pairs (z_q ~ N(0,4), z_p = z_q + N(0, sigma^2))"}
 
 
+def draft_step_bench(args):
+    """The draft side of one SpS loop: sps_draft_step (K draft tokens, each a
+    forward of the 3072-wide, 24-layer draft over its pending tokens plus the
+    softmax and draw) for B sequences at KV context ctx, with bf16 and with
+    weight-only FP8 projections. Algorithmic bytes per draft token: the
+    draft's weights once plus the KV cache it reads (verify_bytes with no
+    lookahead); the first forward of a step runs two pending tokens. The
+    draft's weights follow --weights."""
+    import torch
+    from paper_2302_01318_amd import configs, sps, synth
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+    B, K, ctx = args.B, args.K, args.ctx
+    rows = []
+    for w in (args.weights,):
+        dshape = configs.DRAFT_70B if w == "bf16" else configs.DRAFT_70B.with_(dtype="fp8")
+        draft = device_model(sps, synth, dshape, args.seed + 10)
+        T_cap = round_up(ctx + K + 2, 32)
+        kv = sps.KVCache(dshape, B, T_cap)
+        kv.buf.view(torch.bfloat16).normal_()
+        kv.lengths.fill_(ctx)
+        ws = sps.workspace(dshape, B, 2, T_cap)
+        pending = torch.randint(0, dshape.vocab, (B, 2), device="cuda", dtype=torch.int32)
+        toks = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+        pbuf = torch.empty((B, K, dshape.vocab), device="cuda")
+        ms = timed(lambda i: sps.draft_step(draft, kv, pending, K, 1.0, (args.seed, i), toks, pbuf, ws),
+                   args.steps, args.warmup)
+        assert sps.device_error() == 0
+        nbytes = verify_bytes(dshape, B, 0, ctx)
+        gbs = nbytes / (ms / K * 1e-3) / 1e9
+        rows.append({"weights": w, "ms_per_step": round(ms, 4), "ms_per_token": round(ms / K, 4),
+                     "bytes_per_token": nbytes, "gbs": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)})
+        log("draft %s: %.3f ms per step of %d tokens, %.3f ms per token, %.0f GB/s" % (w, ms, K, ms / K, gbs))
+        del draft, kv, ws
+        torch.cuda.empty_cache()
+    return {"metric": "draft step ms per draft token", "draft": configs.DRAFT_70B.name, "B": B, "K": K,
+            "ctx": ctx, "steps": args.steps, "warmup": args.warmup, "rows": rows}
+
+
 def k_study(args):
     """Time to generate n_new tokens with SpS against K (a Figure 1
     analogue): the 70B target and the 3072-wide draft built as a coupled
@@ -416,6 +454,8 @@ def main():
     ap.add_argument("--top-p", type=float, default=1.0, help="nucleus modifier of p and q (1: off)")
     ap.add_argument("--sweep", action="store_true", help="70B verify over K, B, ctx (+ accept-stage projection)")
     ap.add_argument("--accept-grid", action="store_true", help="accept/resample alone over the B x K grid")
+    ap.add_argument("--draft-step", action="store_true",
+                    help="the draft side alone: K draft tokens per step (draft weights per --weights)")
     ap.add_argument("--k-study", action="store_true",
                     help="SpS generation time vs K on a coupled 70B / draft pair (acceptance set by the draft's "
                          "logit perturbation)")
@@ -431,8 +471,9 @@ def main():
               "(requested --gpus %d)" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
-    if args.sweep or args.accept_grid or args.k_study:
-        res = sweep(args) if args.sweep else accept_grid(args) if args.accept_grid else k_study(args)
+    if args.sweep or args.accept_grid or args.k_study or args.draft_step:
+        res = (sweep(args) if args.sweep else accept_grid(args) if args.accept_grid else
+               draft_step_bench(args) if args.draft_step else k_study(args))
         print(json.dumps(res), flush=True)
         return
 
