@@ -20,7 +20,7 @@ about as often as the paper's trained drafts (and on an unrelated random
 pair beside it), and the CPU oracle timed on a bounded sample.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--K 4] [--B 1] [--ctx 2048]
-    python bench.py --sweep | --accept-grid | --k-study | --draft-step
+    python bench.py --sweep | --accept-grid | --k-study | --draft-step | --cpu-oracle
 """
 import argparse
 import json
@@ -152,21 +152,10 @@ def cpu_baseline(shape, K, ctx):
     positions of one sequence against a random ctx-token cache."""
     import numpy as np
     from oracle import model as om
-    from oracle.model import ModelSpec
     from paper_2302_01318_amd import synth
     one = shape.with_(n_layers=1)
-    spec = ModelSpec(one.d_model, 1, one.n_heads, one.head_dim, one.d_ff, one.vocab, one.ffn,
-                     "bf16" if one.dtype == "fp8" else one.dtype, one.eps, one.rope_base)
-    f = lambda t: t.float().numpy()
-    w = {k: synth.weight(one, k[0], k[1], 0) for k in synth.tensor_shapes(one)}
-    W = {"embed": f(w[("embed", -1)]), "final_norm": f(w[("final_norm", -1)]), "unembed": f(w[("unembed", -1)]),
-         "layers": [{"attn_norm": f(w[("attn_norm", 0)]), "wq": f(w[("wq", 0)]), "wk": f(w[("wk", 0)]),
-                     "wv": f(w[("wv", 0)]), "wo": f(w[("wo", 0)]), "ffn_norm": f(w[("ffn_norm", 0)]),
-                     "w1": f(w[("w1", 0)]), "w2": f(w[("w2", 0)])}]}
-    del w
-    if one.dtype == "fp8":                   # the oracle's own quantisation, outside the timed region
-        from oracle import fp8
-        W = fp8.fp8_weights(W)
+    spec = _oracle_spec(one)
+    W = _oracle_weights(shape, 1, 0)          # FP8: the oracle's own quantisation, outside the timed region
     cache = om.new_cache(spec, 1, ctx + K + 1)
     k, v = synth.kv_prior(one, 1, 0, 1, ctx)
     cache["k"][0, 0, :, :ctx] = k[0].double().numpy()
@@ -189,6 +178,108 @@ def cpu_baseline(shape, K, ctx):
             "seconds_per_sample": dt, "repeats": reps,
             "sample": "oracle fp64 forward of one full-width 70B-shaped block + embedding + unembedding, "
                       "K+1=%d positions, B=1, ctx %d (%.2f GB algorithmic)" % (K + 1, ctx, nbytes / 1e9)}
+
+
+def _oracle_weights(shape, n_layers, seed):
+    """The oracle's weight dict (fp32 numpy) of the first n_layers layers of
+    the synthetic model `shape` with weight seed `seed` (FP8 models: the
+    oracle's own quantisation)."""
+    f = lambda t: t.float().numpy()
+    from paper_2302_01318_amd import synth
+    one = shape.with_(n_layers=n_layers)
+    w = {k: synth.weight(one, k[0], k[1], seed) for k in synth.tensor_shapes(one)}
+    W = {"embed": f(w[("embed", -1)]), "final_norm": f(w[("final_norm", -1)]), "unembed": f(w[("unembed", -1)]),
+         "layers": []}
+    for l in range(n_layers):
+        lw = {k: f(w[(k, l)]) for k in ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm")}
+        if shape.ffn == "gelu":
+            lw.update(w1=f(w[("w1", l)]), w2=f(w[("w2", l)]))
+        else:
+            lw.update(wg=f(w[("w1", l)]), wu=f(w[("w3", l)]), wd=f(w[("w2", l)]))
+        W["layers"].append(lw)
+    del w
+    if shape.dtype == "fp8":
+        from oracle import fp8
+        W = fp8.fp8_weights(W)
+    return W
+
+
+def _oracle_spec(shape, n_layers=None):
+    from oracle.model import ModelSpec
+    return ModelSpec(shape.d_model, shape.n_layers if n_layers is None else n_layers, shape.n_heads, shape.head_dim,
+                     shape.d_ff, shape.vocab, shape.ffn, "bf16" if shape.dtype == "fp8" else shape.dtype, shape.eps,
+                     shape.rope_base)
+
+
+def cpu_oracle(args):
+    """The oracle's cost on the host's CPUs (numpy as it stands, BLAS threads
+    as the host gives them), on bounded samples: the tiny fp32 pair's SpS
+    and ArS generations end to end (prompt 32, 64 new tokens, K = 4, T = 1),
+    and the verify step (K = 4, B = 1, ctx 2048) of the 7B and 70B shapes,
+    timed on 1- and 2-layer models and extrapolated to all layers (the full
+    fp32 models do not fit the host: 27 and 260 GB). Reported baselines,
+    not targets."""
+    import numpy as np
+    from oracle import generate as ogen
+    from oracle import model as om
+    from paper_2302_01318_amd import configs, synth
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+    host = {"cpu_count": os.cpu_count(), "affinity_cores": len(os.sched_getaffinity(0))}
+    try:
+        host["ram_gb"] = round(os.sysconf("SC_PAGE_SIZE") * os.sysconf("SC_PHYS_PAGES") / 1e9, 1)
+    except (ValueError, OSError):
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        host["blas"] = [{k: i.get(k) for k in ("internal_api", "num_threads")} for i in threadpool_info()]
+    except Exception:
+        pass
+    out = {"metric": "oracle CPU time", "host": host}
+    # tiny pair end to end
+    tgt, drf = configs.TINY_TARGET, configs.TINY_DRAFT
+    Wt, Wd = _oracle_weights(tgt, tgt.n_layers, 100), _oracle_weights(drf, drf.n_layers, 101)
+    prompt = synth.tokens(102, 1, 32, tgt.vocab)[0]
+    t0 = time.perf_counter()
+    toks, acc = ogen.sps_generate_one(_oracle_spec(tgt), Wt, _oracle_spec(drf), Wd, prompt, 64, 4, 1.0, 7)
+    t_sps = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    ogen.ars_generate_one(_oracle_spec(tgt), Wt, prompt, 64, 1.0, 7)
+    t_ars = time.perf_counter() - t0
+    out["tiny_e2e"] = {"sps_tokens_per_s": round(64 / t_sps, 2), "ars_tokens_per_s": round(64 / t_ars, 2),
+                       "sps_seconds": round(t_sps, 3), "ars_seconds": round(t_ars, 3),
+                       "sps_mean_accepted": round(float(np.mean(acc)), 3),
+                       "note": "oracle generation recomputes the full prefix for every forward"}
+    log("tiny e2e: sps %.2f tokens/s, ars %.2f tokens/s" % (64 / t_sps, 64 / t_ars))
+    # verify step of the 7B and 70B shapes, from 1- and 2-layer models
+    K, ctx = 4, 2048
+    for shape in (configs.SEVEN_B, configs.SEVENTY_B):
+        t = {}
+        for n in (1, 2):
+            W = _oracle_weights(shape, n, 0)
+            spec = _oracle_spec(shape, n)
+            cache = om.new_cache(spec, 1, ctx + K + 1)
+            for l in range(n):
+                k, v = synth.kv_prior(shape.with_(n_layers=n), 1, l, 1, ctx)
+                cache["k"][l, 0, :, :ctx] = k[0].double().numpy()
+                cache["v"][l, 0, :, :ctx] = v[0].double().numpy()
+            toks = synth.tokens(2, 1, K + 1, shape.vocab)
+            reps, t0 = 0, time.perf_counter()
+            while reps < 2 or time.perf_counter() - t0 < CPU_BASELINE_SECONDS / 2:
+                om.forward_cached(spec, W, cache, toks, np.array([ctx]))
+                reps += 1
+            t[n] = (time.perf_counter() - t0) / reps
+            del W, cache
+        per_layer = t[2] - t[1]
+        total = t[1] + (shape.n_layers - 1) * per_layer
+        nbytes = verify_bytes(shape, 1, K, ctx)
+        out["verify_" + shape.name] = {"seconds_1_layer": round(t[1], 3), "seconds_2_layers": round(t[2], 3),
+                                       "seconds_per_layer": round(per_layer, 3),
+                                       "seconds_extrapolated": round(total, 2),
+                                       "gbs_extrapolated": round(nbytes / total / 1e9, 3),
+                                       "note": "extrapolated: 1-layer time + (L - 1) x per-layer time"}
+        log("%s verify: %.3f s per layer, %.1f s extrapolated (%.3f GB/s)" % (shape.name, per_layer, total,
+                                                                          nbytes / total / 1e9))
+    return out
 
 
 def cpu_baseline_accept(inputs, B, K, seed):
@@ -454,6 +545,8 @@ def main():
     ap.add_argument("--top-p", type=float, default=1.0, help="nucleus modifier of p and q (1: off)")
     ap.add_argument("--sweep", action="store_true", help="70B verify over K, B, ctx (+ accept-stage projection)")
     ap.add_argument("--accept-grid", action="store_true", help="accept/resample alone over the B x K grid")
+    ap.add_argument("--cpu-oracle", action="store_true",
+                    help="the oracle's CPU time: tiny pair end to end, 7B and 70B verify (extrapolated)")
     ap.add_argument("--draft-step", action="store_true",
                     help="the draft side alone: K draft tokens per step (draft weights per --weights)")
     ap.add_argument("--k-study", action="store_true",
@@ -471,6 +564,9 @@ def main():
               "(requested --gpus %d)" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
+    if args.cpu_oracle:
+        print(json.dumps(cpu_oracle(args)), flush=True)
+        return
     if args.sweep or args.accept_grid or args.k_study or args.draft_step:
         res = (sweep(args) if args.sweep else accept_grid(args) if args.accept_grid else
                draft_step_bench(args) if args.draft_step else k_study(args))
