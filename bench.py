@@ -148,8 +148,9 @@ def coupled_model(sps, synth, shape, model_seed, code_pert, st):
 
 def cpu_baseline(shape, K, ctx):
     """The oracle (fp64 numpy, as it stands) on a bounded sample: one
-    full-width block of the 70B shape plus embedding and unembedding, K+1
-    positions of one sequence against a random ctx-token cache."""
+    full-width block of the benchmarked shape plus embedding and
+    unembedding, K+1 positions of one sequence against a random ctx-token
+    cache."""
     import numpy as np
     from oracle import model as om
     from paper_2302_01318_amd import synth
@@ -176,8 +177,8 @@ def cpu_baseline(shape, K, ctx):
         threads = len(os.sched_getaffinity(0))
     return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
             "seconds_per_sample": dt, "repeats": reps,
-            "sample": "oracle fp64 forward of one full-width 70B-shaped block + embedding + unembedding, "
-                      "K+1=%d positions, B=1, ctx %d (%.2f GB algorithmic)" % (K + 1, ctx, nbytes / 1e9)}
+            "sample": "oracle fp64 forward of one full-width %s-shaped block + embedding + unembedding, "
+                      "K+1=%d positions, B=1, ctx %d (%.2f GB algorithmic)" % (shape.name, K + 1, ctx, nbytes / 1e9)}
 
 
 def _oracle_weights(shape, n_layers, seed):
