@@ -38,7 +38,7 @@ typedef enum {
   SPS_E_INVALID = 1,      /* null pointer, negative size, bad enum value      */
   SPS_E_SHAPE = 2,        /* shape the kernels do not support (see sps_config) */
   SPS_E_CAPACITY = 3,     /* workspace / KV buffer too small                   */
-  SPS_E_UNSUPPORTED = 4,  /* valid request this build does not implement      */
+  SPS_E_UNSUPPORTED = 4,  /* valid request the library does not implement     */
   SPS_E_HIP = 5           /* a HIP runtime call or kernel launch failed       */
 } sps_status;
 

@@ -9,7 +9,7 @@ paragraph; Table 1 and its caption: nucleus 0.8 on XSum, 0.95 with
 temperature 0.8 on HumanEval). Theorem 1 then holds for the modified
 distributions: the draft must be sampled from exactly the modified p that
 acceptance uses, and the output follows the modified q. The paper gives no
-formula for the modifiers; this build reads them as follows (both the GPU
+formula for the modifiers; they are read here as follows (both the GPU
 path and this oracle):
 
 * order: temperature first (the softmax), then top-k, then nucleus on what
