@@ -409,8 +409,8 @@ def draft_step_bench(args):
         pending = torch.randint(0, dshape.vocab, (B, 2), device="cuda", dtype=torch.int32)
         toks = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
         pbuf = torch.empty((B, K, dshape.vocab), device="cuda")
-        ms = timed(lambda i: sps.draft_step(draft, kv, pending, K, 1.0, (args.seed, i), toks, pbuf, ws),
-                   args.steps, args.warmup)
+        ms = timed(lambda i: sps.draft_step(draft, kv, pending, K, args.temperature, (args.seed, i), toks, pbuf, ws,
+                                            top_k=args.top_k, top_p=args.top_p), args.steps, args.warmup)
         assert sps.device_error() == 0
         nbytes = verify_bytes(dshape, B, 0, ctx)
         gbs = nbytes / (ms / K * 1e-3) / 1e9
@@ -420,7 +420,8 @@ def draft_step_bench(args):
         del draft, kv, ws
         torch.cuda.empty_cache()
     return {"metric": "draft step ms per draft token", "draft": configs.DRAFT_70B.name, "B": B, "K": K,
-            "ctx": ctx, "steps": args.steps, "warmup": args.warmup, "rows": rows}
+            "ctx": ctx, "temperature": args.temperature, "top_k": args.top_k, "top_p": args.top_p,
+            "steps": args.steps, "warmup": args.warmup, "rows": rows}
 
 
 def k_study(args):
