@@ -120,11 +120,13 @@ def verify_bytes(shape, B, K, ctx):
 
 def model_shapes(configs, args):
     """Target (70B or 7B shape) and draft shapes, with FP8 projections when
-    --weights fp8."""
+    --weights fp8 (both models) or --draft-weights fp8 (the draft only)."""
     shape = configs.SEVENTY_B if args.shape == "70b" else configs.SEVEN_B
     dshape = configs.DRAFT_70B
     if args.weights == "fp8":
         shape, dshape = shape.with_(dtype="fp8"), dshape.with_(dtype="fp8")
+    if getattr(args, "draft_weights", None) == "fp8":
+        dshape = dshape.with_(dtype="fp8")
     return shape, dshape
 
 
@@ -490,7 +492,7 @@ def k_study(args):
         del draft
         torch.cuda.empty_cache()
     return {"k_study": rows, "ars": ars, "layer_std": st["layer_std"], "prompt": plen,
-            "n_new": n_new, "temperature": 1.0,
+            "n_new": n_new, "temperature": 1.0, "target_weights": shape.dtype, "draft_weights": dshape.dtype,
             "note": "coupled synthetic pair: shared rank-%d bigram skip path, target logit spread %.1f, draft logits "
                     "= target logits + N(0, code_pert^2); times are wall-clock per generation of n_new tokens after "
                     "prefill" % (st["rank"], st["logit_std"])}
@@ -539,6 +541,8 @@ def main():
     ap.add_argument("--shape", default="70b", choices=["70b", "7b"])
     ap.add_argument("--weights", default="bf16", choices=["bf16", "fp8"],
                     help="projection weights of target and draft: bf16, or weight-only FP8 (E4M3)")
+    ap.add_argument("--draft-weights", default=None, choices=["bf16", "fp8"],
+                    help="the draft's projections (default: as --weights); for --k-study")
     ap.add_argument("--no-e2e", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
