@@ -460,7 +460,8 @@ def k_study(args):
             torch.cuda.synchronize()
             acc_log = []
             t0 = time.perf_counter()
-            g.run(n_new, 1.0, args.seed + 1000 * r + K, accepted_log=acc_log)
+            g.run(n_new, args.temperature, args.seed + 1000 * r + K, accepted_log=acc_log, top_k=args.top_k,
+                  top_p=args.top_p)
             torch.cuda.synchronize()
             times.append(time.perf_counter() - t0)
             loops += g.loops
@@ -492,7 +493,8 @@ def k_study(args):
         del draft
         torch.cuda.empty_cache()
     return {"k_study": rows, "ars": ars, "layer_std": st["layer_std"], "prompt": plen,
-            "n_new": n_new, "temperature": 1.0, "target_weights": shape.dtype, "draft_weights": dshape.dtype,
+            "n_new": n_new, "temperature": args.temperature, "top_k": args.top_k, "top_p": args.top_p,
+            "target_weights": shape.dtype, "draft_weights": dshape.dtype,
             "note": "coupled synthetic pair: shared rank-%d bigram skip path, target logit spread %.1f, draft logits "
                     "= target logits + N(0, code_pert^2); times are wall-clock per generation of n_new tokens after "
                     "prefill" % (st["rank"], st["logit_std"])}
