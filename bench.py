@@ -659,6 +659,7 @@ def main():
                     "bytes_per_launch": g_bytes / g_n,
                     "frac_of_stream_read": round(g_gbs / read_gbs, 4), "mfma": measured_mfma(args.weights)}
     del kv, ws
+    torch.cuda.empty_cache()     # the end-to-end caches differ in size from the timing cache
 
     # ---- SpS and ArS tokens/s end to end ---------------------------------------------
     # Two pairs: the coupled pair (draft logits = target logits + N(0, 0.5^2),
