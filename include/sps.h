@@ -17,8 +17,9 @@
  *    failures leave device memory untouched.
  *  - Errors that only the device can see (a token id outside [0, V), a KV
  *    position at or beyond the cache capacity, a distribution whose weights
- *    are all zero) set a sticky per-device flag read by sps_device_error.
- *    The kernels then write defined outputs and make no out-of-bounds access.
+ *    are all zero, a NaN or infinite logit or probability) set a sticky
+ *    per-device flag read by sps_device_error. The kernels then write
+ *    defined outputs and make no out-of-bounds access.
  *  - Handles (sps_model_t, sps_kv_t) are small host objects holding a
  *    configuration and non-owning device pointers. They are not thread safe.
  *  - Calls that share a workspace or a KV cache must not run concurrently.
@@ -46,6 +47,16 @@ typedef enum {
 #define SPS_DEV_BAD_TOKEN 1  /* token id outside [0, V)                        */
 #define SPS_DEV_EMPTY 2      /* categorical draw with all weights zero         */
 #define SPS_DEV_CAPACITY 4   /* KV write at a position >= T_cap (write skipped) */
+/* A row of logits with a NaN or +Inf entry (or one that overflows to +Inf
+ * when divided by the temperature) has no distribution: its probabilities
+ * are defined as one-hot at token 0 (exported q / p rows, draft draws). In
+ * modified rejection sampling a sequence with such a target row, or with a
+ * NaN or infinite value among the probabilities the accept tests and the
+ * final draw read, is given a = 0 accepted drafts and token 0. -Inf logits
+ * are valid (probability 0). The paper's method assumes valid distributions
+ * (Modified Rejection Sampling section); this is the library's definition
+ * for inputs that are not. */
+#define SPS_DEV_NONFINITE 8
 
 enum { SPS_FFN_GELU = 0, SPS_FFN_SWIGLU = 1 };
 enum { SPS_DTYPE_F32 = 0, SPS_DTYPE_BF16 = 1, SPS_DTYPE_FP8 = 2 };
@@ -55,7 +66,8 @@ enum { SPS_DTYPE_F32 = 0, SPS_DTYPE_BF16 = 1, SPS_DTYPE_FP8 = 2 };
  * with rotate-half rotary position encoding, FFN = GELU(tanh) with two
  * matrices or SwiGLU with three, untied embedding / unembedding, no biases.
  * Supported: d_model % 32 == 0, d_model <= 16384, head_dim in {64, 128},
- * (n_heads * head_dim) % 32 == 0, d_ff % 32 == 0, 2 <= vocab < 2^24.
+ * (n_heads * head_dim) % 32 == 0, d_ff % 32 == 0, 2 <= vocab < 2^24,
+ * 1 <= n_layers <= 4096, 1 <= n_heads <= 1024, d_ff <= 2^20.
  *
  * dtype SPS_DTYPE_FP8 is a weight-only FP8 model (the paper notes SpS is
  * compatible with quantisation: Introduction; Modified Rejection Sampling
@@ -183,8 +195,11 @@ sps_status sps_kv_read(sps_kv_t kv, int32_t layer, int32_t b, int32_t pos0, int3
 /* ---- workspace ------------------------------------------------------- */
 
 /* Bytes of scratch a forward / verify / draft call needs for B sequences of
- * up to max_tokens_per_seq new tokens each (<= 64; B * max_tokens_per_seq <=
- * 160) against a cache of capacity T_cap. */
+ * up to max_tokens_per_seq new tokens each against a cache of capacity
+ * T_cap: any call with B sequences and at most that many tokens per sequence
+ * (a verify step takes K + 1, a draft step 2) fits. 0 for an invalid config,
+ * T_cap < 32, or a request no call admits (max_tokens_per_seq > 64 or
+ * B * max_tokens_per_seq > 160). */
 size_t sps_workspace_bytes(const sps_config* cfg, int32_t B, int32_t max_tokens_per_seq,
                            int32_t T_cap);
 
@@ -251,12 +266,18 @@ sps_status sps_accept_resample(const float* p_draft, const float* q_target,
  * Each step forms p_t = the modified softmax(logits / T) of `sampling`,
  * writes it to p_out[b][t-1][:],
  * and draws x~_t with Philox purpose DRAFT, j = t-1. Writes the verify input
- * tokens[b] = (ctx[b][1], x~_1..x~_K) ([B][K+1]). Requires lengths[b] >= 1. */
+ * tokens[b] = (ctx[b][1], x~_1..x~_K) ([B][K+1]). Requires lengths[b] >= 1.
+ * p_out is [B][K][V] fp32 with V the draft's vocabulary: a draft whose p rows
+ * feed a target's verify step must have the target's vocabulary (the accept
+ * ratio compares the two distributions over one token space). The
+ * workspace must hold sps_workspace_bytes(cfg, B, 2, T_cap) bytes. */
 sps_status sps_draft_step(sps_model_t draft, sps_kv_t kv, const int32_t* ctx, int32_t B,
                           int32_t K, sps_sampling sampling, sps_philox rng, int32_t* tokens,
                           float* p_out, void* workspace, size_t ws_bytes, void* stream);
 
-/* End of an SpS loop, on the device (no host synchronisation): for each
+/* End of an SpS loop (Algorithm 2: after the accept loop the sequence grows
+ * by the a accepted drafts plus the resampled or bonus token, so n advances
+ * by a + 1), on the device (no host synchronisation): for each
  * sequence with a = n_accepted[b], lengths[b] += a + 1, ctx[b] =
  * (tokens[b][a], out_tokens[b][a]); the a + 1 emitted tokens are appended to
  * seq_out[b][*] (capacity `cap` per sequence, int32 [B][cap]) at n_out[b].

@@ -30,7 +30,12 @@ sequential law by exact enumeration and by chi-square.
 
 Error handling (defined outputs, no exceptions): a draft token outside
 [0, V) is treated as rejected at its position and sets FLAG_BAD_TOKEN; a
-draw whose weights are all zero returns token 0 and sets FLAG_EMPTY.
+draw whose weights are all zero returns token 0 and sets FLAG_EMPTY. The
+paper assumes valid distributions; a sequence whose inputs are not -- a
+target row marked as having non-finite logits, a NaN or infinite value
+among the gathered q_t(x~_t), p_t(x~_t) (every t with a valid draft
+token), or among the entries of the rows the final draw reads -- is given
+a = 0 and token 0 and sets FLAG_NONFINITE.
 """
 import numpy as np
 
@@ -39,6 +44,11 @@ from .sampling import to_weights, categorical
 
 FLAG_BAD_TOKEN = 1
 FLAG_EMPTY = 2
+FLAG_NONFINITE = 8
+
+
+def _finite(x):
+    return bool(np.all(np.isfinite(np.asarray(x, dtype=np.float32))))
 
 
 def accept_test(r, pi, rho):
@@ -53,14 +63,21 @@ def residual_weights(q_row, p_row):
     return np.maximum(wq - wp, 0).astype(np.uint64)
 
 
-def accept_resample_one(p, q, drafts, unif):
-    """One sequence. p: [K][V], q: [K+1][V] fp32; drafts: [K]; unif: [K+1].
+def accept_resample_one(p, q, drafts, unif, bad_rows=None):
+    """One sequence. p: [K][V], q: [K+1][V] fp32; drafts: [K]; unif: [K+1];
+    bad_rows: optional [K+1] bools, target rows whose logits were
+    non-finite.
 
     Returns (tokens, a, flags) where tokens has length a + 1.
     """
     K = len(drafts)
     V = q.shape[-1]
     flags = 0
+    nonfinite = bad_rows is not None and bool(np.any(bad_rows))
+    for t in range(K):                     # every gathered value is checked
+        x = int(drafts[t])
+        if 0 <= x < V and not (_finite(q[t][x]) and _finite(p[t][x])):
+            nonfinite = True
     a = K
     for t in range(K):                     # draft position t+1 in the paper
         x = int(drafts[t])
@@ -71,21 +88,26 @@ def accept_resample_one(p, q, drafts, unif):
         if not accept_test(unif[t], p[t][x], q[t][x]):
             a = t
             break
-    if a < K:
-        w = residual_weights(q[a], p[a])
-        if int(w.sum(dtype=np.uint64)) == 0:
-            w = to_weights(q[a])
-    else:
-        w = to_weights(q[K])
+    if not nonfinite:
+        if a < K:
+            nonfinite = not (_finite(q[a]) and _finite(p[a]))
+            w = residual_weights(q[a], p[a])
+            if int(w.sum(dtype=np.uint64)) == 0:
+                w = to_weights(q[a])
+        else:
+            nonfinite = not _finite(q[K])
+            w = to_weights(q[K])
+    if nonfinite:
+        return [0], 0, flags | FLAG_NONFINITE
     y, ok = categorical(w, unif[K])
     if not ok:
         flags |= FLAG_EMPTY
     return [int(v) for v in drafts[:a]] + [y], a, flags
 
 
-def accept_resample(p_draft, q_target, draft_tokens, unif):
+def accept_resample(p_draft, q_target, draft_tokens, unif, bad_rows=None):
     """Batched: p_draft [B][K][V], q_target [B][K+1][V], draft_tokens [B][K],
-    unif [B][K+1] (r_1..r_K, then u).
+    unif [B][K+1] (r_1..r_K, then u), bad_rows [B][K+1] or None.
 
     Returns out_tokens [B][K+1] int32 (entries after the a+1 emitted tokens
     are -1), n_accepted [B] int32, flags [B] int32.
@@ -101,7 +123,8 @@ def accept_resample(p_draft, q_target, draft_tokens, unif):
     flags = np.zeros(B, dtype=np.int32)
     for b in range(B):
         toks, a, f = accept_resample_one(p_draft[b] if K else np.zeros((0, q_target.shape[-1]), np.float32),
-                                         q_target[b], draft_tokens[b][:K], unif[b])
+                                         q_target[b], draft_tokens[b][:K], unif[b],
+                                         None if bad_rows is None else bad_rows[b])
         out[b, :a + 1] = toks
         n_acc[b] = a
         flags[b] = f

@@ -35,15 +35,21 @@ def probs_fp32(logits, temperature):
     return softmax(logits, temperature).astype(np.float32)
 
 
-def sps_generate_one(tspec, tW, dspec, dW, prompt, n_new, K, temperature, seed, b=0):
+def sps_generate_one(tspec, tW, dspec, dW, prompt, n_new, K, temperature, seed, b=0, loop0=0, truncate=True,
+                     trace=None):
     """Generate n_new tokens for one sequence (batch index b in the RNG).
 
-    Returns (tokens, accepted) where accepted lists a per loop.
+    Returns (tokens, accepted) where accepted lists a per loop. The SpS
+    state at a loop boundary is the token sequence and the loop index, so a
+    run can stop there (truncate=False keeps every token of the last loop)
+    and resume: the next call takes prompt + the tokens so far and loop0 =
+    the loops done. If trace is a list, each loop appends a dict of its
+    drafts, p rows, q rows, uniforms and outcome.
     """
     seq = [int(t) for t in prompt]
     out = []
     accepted = []
-    loop = 0
+    loop = loop0
     while len(out) < n_new:
         drafts, ps = [], []
         if K > 0:
@@ -62,11 +68,14 @@ def sps_generate_one(tspec, tW, dspec, dW, prompt, n_new, K, temperature, seed, 
         unif = np.concatenate([r, u])
         p_arr = np.array(ps, dtype=np.float32).reshape(K, q.shape[-1])
         toks, a, _ = accept_resample_one(p_arr, q, drafts, unif)
+        if trace is not None:
+            trace.append({"loop": loop, "drafts": list(drafts), "ud": ud[:K] if K else None, "p": p_arr, "q": q,
+                          "unif": unif, "a": a, "tokens": toks})
         seq += toks
         out += toks
         accepted.append(a)
         loop += 1
-    return out[:n_new], accepted
+    return (out[:n_new] if truncate else out), accepted
 
 
 def ars_generate_one(tspec, tW, prompt, n_new, temperature, seed, b=0):

@@ -29,9 +29,25 @@ import numpy as np
 TWO32 = 1 << 32
 
 
+def nonfinite_rows(logits, temperature):
+    """Rows that have no distribution: a NaN or +Inf logit, or (T > 0) a
+    logit whose fp32 quotient by T, formed as z * fp32(1 / T) in fp32,
+    overflows to +Inf. -Inf logits are valid (probability 0). The paper
+    assumes valid distributions (Modified Rejection Sampling section); the
+    library defines such a row as one-hot at token 0."""
+    z = np.asarray(logits, dtype=np.float32)
+    with np.errstate(over="ignore", invalid="ignore"):
+        if temperature != 0.0:
+            z = z * np.float32(np.float32(1.0) / np.float32(temperature))
+        return ~np.all(z < np.float32(np.inf), axis=-1)
+
+
 def softmax(logits, temperature):
-    """Row-wise softmax(logits / T) in fp64; T == 0 gives one-hot argmax."""
+    """Row-wise softmax(logits / T) in fp64; T == 0 gives one-hot argmax.
+    Rows in nonfinite_rows are one-hot at index 0."""
     z = np.asarray(logits, dtype=np.float64)
+    bad = nonfinite_rows(logits, temperature)
+    z = np.where(bad[..., None], 0.0, z)
     if temperature == 0.0:
         out = np.zeros_like(z)
         idx = np.argmax(z, axis=-1)          # first index among equal maxima
@@ -40,7 +56,10 @@ def softmax(logits, temperature):
     z = z / float(temperature)
     z = z - z.max(axis=-1, keepdims=True)
     e = np.exp(z)
-    return e / e.sum(axis=-1, keepdims=True)
+    out = e / e.sum(axis=-1, keepdims=True)
+    out[bad] = 0.0
+    out[bad, ..., 0] = 1.0
+    return out
 
 
 def to_weights(x):

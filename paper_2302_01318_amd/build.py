@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(os.path.dirname(HERE), "_build")
 LIB = os.path.join(HERE, "libsps.so")
-SOURCES = ["gemm.hip", "gemm_wide.hip", "layers.hip", "attention.hip", "sampling.hip", "sps_api.hip"]
+SOURCES = ["plan.cpp", "gemm.hip", "gemm_wide.hip", "layers.hip", "attention.hip", "sampling.hip", "sps_api.hip"]
 ARCH = "gfx950"
 FLAGS = ["--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

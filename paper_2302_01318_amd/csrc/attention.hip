@@ -17,7 +17,7 @@
 
 namespace sps {
 
-constexpr int kWavePos = 64;         // positions per wave (prefill chunks): two 32-position blocks
+constexpr int kWavePos = kAttnWavePos;   // positions per wave (prefill chunks): two 32-position blocks
 
 // One 32-position block for one query tile: scores, masked online softmax,
 // and accumulation of O^T. For bf16 the softmax weights enter the P V MFMA
@@ -259,8 +259,6 @@ __global__ __launch_bounds__(DH) void attn_combine_kernel(const float* __restric
   store_act(o, oplane, static_cast<size_t>(row) * H * DH + h * DH + d, L > 0.f ? acc / L : 0.f);
 }
 
-// Upper bound of partials per (sequence, head): one per wave (prefill).
-int attn_partials(int T_cap) { return (T_cap + kWavePos - 1) / kWavePos; }
 
 // Decode launches (up to 16 new tokens per sequence): WP positions per wave,
 // partials merged per work-group of 4 WP positions.

@@ -16,6 +16,7 @@ constexpr int kWave = 64;
 constexpr int kErrBadToken = 1;
 constexpr int kErrEmpty = 2;
 constexpr int kErrCapacity = 4;
+constexpr int kErrNonFinite = 8;
 
 // ---------------------------------------------------------------------------
 // Eight-element operand fragments.

@@ -259,14 +259,6 @@ static hipError_t gemm_launch(const GemmParams& p, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Two output tiles per wave (half the activation loads per weight byte, 8
-// waves per work-group) once the matrix is large enough (>= 512 tiles wide,
-// >= ~120 MB of bf16 weights) for 256+ work-groups to stream long enough;
-// smaller matrices keep one tile per wave and 16 waves.
-static int single_tile_ntw(int NT, int KT) {
-  return (NT % 2 == 0 && NT >= 512 && static_cast<long>(NT) * KT >= 120000) ? 2 : 1;
-}
-
 // fp32 models (16-row M tiles) at any row count, bf16 models at <= 8 rows.
 // bf16 launches over more rows go to the wide kernel (gemm_wide.hip).
 static hipError_t gemm_dispatch_f32(const GemmParams& p, hipStream_t st) {
@@ -299,16 +291,6 @@ static hipError_t gemm_dispatch_bf16(const GemmParams& p, hipStream_t st) {
   return gemm_launch<T, 1, 1, 16, 4>(p, st);
 }
 
-// FP8 weights, one M tile (8 rows; more rows take the wide kernel). From a
-// launch-shape sweep over the 70B, 7B and draft matrices at 0, 1 and 5 rows:
-// from 512 n-tiles, two n-tiles per wave (each activation fragment feeds two
-// MFMA pairs), 8-wave work-groups and 4 k-tiles (2 code loads of 16 B per
-// lane and n-tile) per chunk; below, one n-tile, 16 waves and 8 k-tiles
-// (enough work-groups for the 3072- and 4096-wide outputs). At 5 rows the
-// activation fragments, read by every wave from L2, cost ~10 % of the 70B
-// launches against the same launch with no activation rows.
-static int fp8_ntw(int NT, int) { return NT % 2 == 0 && NT >= 512 ? 2 : 1; }
-
 static hipError_t gemm_dispatch_fp8(const GemmParams& p, hipStream_t st) {
   using T = bf16;
   if (!p.wscale || p.KT % 2) return hipErrorInvalidValue;
@@ -318,22 +300,6 @@ static hipError_t gemm_dispatch_fp8(const GemmParams& p, hipStream_t st) {
   return gemm_launch<T, 1, 1, 16, 8, true>(p, st);
 }
 
-// One launch covers up to 160 rows (20 M tiles of 8 bf16 rows, 10 of 16
-// fp32); bf16 and FP8 weights take the wide kernel above 8 rows.
-int gemm_max_rows(int dtype) { return dtype == 0 ? 10 * ActRows<float>::kRows : 20 * ActRows<bf16>::kRows; }
-
-bool gemm_is_wide(int dtype, int Mtot) { return dtype != 0 && Mtot > ActRows<bf16>::kRows; }
-
-int gemm_groups(int dtype, int NT, int KT, int Mtot) {
-  if (gemm_is_wide(dtype, Mtot)) return wide_groups(NT);
-  if (dtype == 2) {
-    const int ntw = fp8_ntw(NT, KT);
-    return (NT + ntw - 1) / ntw;
-  }
-  const int rows = dtype == 1 ? ActRows<bf16>::kRows : ActRows<float>::kRows;
-  const int ntw = (Mtot <= rows) ? single_tile_ntw(NT, KT) : 1;
-  return (NT + ntw - 1) / ntw;
-}
 
 hipError_t launch_gemm(int dtype, const GemmParams& p, hipStream_t st) {
   return dtype == 2 ? gemm_dispatch_fp8(p, st) : dtype == 1 ? gemm_dispatch_bf16(p, st) : gemm_dispatch_f32(p, st);

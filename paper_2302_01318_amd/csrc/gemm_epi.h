@@ -15,8 +15,8 @@ __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 // Activation rows per 16-row MFMA tile: bf16 tiles carry 8 rows as hi and lo
 // planes, fp32 tiles 16 rows.
 template <typename T> struct ActRows;
-template <> struct ActRows<bf16> { static constexpr int kRows = 8; };
-template <> struct ActRows<float> { static constexpr int kRows = 16; };
+template <> struct ActRows<bf16> { static constexpr int kRows = kActRowsBf16; };
+template <> struct ActRows<float> { static constexpr int kRows = kActRowsF32; };
 
 // Packed position of dim f of a head in a QKV tile: the rotate-half partners
 // f and f + DH/2 sit in rows r and r + 8 of the same 16-row tile.

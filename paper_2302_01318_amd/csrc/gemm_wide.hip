@@ -38,23 +38,6 @@
 
 namespace sps {
 
-constexpr int kWideWaves = 4;                      // waves per work-group
-constexpr int kCUs = 256;                          // compute units of the GPU (MI355X)
-constexpr long kLdsBytes = 160 * 1024;             // LDS per CU
-constexpr int kNormTiles = 8;                      // n-tiles per norm group (128 columns)
-
-// n-tiles per wave. (With register-held weights, 4 at 14 M tiles ran the
-// 70B W_1 and W_2 22-24 % faster than 2; the staged loop at 2 beats both.)
-static constexpr int wide_ntw(int) { return 2; }
-
-// Where the weights go through LDS too (wide_mainloop_staged): from 14 M
-// tiles for bf16 weights, where one wave per SIMD with register-held weights
-// has one chunk in flight, and from 8 for FP8 codes, whose register path
-// keeps only 4 KiB per wave in flight. Below, the register path with two to
-// three work-groups per CU is faster.
-static constexpr bool wide_staged(int MT, bool w8) { return MT >= (w8 ? 8 : 14); }
-constexpr int kWideStages = 4;
-
 // s_waitcnt operand that waits until at most n vector memory operations of
 // this wave are outstanding, ignoring the export and LDS/scalar counters
 // (gfx9 encoding: vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
@@ -64,9 +47,6 @@ constexpr int vmcnt_only(int n) { return (n & 15) | ((n >> 4) & 3) << 14 | 7 << 
 // hi rows after folding the lo rows in), in register order.
 template <int MT, int NTW> constexpr int wide_part_floats() { return NTW * MT * 128; }
 
-// Waves per SIMD the register allocation must allow (the compiler would
-// otherwise hoist every LDS fragment read of a chunk into registers).
-static constexpr int waves_per_simd(int MT) { return MT > 12 ? 1 : MT <= 6 ? 3 : 2; }
 template <int MT, int NTW> constexpr int wide_waves_per_simd() { return waves_per_simd(MT); }
 
 // Weight registers of one chunk: bf16 fragments, or the raw FP8 code loads
@@ -555,55 +535,6 @@ __global__ __launch_bounds__(kWideWaves * 64) void gemm_wide_reduce_kernel(const
 // ---------------------------------------------------------------------------
 // Launch planning.
 // ---------------------------------------------------------------------------
-static const int kWideMT[] = {2, 3, 4, 5, 6, 8, 10, 12, 14, 16, 18, 20};
-
-// k-tiles per chunk, whole pairs (activation blocks, FP8 codes): the two
-// chunk buffers (2 MT KC KiB of LDS) leave room for two to three
-// work-groups per CU up to 12 M tiles (one from 14, where registers allow
-// one wave per SIMD; from 16 the staged loop also needs LDS for its weight
-// ring) and hold a norm group's output tile (4 MT KiB).
-static constexpr int wide_kc(int MT, bool w8) { return wide_staged(MT, w8) ? 2 : MT <= 10 ? 4 : 2; }
-
-WidePlan wide_plan(int NT, int KT, int M, bool w8) {
-  WidePlan w{};
-  const int mt = (M + 7) / 8;
-  w.MT = 20;
-  for (int v : kWideMT)
-    if (v >= mt) { w.MT = v; break; }
-  w.w8 = w8;
-  w.KC = wide_kc(w.MT, w8);
-  w.NTW = wide_ntw(w.MT);
-  w.G = (NT + kWideWaves * w.NTW - 1) / (kWideWaves * w.NTW);
-  w.chunks = (KT + w.KC - 1) / w.KC;
-  // Split count: the work-groups a CU holds at once (LDS of the split
-  // kernel, waves per SIMD the registers allow) give the launch's slots; a
-  // launch of G S work-groups runs in ceil(G S / slots) rounds of ~chunks / S
-  // chunks plus a fixed cost per work-group (~8 chunks). Minimising that over
-  // the measured split counts picks full last rounds: 4 splits for 192
-  // column groups at one work-group per CU (768 = 3 x 256; 2 splits leave a
-  // half-empty second round, 16 % slower), 2 for 250 at two per CU.
-  const bool staged = wide_staged(w.MT, w8);
-  const long lds = 2L * w.MT * w.KC * 1024 +
-                   (staged ? static_cast<long>(kWideStages) * kWideWaves * w.NTW * (w8 ? w.KC / 2 : w.KC) * 1024 : 0);
-  const int occ = std::max(1, std::min(static_cast<int>(kLdsBytes / lds), waves_per_simd(w.MT)));
-  const long slots = static_cast<long>(kCUs) * occ;
-  long best = -1;
-  w.S = 1;
-  for (int S : {1, 2, 3, 4, 6, 8}) {
-    if (S > 1 && S > w.chunks / 2) break;
-    const long rounds = (static_cast<long>(w.G) * S + slots - 1) / slots;
-    const long cost = rounds * ((w.chunks + S - 1) / S + 8);
-    if (best < 0 || cost < best) { best = cost; w.S = S; }
-  }
-  return w;
-}
-
-size_t wide_part_bytes(const WidePlan& w) {
-  return w.S > 1 ? static_cast<size_t>(w.S) * w.G * kWideWaves * w.NTW * w.MT * 128 * sizeof(float) : 0;
-}
-
-int wide_groups(int NT) { return (NT + kNormTiles - 1) / kNormTiles; }
-
 template <int MT, bool W8, int KC = wide_kc(MT, W8), int NTW = wide_ntw(MT)>
 static hipError_t wide_launch(const GemmParams& p, const WidePlan& w, hipStream_t st) {
   const dim3 block(kWideWaves * 64);

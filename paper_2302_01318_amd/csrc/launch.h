@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "plan.h"
+
 namespace sps {
 
 enum Epilogue { kEpiStore = 0, kEpiGelu = 1, kEpiSwiglu = 2, kEpiResid = 3, kEpiQkv = 4 };
@@ -42,17 +44,9 @@ struct GemmParams {
   int epi;
 };
 hipError_t launch_gemm(int dtype, const GemmParams& p, hipStream_t st);
-int gemm_max_rows(int dtype);                 // rows one launch handles
-int gemm_groups(int dtype, int NT, int KT, int Mtot); // column groups (ss_out groups) of a GEMM
 
 // Wide GEMM (bf16 activations, bf16 or FP8 weights, more than 8 rows;
-// gemm_wide.hip): M tiles, k-tiles per chunk, n-tiles per wave, column groups
-// (4 NTW n-tiles each), k splits and chunks of one launch.
-struct WidePlan { int MT, KC, NTW, G, S, chunks; bool w8; };
-bool gemm_is_wide(int dtype, int Mtot);
-WidePlan wide_plan(int NT, int KT, int M, bool w8);   // w8: FP8 weight codes
-size_t wide_part_bytes(const WidePlan& w);    // workspace for the split-K partials
-int wide_groups(int NT);                      // norm groups (8 n-tiles each)
+// gemm_wide.hip) with the launch plan of plan.h.
 hipError_t launch_gemm_wide(const GemmParams& p, const WidePlan& w, hipStream_t st);
 
 // Pack canonical rows src[n][k] (n < n_src, k < Kd) into tile order. Row n goes
@@ -83,7 +77,6 @@ hipError_t launch_embed(int dtype, const int32_t* tokens, int tok_stride, int Mp
 hipError_t launch_attention(int dtype, const void* q, const void* kc, const void* vc,
                             const int32_t* lengths, int pos_offset, int B, int Mps, int H, int DH,
                             int T_cap, float* part, void* o, size_t oplane, hipStream_t st);
-int attn_partials(int T_cap);
 hipError_t launch_kv_copy(int dtype, int to_cache, void* kc, void* vc, int H, int DH, int T_cap,
                           int pos0, int n, void* k, void* v, hipStream_t st);
 
@@ -92,9 +85,7 @@ hipError_t launch_kv_copy(int dtype, int to_cache, void* kc, void* vc, int H, in
 // != NULL, the probabilities after temperature and the top-k / nucleus
 // modifiers (top_k <= 0 or >= V: off; top_p >= 1: off).
 hipError_t launch_row_softmax(const float* logits, int rows, int V, float temperature, int top_k, float top_p,
-                              void* stats, float* probs, hipStream_t st);
-size_t row_stat_bytes();
-int modifier_max_vocab();        // largest vocabulary the top-k / nucleus cut-off handles
+                              void* stats, float* probs, int* err, hipStream_t st);
 hipError_t launch_accept_probs(const float* p, const float* q, const int32_t* drafts,
                                const float* unif, uint64_t seed, uint64_t loop, int B, int K,
                                int V, int32_t* out, int32_t* n_acc, int* err, hipStream_t st);

@@ -17,8 +17,6 @@
 
 namespace sps {
 
-constexpr int kSampleThreads = 1024;
-constexpr int kPerLane = 32;            // row entries per thread read together (row statistics)
 constexpr int kTotalBatch = 8;          // entries per lane read together (segment totals)
 constexpr int kScanPerLane = 16;        // entries per lane of the threshold search (registers)
 
@@ -63,11 +61,16 @@ __device__ __forceinline__ uint64_t grid_threshold(float u, uint64_t W) {
 // exp(z/T - max)), for T == 0 (greedy) (index of the first maximum, -1).
 // With a top-k / nucleus modifier, s > 0 is the renormaliser and tau the
 // smallest kept ranking key (see row_cutoff); s == 0 means unmodified.
+// A row with a NaN or +Inf logit (or z/T overflowing to +Inf) has no
+// distribution: it is marked non-finite and defined as one-hot at index 0
+// (a = 0, b = -1, like a greedy row), and whoever uses it raises the device
+// flag.
 struct RowStat {
   float a, b, s;
-  uint32_t pad;
+  uint32_t nonfinite;
   uint64_t tau;
 };
+static_assert(sizeof(RowStat) == kRowStatBytes, "workspace row statistics");
 
 // Probability of entry i of a row. The same expression (no contraction) is
 // used wherever q or p is materialised, so exported probabilities and the
@@ -104,13 +107,15 @@ __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, 
                                           int* ired) {
   RowStat st;
   st.s = 0.f;
-  st.pad = 0;
+  st.nonfinite = 0;
   st.tau = 0;
   if (temperature == 0.f) {
     float best = -INFINITY;
     int bi = 0x7fffffff;
+    bool bad = false;
     for (int i = threadIdx.x; i < V; i += blockDim.x) {
       const float v = z[i];
+      bad |= !(v < INFINITY);                       // NaN or +Inf
       if (v > best || (bi == 0x7fffffff)) { best = v; bi = i; }
     }
     // arg-max with the lowest index on ties
@@ -125,7 +130,8 @@ __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, 
     best = red[0]; bi = ired[0];
     for (int w = 1; w < static_cast<int>(blockDim.x >> 6); ++w)
       if (red[w] > best || (red[w] == best && ired[w] < bi)) { best = red[w]; bi = ired[w]; }
-    st.a = static_cast<float>(bi);
+    st.nonfinite = __syncthreads_or(bad) ? 1u : 0u;
+    st.a = st.nonfinite ? 0.f : static_cast<float>(bi);
     st.b = -1.f;
     return st;
   }
@@ -134,6 +140,7 @@ __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, 
   // from the registers; longer rows keep a running (max, sum) per thread.
   const float inv_t = 1.0f / temperature;
   float mx = -INFINITY, sm = 0.f;
+  bool bad = false;
   if (V <= kPerLane * static_cast<int>(blockDim.x)) {
     float x[kPerLane];
 #pragma unroll
@@ -142,6 +149,7 @@ __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, 
 #pragma unroll
     for (int k = 0; k < kPerLane; ++k) {
       x[k] = threadIdx.x + k * blockDim.x < static_cast<unsigned>(V) ? __fmul_rn(x[k], inv_t) : -INFINITY;
+      bad |= !(x[k] < INFINITY);
       mx = fmaxf(mx, x[k]);
     }
     if (mx > -INFINITY) {
@@ -151,6 +159,7 @@ __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, 
   } else {
     for (int i = threadIdx.x; i < V; i += blockDim.x) {
       const float x = __fmul_rn(z[i], inv_t);
+      bad |= !(x < INFINITY);
       if (x > mx) {
         sm = sm * expf(mx - x) + 1.f;
         mx = x;
@@ -178,6 +187,11 @@ __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, 
   for (int w = 1; w < static_cast<int>(blockDim.x >> 6); ++w) merge(mx, sm, red[w], red[16 + w]);
   st.a = mx;
   st.b = sm;
+  if (__syncthreads_or(bad)) {
+    st.nonfinite = 1;
+    st.a = 0.f;
+    st.b = -1.f;
+  }
   return st;
 }
 
@@ -326,6 +340,22 @@ __device__ __forceinline__ bool modifiers_active(float temperature, int top_k, f
   return temperature > 0.f && ((top_k >= 1 && top_k < V) || top_p < 1.f);
 }
 
+// Row statistics with the top-k / nucleus cut-off applied (block-wide). A
+// non-finite row stays one-hot at index 0 (never cut) and raises the flag.
+__device__ __forceinline__ RowStat row_stat_final(const float* __restrict__ z, int V, float temperature, int top_k,
+                                                  float top_p, float* red, int* ired, CutScratch& sc,
+                                                  uint32_t* lds, int* err) {
+  RowStat st = row_stat(z, V, temperature, red, ired);
+  if (st.nonfinite) {
+    if (threadIdx.x == 0) atomicOr(err, kErrNonFinite);
+  } else if (modifiers_active(temperature, top_k, top_p, V)) {
+    const float inv_t = 1.0f / temperature;
+    const RowStat base = st;
+    row_cutoff([&](int i) { return prob_of(z[i], base, inv_t, i); }, V, top_k, top_p, st, sc, lds);
+  }
+  return st;
+}
+
 // pr[i] = prob_final(z[i]) for the whole row, 8 loads per thread in flight.
 template <bool MOD>
 __device__ __forceinline__ void write_probs_t(const float* __restrict__ z, int V, const RowStat& st, float inv_t,
@@ -351,19 +381,15 @@ __device__ __forceinline__ void write_probs(const float* __restrict__ z, int V, 
 __global__ __launch_bounds__(kSampleThreads) void row_softmax_kernel(const float* __restrict__ logits, int V,
                                                                      float temperature, int top_k, float top_p,
                                                                      RowStat* __restrict__ stats,
-                                                                     float* __restrict__ probs) {
+                                                                     float* __restrict__ probs, int* err) {
   __shared__ float red[32];
   __shared__ int ired[16];
   __shared__ CutScratch sc;
   extern __shared__ uint32_t s_rowkeys[];
   const int row = blockIdx.x;
   const float* z = logits + static_cast<size_t>(row) * V;
-  RowStat st = row_stat(z, V, temperature, red, ired);
+  const RowStat st = row_stat_final(z, V, temperature, top_k, top_p, red, ired, sc, s_rowkeys, err);
   const float inv_t = temperature == 0.f ? 0.f : 1.0f / temperature;
-  if (modifiers_active(temperature, top_k, top_p, V)) {
-    const RowStat base = st;
-    row_cutoff([&](int i) { return prob_of(z[i], base, inv_t, i); }, V, top_k, top_p, st, sc, s_rowkeys);
-  }
   if (threadIdx.x == 0 && stats) stats[row] = st;
   if (probs) write_probs(z, V, st, inv_t, probs + static_cast<size_t>(row) * V);
 }
@@ -463,6 +489,7 @@ struct QProbs {
   struct Row {
     const float* q;
     __device__ bool modified() const { return false; }
+    __device__ bool nonfinite() const { return false; }   // given values: checked where read
     template <bool MOD> __device__ float get(int i) const { return q[i]; }
     __device__ float operator()(int i) const { return q[i]; }
   };
@@ -479,6 +506,7 @@ struct QLogits {
     RowStat st;
     float inv_t;
     __device__ bool modified() const { return row_modified(st); }
+    __device__ bool nonfinite() const { return st.nonfinite != 0; }
     template <bool MOD> __device__ float get(int i) const { return prob_final<MOD>(z[i], st, inv_t, i); }
     __device__ float operator()(int i) const {
       return modified() ? get<true>(i) : get<false>(i);
@@ -487,24 +515,38 @@ struct QLogits {
   __device__ Row row(int r) const { return Row{z + static_cast<size_t>(r) * V, st[r], inv_t}; }
 };
 
+__device__ __forceinline__ bool not_finite(float x) { return !(fabsf(x) < INFINITY); }
+
 // The final draw of one sequence: from (q - p)_+ if resid (falling back to
-// q when its weights sum to 0), else from q. -1 if q's weights are all 0.
+// q when its weights sum to 0), else from q. -1 if q's weights are all 0,
+// -2 if a value of a row it read is NaN or infinite.
 template <bool MOD, class Row>
 __device__ __forceinline__ int accept_draw(const Row& qr, const float* __restrict__ prow, bool resid, int V,
                                            float u, uint64_t* wsum, int* s_y) {
   const Segment sg = wave_segment(V);
-  auto wq = [&](int i) -> uint64_t { return fixed_weight(qr.template get<MOD>(i)); };
+  bool nf = false;
+  auto wq = [&](int i) -> uint64_t {
+    const float x = qr.template get<MOD>(i);
+    nf |= not_finite(x);
+    return fixed_weight(x);
+  };
   auto wr = [&](int i) -> uint64_t {
-    const uint64_t x = fixed_weight(qr.template get<MOD>(i)), y = fixed_weight(prow[i]);
+    const float xq = qr.template get<MOD>(i), xp = prow[i];
+    nf |= not_finite(xq) | not_finite(xp);
+    const uint64_t x = fixed_weight(xq), y = fixed_weight(xp);
     return x > y ? x - y : 0;
   };
   int y = -1;
   if (resid) y = block_draw(wr, sg, segment_total(wr, sg), u, wsum, s_y);
   if (y < 0) y = block_draw(wq, sg, segment_total(wq, sg), u, wsum, s_y);
-  return y;
+  return __syncthreads_or(nf) ? -2 : y;
 }
 
 // One block per sequence. drafts[b * dstride + doff + t] is x~_{t+1}.
+// A sequence whose inputs hold a non-finite value -- a target row with a
+// NaN / +Inf logit, a NaN or infinite gathered probability, or one in a row
+// of the final draw -- has no defined outcome: it is given a = 0 and token
+// 0, and the device flag is raised.
 template <class QS>
 __global__ __launch_bounds__(kSampleThreads) void accept_kernel(QS qs, const float* __restrict__ p,
                                                                 const int32_t* __restrict__ drafts, int dstride,
@@ -512,14 +554,14 @@ __global__ __launch_bounds__(kSampleThreads) void accept_kernel(QS qs, const flo
                                                                 uint64_t seed, uint64_t loop, int K, int V,
                                                                 int32_t* __restrict__ out,
                                                                 int32_t* __restrict__ n_acc, int* err) {
-  __shared__ int s_a, s_y;
+  __shared__ int s_a, s_y, s_nf;
   __shared__ uint64_t wsum[17];
   const int b = blockIdx.x, tid = threadIdx.x;
   const int32_t* dr = drafts + static_cast<size_t>(b) * dstride + doff;
 
   // 1. left-to-right accept tests r_t * p_t(x~_t) < q_t(x~_t), exact in fp64
   if (tid < 64) {
-    bool rejected = false, bad = false;
+    bool rejected = false, bad = false, nf = false;
     if (tid < K) {
       const int x = dr[tid];
       if (x < 0 || x >= V) {
@@ -529,26 +571,36 @@ __global__ __launch_bounds__(kSampleThreads) void accept_kernel(QS qs, const flo
         const float rho = qs.row(b * (K + 1) + tid)(x);
         const float pi = p[(static_cast<size_t>(b) * K + tid) * V + x];
         const float r = unif ? unif[b * (K + 1) + tid] : philox_uniform(seed, loop, 1, b, tid);
+        nf = not_finite(rho) | not_finite(pi);
         rejected = !(static_cast<double>(r) * static_cast<double>(pi) < static_cast<double>(rho));
       }
     }
+    if (tid <= K) nf |= qs.row(b * (K + 1) + tid).nonfinite();
     const uint64_t rej = __ballot(rejected);
     const int a = rej ? __ffsll(static_cast<long long>(rej)) - 1 : K;
     if (tid == a && bad) atomicOr(err, kErrBadToken);
-    if (tid == 0) { s_a = a; s_y = 0; }
+    if (tid == 0) { s_a = a; s_y = 0; s_nf = __ballot(nf) != 0; }
   }
   __syncthreads();
-  const int a = s_a;
+  int a = s_a;
+  const bool nf_in = s_nf != 0;
   const int row = b * (K + 1) + a;
   const bool resid = a < K;
   const float* prow = p + (static_cast<size_t>(b) * K + (resid ? a : 0)) * V;
 
   // 2. draw from (q - p)_+ (or q for the bonus / the zero-residual fallback)
-  const typename QS::Row qr = qs.row(row);
-  const float u = unif ? unif[b * (K + 1) + K] : philox_uniform(seed, loop, 2, b, 0);
-  int y = qr.modified() ? accept_draw<true>(qr, prow, resid, V, u, wsum, &s_y)
-                        : accept_draw<false>(qr, prow, resid, V, u, wsum, &s_y);
-  if (y < 0) {
+  int y = -2;
+  if (!nf_in) {                            // uniform over the block
+    const typename QS::Row qr = qs.row(row);
+    const float u = unif ? unif[b * (K + 1) + K] : philox_uniform(seed, loop, 2, b, 0);
+    y = qr.modified() ? accept_draw<true>(qr, prow, resid, V, u, wsum, &s_y)
+                      : accept_draw<false>(qr, prow, resid, V, u, wsum, &s_y);
+  }
+  if (y == -2) {
+    a = 0;
+    y = 0;
+    if (tid == 0) atomicOr(err, kErrNonFinite);
+  } else if (y < 0) {
     y = 0;
     if (tid == 0) atomicOr(err, kErrEmpty);
   }
@@ -570,12 +622,10 @@ __global__ __launch_bounds__(kSampleThreads) void draft_sample_kernel(
   extern __shared__ uint32_t s_rowkeys[];
   const int b = blockIdx.x, tid = threadIdx.x;
   const float* z = logits + (static_cast<size_t>(b) * Mps + Mps - 1) * V;
-  RowStat st = row_stat(z, V, temperature, red, ired);
+  // (A row with a NaN / +Inf logit becomes p_t = one-hot at token 0, a valid
+  // draft distribution, so the draw gives token 0 and the flag is raised.)
+  const RowStat st = row_stat_final(z, V, temperature, top_k, top_p, red, ired, sc, s_rowkeys, err);
   const float inv_t = temperature == 0.f ? 0.f : 1.0f / temperature;
-  if (modifiers_active(temperature, top_k, top_p, V)) {
-    const RowStat base = st;
-    row_cutoff([&](int i) { return prob_of(z[i], base, inv_t, i); }, V, top_k, top_p, st, sc, s_rowkeys);
-  }
   // p_t once into p_out, then the draw from the stored values (visible to
   // the whole block after the barrier).
   float* pr = p_out + (static_cast<size_t>(b) * K + t) * V;
@@ -640,14 +690,14 @@ static hipError_t cutoff_lds(const void* kernel, float temperature, int top_k, f
 }
 
 hipError_t launch_row_softmax(const float* logits, int rows, int V, float temperature, int top_k, float top_p,
-                              void* stats, float* probs, hipStream_t st) {
+                              void* stats, float* probs, int* err, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   size_t lds = 0;
   const hipError_t e = cutoff_lds(reinterpret_cast<const void*>(&row_softmax_kernel), temperature, top_k, top_p, V,
                                   &lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(row_softmax_kernel, dim3(rows), dim3(kSampleThreads), lds, st, logits, V, temperature, top_k,
-                     top_p, reinterpret_cast<RowStat*>(stats), probs);
+                     top_p, reinterpret_cast<RowStat*>(stats), probs, err);
   return hipGetLastError();
 }
 
@@ -705,9 +755,5 @@ hipError_t launch_philox(uint64_t seed, uint64_t loop, int purpose, int B, int n
                      purpose, B, n, out);
   return hipGetLastError();
 }
-
-size_t row_stat_bytes() { return sizeof(RowStat); }
-
-int modifier_max_vocab() { return kPerLane * kSampleThreads; }
 
 }  // namespace sps

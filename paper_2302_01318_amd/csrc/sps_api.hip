@@ -16,138 +16,16 @@ __device__ int sps_dev_err;
 namespace {
 
 using sps::GemmParams;
-
-constexpr int kMaxTokensPerSeq = 64;
-constexpr int kMaxRows = 160;
-constexpr int kMaxK = 63;
-
-size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
-
-bool valid_config(const sps_config* c) {
-  if (!c) return false;
-  if (c->d_model < 32 || c->d_model % 32 || c->d_model > 16384) return false;
-  if (c->n_layers < 1 || c->n_heads < 1) return false;
-  if (c->head_dim != 64 && c->head_dim != 128) return false;
-  if ((c->n_heads * c->head_dim) % 32) return false;
-  if (c->d_ff < 32 || c->d_ff % 32) return false;
-  if (c->vocab < 2 || c->vocab >= (1 << 24)) return false;
-  if (c->ffn_kind != SPS_FFN_GELU && c->ffn_kind != SPS_FFN_SWIGLU) return false;
-  if (c->dtype != SPS_DTYPE_F32 && c->dtype != SPS_DTYPE_BF16 && c->dtype != SPS_DTYPE_FP8) return false;
-  // FP8 codes are packed in 64-deep k-tile pairs: every contraction depth of
-  // the forward (d_model, n_heads * head_dim, d_ff) must be a multiple of 64.
-  if (c->dtype == SPS_DTYPE_FP8 && (c->d_model % 64 || (c->n_heads * c->head_dim) % 64 || c->d_ff % 64))
-    return false;
-  if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f)) return false;
-  return true;
-}
-
-// Element type of the activations, the embedding and the KV cache: fp32
-// for fp32 models, bf16 for bf16 and FP8-weight models.
-int act_dtype(const sps_config& c) { return c.dtype == SPS_DTYPE_F32 ? 0 : 1; }
-
-// Byte offsets of every tensor in the packed weight buffer. For FP8 models
-// each projection's codes are followed by its fp32 row scales (`*_sc`).
-struct Layout {
-  int es, wes, d, L, H, DH, HD, F, V, NU, N1;   // es: activation / KV element bytes; wes: weight
-  bool swiglu, fp8;
-  size_t embed, final_norm, unembed, unembed_sc, layer0, layer_stride;
-  size_t l_attn_norm, l_ffn_norm, l_qkv, l_o, l_w1, l_w2, l_qkv_sc, l_o_sc, l_w1_sc, l_w2_sc;
-  size_t total;
-};
-
-Layout make_layout(const sps_config* c) {
-  Layout L{};
-  L.es = c->dtype == SPS_DTYPE_F32 ? 4 : 2;
-  L.fp8 = c->dtype == SPS_DTYPE_FP8;
-  L.wes = L.fp8 ? 1 : L.es;
-  L.d = c->d_model; L.L = c->n_layers; L.H = c->n_heads; L.DH = c->head_dim;
-  L.HD = L.H * L.DH; L.F = c->d_ff; L.V = c->vocab;
-  L.NU = (L.V + 15) / 16 * 16;
-  L.swiglu = c->ffn_kind == SPS_FFN_SWIGLU;
-  L.N1 = L.swiglu ? 2 * L.F : L.F;
-  const size_t es = L.es, wes = L.wes;
-  // Row scales of a projection with n packed rows (FP8 models only).
-  auto scales = [&](size_t n) { return L.fp8 ? align256(n * 4) : 0; };
-  size_t o = 0;
-  L.embed = o; o = align256(o + static_cast<size_t>(L.V) * L.d * es);
-  L.final_norm = o; o = align256(o + static_cast<size_t>(L.d) * 4);
-  L.unembed = o; o = align256(o + static_cast<size_t>(L.NU) * L.d * wes);
-  L.unembed_sc = o; o += scales(L.NU);
-  L.layer0 = o;
-  size_t lo = 0;
-  L.l_attn_norm = lo; lo = align256(lo + static_cast<size_t>(L.d) * 4);
-  L.l_ffn_norm = lo; lo = align256(lo + static_cast<size_t>(L.d) * 4);
-  L.l_qkv = lo; lo = align256(lo + static_cast<size_t>(3) * L.HD * L.d * wes);
-  L.l_qkv_sc = lo; lo += scales(static_cast<size_t>(3) * L.HD);
-  L.l_o = lo; lo = align256(lo + static_cast<size_t>(L.d) * L.HD * wes);
-  L.l_o_sc = lo; lo += scales(L.d);
-  L.l_w1 = lo; lo = align256(lo + static_cast<size_t>(L.N1) * L.d * wes);
-  L.l_w1_sc = lo; lo += scales(L.N1);
-  L.l_w2 = lo; lo = align256(lo + static_cast<size_t>(L.d) * L.F * wes);
-  L.l_w2_sc = lo; lo += scales(L.d);
-  L.layer_stride = lo;
-  L.total = L.layer0 + L.layer_stride * L.L;
-  return L;
-}
-
-// Offsets of the forward's scratch buffers.
-struct WsLayout {
-  size_t h, x, o, q, rope, apart, act, ss_a, ss_b, logits, stats, gpart, total;
-};
-
-// The GEMMs of one forward as (n-tiles, k-tiles).
-void forward_gemms(const Layout& L, int out[5][2]) {
-  const int shapes[5][2] = {{3 * L.HD / 16, L.d / 32}, {L.d / 16, L.HD / 32}, {L.N1 / 16, L.d / 32},
-                            {L.d / 16, L.F / 32}, {L.NU / 16, L.d / 32}};
-  std::memcpy(out, shapes, sizeof(shapes));
-}
-
-WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
-  WsLayout w{};
-  const int dt = L.fp8 ? SPS_DTYPE_FP8 : L.es == 2 ? SPS_DTYPE_BF16 : SPS_DTYPE_F32;   // GEMM dtype
-  const size_t M = static_cast<size_t>(B) * Mps;
-  const size_t NP = sps::attn_partials(T_cap);
-  const size_t ng = (L.d + 15) / 16;   // column groups a residual GEMM can produce
-  // Split-K partials of the wide GEMM (bf16, more than 8 rows), for every
-  // launch of the forward: full launches of gemm_max_rows rows and the
-  // remainder, which may split more ways.
-  size_t part = 0;
-  if (sps::gemm_is_wide(dt, static_cast<int>(M))) {
-    int g[5][2];
-    forward_gemms(L, g);
-    const int cap = sps::gemm_max_rows(dt);
-    const int rows[2] = {static_cast<int>(std::min<size_t>(M, cap)), static_cast<int>(M % cap)};
-    for (int r : rows) {            // (every launch of a forward past 8 rows is wide)
-      if (r <= 0) continue;
-      for (int i = 0; i < 5; ++i)
-        part = std::max(part, sps::wide_part_bytes(sps::wide_plan(g[i][0], g[i][1], r, L.fp8)));
-    }
-  }
-  size_t o = 0;
-  w.h = o; o = align256(o + M * L.d * 4);                 // residual stream (fp32)
-  w.x = o; o = align256(o + M * L.d * 4);                 // u = h * gain (activation format)
-  w.o = o; o = align256(o + M * L.HD * 4);                // attention output (activation format)
-  w.q = o; o = align256(o + M * L.HD * L.es);             // rotated queries (model dtype)
-  w.rope = o; o = align256(o + M * (L.DH / 2) * 8);       // rotary (cos, sin) per row and frequency
-  w.apart = o; o = align256(o + static_cast<size_t>(B) * L.H * NP * Mps * (L.DH + 2) * 4);
-  w.act = o; o = align256(o + M * L.F * 4);               // FFN hidden (activation format)
-  w.ss_a = o; o = align256(o + ng * M * 4);               // per-group sums of squares of h
-  w.ss_b = o; o = align256(o + ng * M * 4);
-  w.logits = o; o = align256(o + M * L.V * 4);
-  w.stats = o; o = align256(o + M * sps::row_stat_bytes());
-  w.gpart = o; o = align256(o + part);
-  w.total = o;
-  return w;
-}
-
-// Host-side check of the sampling parameters for a vocabulary of V.
-sps_status check_sampling(const sps_sampling& sp, int V) {
-  if (!(sp.temperature >= 0.f) || sp.temperature > 1e30f) return SPS_E_INVALID;
-  if (sp.top_k < 0 || !(sp.top_p >= 0.f && sp.top_p <= 1.f)) return SPS_E_INVALID;
-  const bool mod = sp.temperature > 0.f && ((sp.top_k >= 1 && sp.top_k < V) || sp.top_p < 1.f);
-  if (mod && V > sps::modifier_max_vocab()) return SPS_E_UNSUPPORTED;
-  return SPS_OK;
-}
+using sps::Layout;
+using sps::WsLayout;
+using sps::act_dtype;
+using sps::check_sampling;
+using sps::kMaxK;
+using sps::kMaxRows;
+using sps::kMaxTokensPerSeq;
+using sps::make_layout;
+using sps::make_ws;
+using sps::valid_config;
 
 int* device_error_ptr() {
   static int* ptrs[64] = {nullptr};
@@ -541,13 +419,7 @@ sps_status sps_kv_read(sps_kv_t kv, int32_t layer, int32_t b, int32_t pos0, int3
 }
 
 size_t sps_workspace_bytes(const sps_config* cfg, int32_t B, int32_t max_tokens_per_seq, int32_t T_cap) {
-  if (!valid_config(cfg) || B < 1 || max_tokens_per_seq < 1 || T_cap < 32) return 0;
-  // Every call with up to max_tokens_per_seq tokens must fit (the split-K
-  // partials of fewer rows can need more room than those of more rows).
-  const Layout L = make_layout(cfg);
-  size_t total = 0;
-  for (int mps = 1; mps <= max_tokens_per_seq; ++mps) total = std::max(total, make_ws(L, B, mps, T_cap).total);
-  return total;
+  return sps::workspace_bytes(cfg, B, max_tokens_per_seq, T_cap);
 }
 
 sps_status sps_forward(sps_model_t model, sps_kv_t kv, const int32_t* tokens, int32_t tok_stride, int32_t B,
@@ -585,7 +457,7 @@ sps_status sps_verify_step(sps_model_t target, sps_kv_t kv, const int32_t* token
   if (s != SPS_OK) return s;
   const int V = target->cfg.vocab;
   SPS_HIP(sps::launch_row_softmax(logits, B * (K + 1), V, sampling.temperature, sampling.top_k, sampling.top_p,
-                                  stats, q_out, st));
+                                  stats, q_out, err, st));
   if (acc)
     SPS_HIP(sps::launch_accept_logits(acc->p_draft, logits, stats, sampling.temperature, tokens, acc->uniforms,
                                       acc->rng.seed, acc->rng.loop, B, K, V, acc->out_tokens, acc->n_accepted, err,
@@ -661,8 +533,10 @@ sps_status sps_softmax(const float* logits, int32_t rows, int32_t V, sps_samplin
   if (!logits || !probs || rows < 0 || V < 2 || V >= (1 << 24)) return SPS_E_INVALID;
   const sps_status s = check_sampling(sampling, V);
   if (s != SPS_OK) return s;
+  int* err = device_error_ptr();
+  if (!err) return SPS_E_HIP;
   SPS_HIP(sps::launch_row_softmax(logits, rows, V, sampling.temperature, sampling.top_k, sampling.top_p, nullptr,
-                                  probs, as_stream(stream)));
+                                  probs, err, as_stream(stream)));
   return SPS_OK;
 }
 

@@ -27,7 +27,7 @@ TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16, "fp8": torch.bfloat
 TENSOR_ID = {"embed": 0, "final_norm": 1, "unembed": 2, "attn_norm": 3, "wq": 4, "wk": 5, "wv": 6,
              "wo": 7, "ffn_norm": 8, "w1": 9, "w3": 10, "w2": 11}
 PURPOSE_DRAFT, PURPOSE_ACCEPT, PURPOSE_RESAMPLE = 0, 1, 2
-DEV_BAD_TOKEN, DEV_EMPTY, DEV_CAPACITY = 1, 2, 4
+DEV_BAD_TOKEN, DEV_EMPTY, DEV_CAPACITY, DEV_NONFINITE = 1, 2, 4, 8
 
 
 class Config(ctypes.Structure):
@@ -147,6 +147,9 @@ class Model:
             raise SPSError(2, "sps_weight_bytes(%s)" % shape.name)
         self.packed = torch.empty(nbytes, dtype=torch.uint8, device=device)
         self.handle = c_void_p()
+        # __del__ may run at interpreter exit, after this module's globals
+        # are cleared: keep the destructor on the instance.
+        self._destroy = lib.sps_model_destroy
         check(lib.sps_model_create(ctypes.byref(self.cfg), _ptr(self.packed), ctypes.byref(self.handle)),
               "sps_model_create")
         if tensors is not None:
@@ -161,9 +164,10 @@ class Model:
         torch.cuda.current_stream().synchronize()   # t may be freed after return
 
     def __del__(self):
-        if getattr(self, "handle", None) and self.handle.value:
-            lib.sps_model_destroy(self.handle)
-            self.handle = c_void_p()
+        h, destroy = getattr(self, "handle", None), getattr(self, "_destroy", None)
+        if h is not None and h.value and destroy is not None:
+            destroy(h)
+        self.handle = None
 
 
 class KVCache:
@@ -178,6 +182,7 @@ class KVCache:
         self.buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
         self.lengths = lengths if lengths is not None else torch.zeros(B, dtype=torch.int32, device=device)
         self.handle = c_void_p()
+        self._destroy = lib.sps_kv_destroy   # see Model.__init__
         check(lib.sps_kv_create(ctypes.byref(self.cfg), B, T_cap, _ptr(self.buf),
                                 _ptr(self.lengths, torch.int32, "lengths"), ctypes.byref(self.handle)),
               "sps_kv_create")
@@ -197,9 +202,10 @@ class KVCache:
         return k, v
 
     def __del__(self):
-        if getattr(self, "handle", None) and self.handle.value:
-            lib.sps_kv_destroy(self.handle)
-            self.handle = c_void_p()
+        h, destroy = getattr(self, "handle", None), getattr(self, "_destroy", None)
+        if h is not None and h.value and destroy is not None:
+            destroy(h)
+        self.handle = None
 
 
 def workspace(shape, B, max_tokens_per_seq, T_cap, device="cuda"):
@@ -324,6 +330,12 @@ class Generator:
     draft model is auto-regressive sampling (Algorithm 1)."""
 
     def __init__(self, target, draft, B, T_cap, K, device="cuda", prefill_chunk=64):
+        if draft is not None and draft.shape.vocab != target.shape.vocab:
+            # p_t and q_t are distributions over one token space (the accept
+            # ratio q(x)/p(x) of Algorithm 2); the draft's p rows are read at
+            # the target's vocabulary stride.
+            raise ValueError("draft vocabulary %d differs from the target's %d"
+                             % (draft.shape.vocab, target.shape.vocab))
         self.target, self.draft, self.B, self.K, self.T_cap = target, draft, B, K, T_cap
         self.chunk = max(1, min(prefill_chunk, 160 // B, 64))
         mps = max(self.chunk, K + 1, 2)
@@ -370,31 +382,73 @@ class Generator:
                     rng=rng, out_tokens=self.out, n_accepted=self.n_acc, top_k=top_k, top_p=top_p)
         commit(self.kv_t, self.tokens, self.out, self.n_acc, K, self.ctx, seq_out, n_out, cap)
 
-    def generate(self, prompt, n_new, temperature, seed, accepted_log=None, top_k=0, top_p=1.0):
+    def generate(self, prompt, n_new, temperature, seed, accepted_log=None, top_k=0, top_p=1.0, loop0=0,
+                 log=None):
         """Prefill, then run(); returns [B][n_new] int32 tokens (device)."""
         self.prefill(prompt)
-        return self.run(n_new, temperature, seed, accepted_log, top_k, top_p)
+        return self.run(n_new, temperature, seed, accepted_log, top_k, top_p, loop0, log)
 
-    def run(self, n_new, temperature, seed, accepted_log=None, top_k=0, top_p=1.0):
+    def run(self, n_new, temperature, seed, accepted_log=None, top_k=0, top_p=1.0, loop0=0, log=None):
         """SpS loops until every sequence has n_new tokens. The host looks at
         the device-side output counts only between bursts of loops: every
         loop emits at most K + 1 tokens, so ceil(remaining / (K + 1)) loops
         can always run before the next look without overshooting the end.
+
+        loop0 is the index of the first loop (the Philox loop counter): the
+        SpS state at a loop boundary is the token sequence and the loop
+        index, so a run resumes by prefilling prompt + the tokens so far and
+        passing the loops done as loop0. self.loops is the index after the
+        last loop.
         If accepted_log is a list, (n_accepted, done-before-loop) device
-        tensors of every loop are appended to it."""
+        tensors of every loop are appended to it. If log is a writable text
+        file, one JSON line per loop -- {"loop", "ms" (HIP events around the
+        loop on the stream), "accepted" and "emitted" per sequence, -1 / 0 for
+        sequences already done} -- and one summary line at the end ({"run":
+        tokens, loops, seconds, tokens per second, mean accepted per loop})
+        are written (the paper logs the tokens each loop generates)."""
+        import json
+        import time
         dev = self.ctx.device
         seq = torch.zeros((self.B, n_new), dtype=torch.int32, device=dev)
         n_out = torch.zeros(self.B, dtype=torch.int32, device=dev)
-        loop_index = 0
+        loop_index = loop0
+        t0 = time.perf_counter()
+        acc_sum, acc_n = 0, 0
         while True:
             remaining = n_new - int(n_out.min().item())
             if remaining <= 0:
                 break
+            burst = []
             for _ in range(max(1, -(-remaining // (self.K + 1)))):
-                done = (n_out >= n_new).clone() if accepted_log is not None else None
+                want = accepted_log is not None or log is not None
+                done = (n_out >= n_new).clone() if want else None
+                before = n_out.clone() if log is not None else None
+                ev = None
+                if log is not None:
+                    ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                    ev[0].record()
                 self.loop(temperature, seed, loop_index, seq, n_out, n_new, top_k, top_p)
+                if log is not None:
+                    ev[1].record()
+                    burst.append((loop_index, ev, self.n_acc.clone(), done, before, n_out.clone()))
                 if accepted_log is not None:
                     accepted_log.append((self.n_acc.clone(), done))
                 loop_index += 1
+            for li, ev, a, done, before, after in burst:   # resolved once the burst has run
+                ev[1].synchronize()
+                live = ~done
+                acc = [int(x) if bool(l) else -1 for x, l in zip(a.tolist(), live.tolist())]
+                emitted = (after - before).tolist()
+                acc_sum += sum(x for x in acc if x >= 0)
+                acc_n += sum(1 for x in acc if x >= 0)
+                log.write(json.dumps({"loop": li, "ms": round(ev[0].elapsed_time(ev[1]), 4), "accepted": acc,
+                                      "emitted": emitted}) + "\n")
         self.loops = loop_index
+        if log is not None:
+            torch.cuda.synchronize()
+            wall = time.perf_counter() - t0
+            log.write(json.dumps({"run": {"tokens": n_new * self.B, "loops": loop_index - loop0,
+                                          "seconds": round(wall, 6), "tokens_per_s": round(n_new * self.B / wall, 3),
+                                          "mean_accepted": round(acc_sum / max(acc_n, 1), 4)}}) + "\n")
+            log.flush()
         return seq

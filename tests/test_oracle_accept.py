@@ -333,3 +333,42 @@ def test_bad_token_and_empty_distribution_flags():
     qz = np.zeros((1, 3), np.float32)
     toks, a, flags = accept.accept_resample_one(np.zeros((0, 3), np.float32), qz, [], np.array([0.3], np.float32))
     assert toks == [0] and flags & accept.FLAG_EMPTY
+
+
+def test_nonfinite_inputs_give_a_defined_outcome():
+    """The library's definition for inputs that are not distributions (the
+    paper assumes valid ones): a NaN or infinite gathered probability, or
+    one in a row the final draw reads, or a target row marked as having
+    non-finite logits, gives a = 0 and token 0 with FLAG_NONFINITE; a NaN in
+    an entry nothing reads changes nothing."""
+    g = np.random.default_rng(5)
+    K, V = 4, 16
+    p = g.dirichlet(np.ones(V), size=K).astype(np.float32)
+    q = g.dirichlet(np.ones(V), size=K + 1).astype(np.float32)
+    drafts = np.array([3, 5, 7, 9])
+    q[0, 3] = 1e-4                             # x~_1 is rejected: the draw reads q_1 and p_1
+    unif = np.array([0.99, 0.99, 0.99, 0.99, 0.4], np.float32)
+    base, a0, f0 = accept.accept_resample_one(p, q, drafts, unif)
+    assert f0 == 0 and a0 == 0
+    for what in ("q_gather_late", "p_gather", "p_row", "q_row", "inf"):
+        pp, qq = p.copy(), q.copy()
+        if what == "q_gather_late":
+            qq[3, 9] = np.nan                  # x~_4's q, read even though the scan stops at x~_1
+        elif what == "p_gather":
+            pp[1, 5] = np.nan
+        elif what == "p_row":
+            pp[0, 0] = np.nan                  # off the draft token, in the row of the residual draw
+        elif what == "q_row":
+            qq[0, 15] = np.nan
+        else:
+            qq[0, 14] = np.inf
+        toks, a, flags = accept.accept_resample_one(pp, qq, drafts, unif)
+        assert toks == [0] and a == 0 and flags & accept.FLAG_NONFINITE, what
+    # an entry nothing reads: q row 3 off its draft token
+    qq = q.copy()
+    qq[3, 0] = np.nan
+    assert accept.accept_resample_one(p, qq, drafts, unif) == (base, a0, f0)
+    bad = np.zeros(K + 1, bool)
+    bad[K] = True
+    toks, a, flags = accept.accept_resample_one(p, q, drafts, unif, bad)
+    assert toks == [0] and a == 0 and flags & accept.FLAG_NONFINITE

@@ -48,3 +48,21 @@ def test_counts_and_ranges():
     assert len(toks) == 20 and all(0 <= t < TGT.vocab for t in toks)
     assert all(0 <= a <= 4 for a in acc)
     assert sum(a + 1 for a in acc) >= 20 > sum(a + 1 for a in acc[:-1])
+
+
+def test_resume_at_a_loop_boundary_equals_one_run():
+    """SpS state at a loop boundary is (tokens, loop index): generating 64
+    tokens in one run equals stopping at the first loop boundary with at
+    least 32 tokens and resuming from prompt + those tokens at the next
+    loop index (Algorithm 2 conditions each loop only on the sequence so
+    far; the uniforms are indexed by the loop)."""
+    ts, tw, ds, dw = models()
+    prompt = synth.tokens(4, 1, 6, TGT.vocab)[0]
+    for K, T in ((3, 1.0), (2, 0.8), (0, 1.0)):
+        full, acc = generate.sps_generate_one(ts, tw, ds, dw, prompt, 64, K, T, seed=9)
+        first, acc1 = generate.sps_generate_one(ts, tw, ds, dw, prompt, 32, K, T, seed=9, truncate=False)
+        assert 32 <= len(first) <= 32 + K
+        rest, acc2 = generate.sps_generate_one(ts, tw, ds, dw, list(prompt) + first, 64 - len(first), K, T,
+                                               seed=9, loop0=len(acc1))
+        assert first + rest == full
+        assert acc1 + acc2 == acc

@@ -111,3 +111,27 @@ def test_softmax_greedy_lowest_index_on_ties():
     z = np.array([[1.0, 3.0, 3.0, 0.0], [-1.0, -1.0, -2.0, -5.0]])
     q = sampling.softmax(z, 0.0)
     assert q.tolist() == [[0, 1, 0, 0], [1, 0, 0, 0]]
+
+
+def test_nonfinite_logit_rows_are_one_hot_at_zero():
+    """Rows with a NaN or +Inf logit, or whose fp32 quotient by T overflows,
+    are one-hot at token 0 (the library's definition); -Inf logits are valid
+    and get probability 0."""
+    z = np.random.default_rng(3).normal(0, 2, (6, 10)).astype(np.float32)
+    z[0, 4] = np.nan
+    z[1, 2] = np.inf
+    z[2, 7] = -np.inf
+    z[3, 1] = 3e38                 # 3e38 / 0.5 overflows fp32
+    for T in (1.0, 0.5, 0.0):
+        bad = sampling.nonfinite_rows(z, T)
+        want_bad = [True, True, False, T == 0.5, False, False]
+        assert list(bad) == want_bad, T
+        out = sampling.softmax(z, T)
+        for r in range(6):
+            if want_bad[r]:
+                assert out[r, 0] == 1.0 and out[r, 1:].sum() == 0.0
+            else:
+                assert np.isfinite(out[r]).all() and abs(out[r].sum() - 1.0) < 1e-12
+        assert out[2, 7] == 0.0
+    ref = torch.softmax(torch.from_numpy(z[4:].astype(np.float64)), dim=-1).numpy()
+    np.testing.assert_allclose(sampling.softmax(z[4:], 1.0), ref, rtol=1e-13)
