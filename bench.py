@@ -172,15 +172,31 @@ def cpu_baseline(shape, K, ctx):
         reps += 1
     dt = (time.perf_counter() - t0) / reps
     nbytes = verify_bytes(one, 1, K, ctx)
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = len(os.sched_getaffinity(0))
+    host = host_info()
+    threads = max([i["num_threads"] or 1 for i in host.get("blas", [])] or [host["affinity_cores"]])
     return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "seconds_per_sample": dt, "repeats": reps,
+            "seconds_per_sample": dt, "repeats": reps, "host": host,
             "sample": "oracle fp64 forward of one full-width %s-shaped block + embedding + unembedding, "
                       "K+1=%d positions, B=1, ctx %d (%.2f GB algorithmic)" % (shape.name, K + 1, ctx, nbytes / 1e9)}
+
+
+def host_info():
+    """The host the CPU oracle runs on: logical CPUs, the cores this process
+    may use, RAM, and the BLAS library numpy calls with its thread count."""
+    host = {"cpu_count": os.cpu_count(), "affinity_cores": len(os.sched_getaffinity(0))}
+    try:
+        host["ram_gb"] = round(os.sysconf("SC_PAGE_SIZE") * os.sysconf("SC_PHYS_PAGES") / 1e9, 1)
+    except (ValueError, OSError):
+        pass
+    try:
+        import numpy  # noqa: F401  (loads the BLAS numpy calls)
+        from threadpoolctl import threadpool_info
+        host["blas"] = [{"api": i.get("internal_api"), "num_threads": i.get("num_threads"),
+                         "library": os.path.basename(i.get("filepath") or "")}
+                        for i in threadpool_info() if i.get("user_api") == "blas"]
+    except Exception:
+        pass
+    return host
 
 
 def _oracle_weights(shape, n_layers, seed):
@@ -227,17 +243,7 @@ def cpu_oracle(args):
     from oracle import model as om
     from paper_2302_01318_amd import configs, synth
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
-    host = {"cpu_count": os.cpu_count(), "affinity_cores": len(os.sched_getaffinity(0))}
-    try:
-        host["ram_gb"] = round(os.sysconf("SC_PAGE_SIZE") * os.sysconf("SC_PHYS_PAGES") / 1e9, 1)
-    except (ValueError, OSError):
-        pass
-    try:
-        from threadpoolctl import threadpool_info
-        host["blas"] = [{k: i.get(k) for k in ("internal_api", "num_threads")} for i in threadpool_info()]
-    except Exception:
-        pass
-    out = {"metric": "oracle CPU time", "host": host}
+    out = {"metric": "oracle CPU time", "host": host_info()}
     # tiny pair end to end
     tgt, drf = configs.TINY_TARGET, configs.TINY_DRAFT
     Wt, Wd = _oracle_weights(tgt, tgt.n_layers, 100), _oracle_weights(drf, drf.n_layers, 101)

@@ -256,7 +256,9 @@ __global__ __launch_bounds__(DH) void attn_combine_kernel(const float* __restric
       acc += w * pr[d];
     }
   }
-  store_act(o, oplane, static_cast<size_t>(row) * H * DH + h * DH + d, L > 0.f ? acc / L : 0.f);
+  // L == 0: no visible position (nothing to average). A NaN among the
+  // scores or values makes L or acc NaN, and the NaN is passed on.
+  store_act(o, oplane, static_cast<size_t>(row) * H * DH + h * DH + d, L == 0.f ? 0.f : acc / L);
 }
 
 

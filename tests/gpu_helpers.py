@@ -40,3 +40,15 @@ def install_prior(shape, kv, ocache, seed, n_prior):
 
 def new_cache(shape, B, T_cap):
     return om.new_cache(spec_of(shape), B, T_cap)
+
+
+def install_oracle_prior(shape, ocache, seed, n_prior):
+    """The oracle half of install_prior (the same random prior keys/values)."""
+    B = len(n_prior)
+    T = max(n_prior)
+    for l in range(shape.n_layers):
+        k, v = synth.kv_prior(shape, seed, l, B, T)
+        for b in range(B):
+            n = int(n_prior[b])
+            ocache["k"][l, b, :, :n] = k[b, :, :n].double().numpy()
+            ocache["v"][l, b, :, :n] = v[b, :, :n].double().numpy()

@@ -19,16 +19,29 @@ from oracle import accept as oacc
 from oracle import model as om
 from oracle import sampling as osamp
 from paper_2302_01318_amd import configs, synth
-from gpu_helpers import build_pair, install_prior, new_cache, round_up
+from gpu_helpers import build_pair, install_oracle_prior, install_prior, new_cache, round_up
 from oracle_helpers import spec_of
 
 pytestmark = pytest.mark.gpu
 
 
-def verify_parity(sps, shape, B, K, n_prior, seed, tol, T=1.0, check_kv=True):
+# Second, tighter bound on the measured logit error, relative to the logit
+# scale (the benchmark spec's tolerance stays the pass criterion; this one catches
+# regressions well below it). Measured: bf16 blocks 5e-5 to 4e-4 at logit
+# std ~0.27; full-width 70B blocks (logit std 1.82) 9.5e-4 at ctx 2048,
+# 4.1e-3 at ctx 8192, 3.6e-3 to 5.0e-3 batched; FP8 70B blocks 1.8e-3 to
+# 8.4e-3 (B = 16, K = 8); fp32 4e-7 to 7e-7.
+TIGHT = {"bf16": 5e-3, "fp8": 8e-3, "f32": 2e-5}
+
+
+def tight_bound(dtype, logit_std):
+    return TIGHT[dtype] * max(1.0, float(logit_std))
+
+
+def verify_parity(sps, shape, B, K, n_prior, seed, tol, T=1.0, check_kv=True, built=None, want_out=None):
     print("verify parity", shape.name, shape.dtype, shape.ffn, "B", B, "K", K, "prior", n_prior, flush=True)
     V = shape.vocab
-    gm, W = build_pair(shape, seed)
+    gm, W = built if built is not None else build_pair(shape, seed)
     T_cap = round_up(max(n_prior) + K + 1, 32)
     kv = sps.KVCache(shape, B, T_cap)
     ocache = new_cache(shape, B, T_cap)
@@ -46,11 +59,16 @@ def verify_parity(sps, shape, B, K, n_prior, seed, tol, T=1.0, check_kv=True):
                     n_accepted=nacc)
     torch.cuda.synchronize()
     assert sps.device_error() == 0
+    if want_out is not None:       # the oracle's inputs, for negative controls
+        want_out.update(toks=toks, n_prior=np.array(n_prior), T_cap=T_cap, seed=seed)
     want = om.forward_cached(spec_of(shape), W, ocache, toks, np.array(n_prior))
     got = logits.cpu().numpy()
     err = np.abs(got - want).max()
-    print("  max |logits - oracle| = %.3g (tol %.1g), logit std %.3g" % (err, tol, want.std()), flush=True)
+    tight = tight_bound(shape.dtype, want.std())
+    print("  max |logits - oracle| = %.3g (tol %.1g, tight %.1g), logit std %.3g" % (err, tol, tight, want.std()),
+          flush=True)
     assert err <= tol
+    assert err <= tight
     qg = q.cpu().numpy()
     np.testing.assert_allclose(qg, osamp.softmax(got.astype(np.float64), T), rtol=2e-5, atol=1e-9)
     w_out, w_n, _ = oacc.accept_resample(p if K else np.zeros((B, 0, V), np.float32), qg, drafts,
@@ -154,11 +172,81 @@ def test_capacity_overflow_is_flagged(sps):
     assert sps.device_error() == 0
 
 
+_BUILT = {}
+
+
+def full_width_layer(shape, seed):
+    """One full-width block of `shape` (weights and oracle copy), kept for
+    the tests that share it; one such model is held at a time."""
+    key = (shape.name, shape.dtype, seed)
+    if key not in _BUILT:
+        _BUILT.clear()
+        _BUILT[key] = build_pair(shape.with_(n_layers=1), seed)
+    return _BUILT[key]
+
+
 @pytest.mark.parametrize("shape", [configs.SEVEN_B, configs.SEVENTY_B], ids=["7b", "70b"])
 def test_full_width_layer(sps, shape):
     """One full-width block + unembedding at K = 4, B = 1 against a 2048-token
     prior context: the per-layer kernels in the benchmark's launch shapes."""
-    verify_parity(sps, shape.with_(n_layers=1), 1, 4, [2048], 21, 2e-2)
+    verify_parity(sps, shape.with_(n_layers=1), 1, 4, [2048], 21, 2e-2, built=full_width_layer(shape, 21))
+
+
+def _planted(kind):
+    """Oracle forward with a plausible kernel mistake planted (CPU): the
+    rotary angle one position late, or the last 32-position block of
+    keys / values each query sees left out."""
+    import contextlib
+
+    @contextlib.contextmanager
+    def ctx():
+        if kind == "rope+1":
+            orig = om.rope
+            om.rope = lambda x, pos, base: orig(x, np.asarray(pos) + 1, base)
+            try:
+                yield
+            finally:
+                om.rope = orig
+        else:
+            orig = om._attend
+
+            def drop_last_block(q, Kc, Vc, scale):
+                last = (len(Kc) - 1) // 32 * 32
+                return orig(q, Kc[:last], Vc[:last], scale) if last > 0 else orig(q, Kc, Vc, scale)
+            om._attend = drop_last_block
+            try:
+                yield
+            finally:
+                om._attend = orig
+    return ctx()
+
+
+def test_full_width_layer_negative_controls(sps):
+    """The parity check bites: the 70B block's GPU logits (ctx 2048, K = 4)
+    fail the 2e-2 tolerance against the oracle with a rotary angle one
+    position late, and with the last 32-position KV block left out."""
+    shape = configs.SEVENTY_B.with_(n_layers=1)
+    built = full_width_layer(configs.SEVENTY_B, 21)
+    inp = {}
+    got = verify_parity(sps, shape, 1, 4, [2048], 21, 2e-2, built=built, want_out=inp)
+    _, W = built
+    for kind in ("rope+1", "drop last block"):
+        ocache = new_cache(shape, 1, inp["T_cap"])
+        install_oracle_prior(shape, ocache, inp["seed"] + 1, list(inp["n_prior"]))
+        with _planted(kind):
+            bad = om.forward_cached(spec_of(shape), W, ocache, inp["toks"], inp["n_prior"])
+        err = np.abs(got - bad).max()
+        print("  planted %s: max |GPU logits - planted oracle| = %.3g" % (kind, err), flush=True)
+        assert err > 10 * 2e-2
+
+
+@pytest.mark.parametrize("B,priors", [(1, [8192]), (4, [8192, 8001, 7777, 8190])], ids=["B1", "B4"])
+def test_full_width_layer_ctx8192(sps, B, priors):
+    """The 70B block at the sweep's long context (ctx 8192, K = 4): 33
+    attention partials per head in the combine, rotary angles and KV tile
+    offsets past position 8000, ragged lengths at B = 4."""
+    verify_parity(sps, configs.SEVENTY_B.with_(n_layers=1), B, 4, priors, 21, 2e-2,
+                  built=full_width_layer(configs.SEVENTY_B, 21), check_kv=B == 1)
 
 
 @pytest.mark.parametrize("shape,B,K", [(configs.SEVENTY_B, 4, 4), (configs.SEVENTY_B, 16, 8),
@@ -198,3 +286,61 @@ def test_max_lookahead(sps):
     """K = 63, the largest lookahead: 64 positions of one sequence (8 M tiles,
     4 query tiles in attention)."""
     verify_parity(sps, SMALL, 1, 63, [100], 163, 2e-2)
+
+
+@pytest.mark.parametrize("B,T", [(1, 1.0), (2, 0.8)])
+def test_draft_step_full_width(sps, B, T):
+    """The 70B draft's shape (d_model 3072, 24 heads of 128, GELU FFN 12288,
+    vocab 32000, bf16) in the launch shapes the end-to-end runs use, with
+    two layers (the per-layer kernels do not depend on the layer count): a
+    K = 4 draft step against a 2048-token prior (ragged at B = 2). Per step,
+    the oracle's forward of the same tokens gives the draft distribution
+    p_t = softmax(logits / T), which the exported p rows match within the
+    bf16 logit tolerance (as log-probabilities); each drawn token equals the
+    oracle's integer inverse-CDF draw from the GPU's own p row (bit-exact);
+    the appended keys and values match the oracle cache."""
+    from oracle import philox as ophil
+    shape = configs.DRAFT_70B.with_(n_layers=2)
+    K, V, tol = 4, shape.vocab, 2e-2
+    n_prior = [2048, 1500][:B]
+    print("draft step full width B", B, "T", T, flush=True)
+    gm, W = build_pair(shape, 51)
+    T_cap = round_up(max(n_prior) + K + 1, 32)
+    kv = sps.KVCache(shape, B, T_cap)
+    ocache = new_cache(shape, B, T_cap)
+    install_prior(shape, kv, ocache, 52, n_prior)
+    ctx = synth.tokens(53, B, 2, V)
+    ws = sps.workspace(shape, B, 2, T_cap)
+    tokens = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+    p_out = torch.empty((B, K, V), dtype=torch.float32, device="cuda")
+    seed, loop = 54, 3
+    sps.draft_step(gm, kv, torch.from_numpy(ctx).cuda(), K, T, (seed, loop), tokens, p_out, ws)
+    torch.cuda.synchronize()
+    assert sps.device_error() == 0
+    got_t, got_p = tokens.cpu().numpy(), p_out.cpu().numpy()
+    np.testing.assert_array_equal(got_t[:, 0], ctx[:, 1])
+    ud = ophil.uniforms(seed, loop, ophil.PURPOSE_DRAFT, B, K)
+    lens = np.array(n_prior)
+    spec = spec_of(shape)
+    worst = 0.0
+    for t in range(K):
+        if t == 0:   # the last committed token and the newest one, at positions len - 1 and len
+            lg = om.forward_cached(spec, W, ocache, ctx, lens - 1)[:, -1]
+        else:
+            lg = om.forward_cached(spec, W, ocache, got_t[:, t:t + 1], lens + t)[:, 0]
+        want_p = osamp.softmax(lg, T)
+        for b in range(B):
+            keep = want_p[b] > 1e-30
+            dlog = np.log(got_p[b, t, keep].astype(np.float64)) - np.log(want_p[b, keep])
+            worst = max(worst, np.abs(dlog).max())
+            y, ok = osamp.categorical(osamp.to_weights(got_p[b, t]), ud[b, t])
+            assert ok and got_t[b, t + 1] == y, (b, t)
+    print("  max |log p - log p_oracle| = %.3g (tol %.2g)" % (worst, 2 * tol / T), flush=True)
+    assert worst <= 2 * tol / T and worst <= tol / T
+    for l in range(shape.n_layers):
+        for b in range(B):
+            k, v = kv.read(l, b, n_prior[b] - 1, K + 1)
+            np.testing.assert_allclose(k.float().cpu().numpy(),
+                                       ocache["k"][l, b, :, n_prior[b] - 1:n_prior[b] + K], atol=tol, rtol=tol)
+            np.testing.assert_allclose(v.float().cpu().numpy(),
+                                       ocache["v"][l, b, :, n_prior[b] - 1:n_prior[b] + K], atol=tol, rtol=tol)

@@ -66,3 +66,30 @@ def test_resume_at_a_loop_boundary_equals_one_run():
                                                seed=9, loop0=len(acc1))
         assert first + rest == full
         assert acc1 + acc2 == acc
+
+
+def test_trace_margins_flag_near_boundary_decisions():
+    """The explained-divergence check of the GPU end-to-end tests: every
+    loop's smallest decision margin is computed from the oracle's own trace;
+    a loop whose final uniform is moved onto a bucket edge has margin ~0."""
+    import sys
+    import os
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    from test_gpu_e2e import loop_margin
+    ts, tw, ds, dw = models()
+    prompt = synth.tokens(5, 1, 6, TGT.vocab)[0]
+    trace = []
+    generate.sps_generate_one(ts, tw, ds, dw, prompt, 12, 3, 1.0, seed=2, trace=trace)
+    margins = [loop_margin(r) for r in trace]
+    assert all(0 <= m <= 1 for m in margins) and min(margins) > 1e-7
+    rec = dict(trace[0])
+    # put the final draw's threshold exactly on a bucket edge
+    from oracle import sampling
+    w = sampling.to_weights(rec["q"][rec["a"]]) if rec["a"] == len(rec["drafts"]) else None
+    if w is not None:
+        W = int(w.sum())
+        edge = int(w[0])
+        m = -(-(edge << 24) // W)        # smallest grid index whose threshold reaches the first edge
+        rec["unif"] = rec["unif"].copy()
+        rec["unif"][-1] = np.float32(m / float(1 << 24))
+        assert loop_margin(rec) < 1e-6
