@@ -196,10 +196,28 @@ __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, 
 }
 
 // Scratch of row_cutoff (LDS).
+// Buckets of the cut-off's first pass: weight 0, then for w >= 1 the
+// position e (0..32) of its leading one bit and the next 4 bits. The bucket
+// is monotone in w, so the buckets split the ranking into contiguous key
+// ranges (~6 % of a weight wide).
+constexpr int kCutBuckets = 1 + 33 * 16;
+constexpr int kCutCand = 1024;            // keys of one bucket resolved exactly
+
+__device__ __forceinline__ int cut_bucket(uint64_t w) {
+  if (w == 0) return 0;
+  const int e = 63 - __clzll(static_cast<long long>(w));
+  const int m = e >= 4 ? static_cast<int>((w >> (e - 4)) & 15) : static_cast<int>((w << (4 - e)) & 15);
+  return 1 + e * 16 + m;
+}
+
 struct CutScratch {
   uint64_t hist[256];
   uint64_t prefix, need;
   uint64_t wsum[16];
+  uint64_t bins[kCutBuckets];
+  uint64_t cand[kCutCand];
+  uint64_t above;
+  int nb, ncand;
 };
 
 // The row's draw weights for the cut-off, in LDS (dynamic shared memory of
@@ -289,6 +307,104 @@ __device__ __forceinline__ uint64_t radix_select(const RowKeys& rk, uint64_t lo,
   return P;
 }
 
+// The same select in two passes where it can: a histogram of the keys >=
+// lo over kCutBuckets weight buckets (counts, or WEIGHTED the weights) finds
+// the bucket holding the answer and what the buckets above it hold; the
+// keys of that bucket are gathered (at most kCutCand) and every candidate
+// counts (sums) the candidates above it, so exactly one sees the total
+// reach `need` at itself. Returns false, leaving the answer to the radix
+// passes, when the bucket holds more than kCutCand keys (a flat or nearly
+// flat run of weights).
+template <bool WEIGHTED>
+__device__ __forceinline__ bool bucket_select(const RowKeys& rk, uint64_t lo, uint64_t need, CutScratch& sc,
+                                              uint64_t* out) {
+  const int tid = threadIdx.x, bd = blockDim.x;
+  for (int b = tid; b < kCutBuckets; b += bd) sc.bins[b] = 0;
+  if (tid == 0) sc.ncand = 0;
+  __syncthreads();
+  // Consecutive entries of a thread that fall in one bucket add once (a flat
+  // row: one atomic per thread instead of one per entry).
+  int cur = -1;
+  uint64_t run = 0;
+  for (int i = tid; i < rk.V; i += bd) {
+    const uint64_t key = rk.key(i);
+    if (key < lo) continue;
+    const uint64_t w = key >> 24;
+    const int b = cut_bucket(w);
+    const uint64_t v = WEIGHTED ? w : 1;
+    if (b != cur) {
+      if (run) atomicAdd(reinterpret_cast<unsigned long long*>(&sc.bins[cur]), run);
+      cur = b;
+      run = 0;
+    }
+    run += v;
+  }
+  if (run) atomicAdd(reinterpret_cast<unsigned long long*>(&sc.bins[cur]), run);
+  __syncthreads();
+  if (tid < 64) {
+    // Lane l owns kPer buckets from the top; the first lane whose inclusive
+    // total reaches `need` walks its buckets.
+    constexpr int kPer = (kCutBuckets + 63) / 64;
+    uint64_t h[kPer], tot = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int b = kCutBuckets - 1 - (tid * kPer + j);
+      h[j] = b >= 0 ? sc.bins[b] : 0;
+      tot += h[j];
+    }
+    const uint64_t inc = wave_incl_scan_u64(tot);
+    const uint64_t hit = __ballot(inc >= need);
+    if (tid == __ffsll(static_cast<long long>(hit)) - 1) {
+      uint64_t c = inc - tot;
+      int jb = kPer - 1;
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        if (c + h[j] >= need) {
+          jb = j;
+          break;
+        }
+        c += h[j];
+      }
+      sc.nb = kCutBuckets - 1 - (tid * kPer + jb);
+      sc.above = c;
+    }
+  }
+  __syncthreads();
+  const int nb = sc.nb;
+  const uint64_t above = sc.above;
+  for (int i = tid; i < rk.V; i += bd) {
+    const uint64_t key = rk.key(i);
+    if (key >= lo && cut_bucket(key >> 24) == nb) {
+      const int slot = atomicAdd(&sc.ncand, 1);
+      if (slot < kCutCand) sc.cand[slot] = key;
+    }
+  }
+  __syncthreads();
+  const int n = sc.ncand;
+  if (n > kCutCand) return false;          // uniform over the block
+  for (int t = tid; t < n; t += bd) {
+    const uint64_t k = sc.cand[t];
+    uint64_t sum = 0;
+    for (int u = 0; u < n; ++u) {
+      const uint64_t ku = sc.cand[u];
+      sum += ku > k ? (WEIGHTED ? ku >> 24 : 1) : 0;
+    }
+    const uint64_t v = WEIGHTED ? k >> 24 : 1;
+    if (above + sum < need && above + sum + v >= need) sc.prefix = k;   // exactly one candidate
+  }
+  __syncthreads();
+  *out = sc.prefix;
+  __syncthreads();                         // sc reusable by the next select
+  return true;
+}
+
+template <bool WEIGHTED>
+__device__ __forceinline__ uint64_t cut_select(const RowKeys& rk, uint64_t lo, uint64_t need, CutScratch& sc) {
+  uint64_t key;
+  if (bucket_select<WEIGHTED>(rk, lo, need, sc, &key)) return key;
+  return radix_select<WEIGHTED>(rk, lo, need, sc);
+}
+
 // LDS bytes row_cutoff needs for a row of V entries.
 __host__ __device__ __forceinline__ size_t cutoff_lds_bytes(int V) {
   return (static_cast<size_t>(V) + (V + 31) / 32) * sizeof(uint32_t);
@@ -324,10 +440,10 @@ __device__ __forceinline__ void row_cutoff(PF pf, int V, int top_k, float top_p,
   }
   __syncthreads();
   uint64_t tau = 1;
-  if (top_k >= 1 && top_k < V) tau = radix_select<false>(rk, 1, static_cast<uint64_t>(top_k), sc);
+  if (top_k >= 1 && top_k < V) tau = cut_select<false>(rk, 1, static_cast<uint64_t>(top_k), sc);
   if (top_p < 1.f) {
     const uint64_t target = grid_threshold(top_p, kept_weight(rk, tau, sc));
-    const uint64_t tp = target == 0 ? radix_select<false>(rk, tau, 1, sc) : radix_select<true>(rk, tau, target, sc);
+    const uint64_t tp = target == 0 ? cut_select<false>(rk, tau, 1, sc) : cut_select<true>(rk, tau, target, sc);
     tau = tp > tau ? tp : tau;
   }
   const uint64_t S = kept_weight(rk, tau, sc);
@@ -577,9 +693,10 @@ __global__ __launch_bounds__(kSampleThreads) void accept_kernel(QS qs, const flo
     }
     if (tid <= K) nf |= qs.row(b * (K + 1) + tid).nonfinite();
     const uint64_t rej = __ballot(rejected);
+    const bool any_nf = __ballot(nf) != 0;          // wave-wide, outside any branch
     const int a = rej ? __ffsll(static_cast<long long>(rej)) - 1 : K;
     if (tid == a && bad) atomicOr(err, kErrBadToken);
-    if (tid == 0) { s_a = a; s_y = 0; s_nf = __ballot(nf) != 0; }
+    if (tid == 0) { s_a = a; s_y = 0; s_nf = any_nf; }
   }
   __syncthreads();
   int a = s_a;
