@@ -240,6 +240,24 @@ sps_status sps_verify_step(sps_model_t target, sps_kv_t kv, const int32_t* token
                            const sps_accept_io* acc, void* workspace, size_t ws_bytes,
                            void* stream);
 
+/* sps_verify_step without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). The library keeps the scratch in a
+ * device array of 64 MiB per device, reserved when the library's code is
+ * loaded on that device and held until the process ends; the call itself
+ * allocates nothing. Calls whose workspace (sps_workspace_bytes(cfg, B,
+ * K + 1, T_cap)) exceeds 64 MiB return SPS_E_CAPACITY and touch nothing
+ * (the 70B shape at B = 1, K = 4 fits caches of up to 24k positions, B = 4
+ * at 2k). Every
+ * call on a device shares that device's array: calls that overlap on one
+ * device (on concurrent streams, or from several threads) race, and must
+ * be serialised by the caller. Same arguments, outputs and errors as
+ * sps_verify_step otherwise; no contents of the array carry over between
+ * calls. */
+sps_status sps_verify_step_noalloc(sps_model_t target, sps_kv_t kv, const int32_t* tokens, int32_t B,
+                                   int32_t K, sps_sampling sampling, float* logits_out, float* q_out,
+                                   const sps_accept_io* acc, void* stream);
+
 /* Modified rejection sampling on given distributions (Algorithm 2, accept
  * loop and final draw; Theorem 1). For each sequence, left to right, draft
  * x~_t = draft_tokens[b][t-1] is accepted iff r_t * p_t(x~_t) < q_t(x~_t),

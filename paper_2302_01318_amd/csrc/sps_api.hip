@@ -13,6 +13,13 @@
 // Sticky device error bits (SPS_DEV_*), one copy per device.
 __device__ int sps_dev_err;
 
+// Workspace of sps_verify_step_noalloc: a file-scope device array, one copy
+// per device, held until the process ends. Host code reaches it only through
+// the device address hipGetSymbolAddress returns (the array's name in host
+// code is a host-side stand-in, not a device address).
+constexpr size_t kNoAllocScratchBytes = static_cast<size_t>(64) << 20;
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 namespace {
 
 using sps::GemmParams;
@@ -40,6 +47,20 @@ int* device_error_ptr() {
 }
 
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+// Device address of this device's `scratch`, looked up once per device (with
+// that device current) on its first use.
+char* scratch_ptr() {
+  static char* ptrs[64] = {nullptr};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  if (!ptrs[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+    ptrs[dev] = static_cast<char*>(p);
+  }
+  return ptrs[dev];
+}
 
 }  // namespace
 
@@ -435,21 +456,25 @@ sps_status sps_forward(sps_model_t model, sps_kv_t kv, const int32_t* tokens, in
                       ws, err, as_stream(stream));
 }
 
-sps_status sps_verify_step(sps_model_t target, sps_kv_t kv, const int32_t* tokens, int32_t B, int32_t K,
-                           sps_sampling sampling, float* logits_out, float* q_out, const sps_accept_io* acc,
-                           void* workspace, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// The verify step on a workspace `base` of ws_bytes bytes (validated here).
+sps_status verify_impl(sps_model_t target, sps_kv_t kv, const int32_t* tokens, int32_t B, int32_t K,
+                       sps_sampling sampling, float* logits_out, float* q_out, const sps_accept_io* acc,
+                       char* base, size_t ws_bytes, void* stream) {
   if (K < 0 || K > kMaxK) return SPS_E_INVALID;
   if (!target) return SPS_E_INVALID;
   sps_status s = check_sampling(sampling, target->cfg.vocab);
   if (s != SPS_OK) return s;
   WsLayout ws;
-  s = check_forward_args(target, kv, B, K + 1, ws_bytes, workspace, &ws);
+  s = check_forward_args(target, kv, B, K + 1, ws_bytes, base, &ws);
   if (s != SPS_OK) return s;
   if (!tokens) return SPS_E_INVALID;
   if (acc && (!acc->out_tokens || !acc->n_accepted || (K > 0 && !acc->p_draft))) return SPS_E_INVALID;
   int* err = device_error_ptr();
   if (!err) return SPS_E_HIP;
-  char* base = static_cast<char*>(workspace);
   float* logits = logits_out ? logits_out : reinterpret_cast<float*>(base + ws.logits);
   void* stats = base + ws.stats;
   const hipStream_t st = as_stream(stream);
@@ -463,6 +488,30 @@ sps_status sps_verify_step(sps_model_t target, sps_kv_t kv, const int32_t* token
                                       acc->rng.seed, acc->rng.loop, B, K, V, acc->out_tokens, acc->n_accepted, err,
                                       st));
   return SPS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sps_status sps_verify_step(sps_model_t target, sps_kv_t kv, const int32_t* tokens, int32_t B, int32_t K,
+                           sps_sampling sampling, float* logits_out, float* q_out, const sps_accept_io* acc,
+                           void* workspace, size_t ws_bytes, void* stream) {
+  return verify_impl(target, kv, tokens, B, K, sampling, logits_out, q_out, acc, static_cast<char*>(workspace),
+                     ws_bytes, stream);
+}
+
+sps_status sps_verify_step_noalloc(sps_model_t target, sps_kv_t kv, const int32_t* tokens, int32_t B, int32_t K,
+                                   sps_sampling sampling, float* logits_out, float* q_out, const sps_accept_io* acc,
+                                   void* stream) {
+  // The size check comes first, so a call past the limit touches nothing.
+  if (!target || !kv || B < 1 || K < 0 || K > kMaxK) return SPS_E_INVALID;
+  if (K + 1 > kMaxTokensPerSeq || B * (K + 1) > kMaxRows) return SPS_E_SHAPE;
+  if (make_ws(target->L, B, K + 1, kv->T_cap).total > kNoAllocScratchBytes) return SPS_E_CAPACITY;
+  char* base = scratch_ptr();
+  if (!base) return SPS_E_HIP;
+  return verify_impl(target, kv, tokens, B, K, sampling, logits_out, q_out, acc, base, kNoAllocScratchBytes,
+                     stream);
 }
 
 sps_status sps_accept_resample(const float* p_draft, const float* q_target, const int32_t* draft_tokens,

@@ -78,6 +78,7 @@ _sig("sps_workspace_bytes", c_size_t, [ctypes.POINTER(Config), c_int32, c_int32,
 _sig("sps_forward", c_int32, [P, P, P, c_int32, c_int32, c_int32, c_int32, P, P, c_size_t, P])
 _sig("sps_verify_step", c_int32, [P, P, P, c_int32, c_int32, Sampling, P, P, ctypes.POINTER(AcceptIO), P,
                                   c_size_t, P])
+_sig("sps_verify_step_noalloc", c_int32, [P, P, P, c_int32, c_int32, Sampling, P, P, ctypes.POINTER(AcceptIO), P])
 _sig("sps_accept_resample", c_int32, [P, P, P, P, Philox, c_int32, c_int32, c_int32, P, P, P])
 _sig("sps_draft_step", c_int32, [P, P, P, c_int32, c_int32, Sampling, Philox, P, P, P, c_size_t, P])
 _sig("sps_commit", c_int32, [P, P, P, P, c_int32, c_int32, P, P, P, c_int32, P])
@@ -97,7 +98,7 @@ EXPORTS = ["sps_status_string", "sps_abi_version", "sps_weight_bytes", "sps_pack
            "sps_kv_write", "sps_kv_read", "sps_workspace_bytes", "sps_forward", "sps_verify_step",
            "sps_accept_resample", "sps_draft_step", "sps_commit", "sps_philox_uniforms", "sps_softmax",
            "sps_device_error", "sps_profile_gemm_begin", "sps_profile_gemm_end",
-           "sps_stream_read", "sps_fp8_decode", "sps_weight_slot"]
+           "sps_stream_read", "sps_fp8_decode", "sps_weight_slot", "sps_verify_step_noalloc"]
 
 
 class SPSError(RuntimeError):
@@ -234,6 +235,20 @@ def verify_step(model, kv, tokens, K, temperature, ws, logits=None, q=None, p_dr
                               sampling_of(temperature, top_k, top_p), _ptr(logits, torch.float32, "logits"),
                               _ptr(q, torch.float32, "q"), ctypes.byref(acc) if acc else None, _ptr(ws),
                               ws.numel(), _stream()), "sps_verify_step")
+
+
+def verify_step_noalloc(model, kv, tokens, K, temperature, logits=None, q=None, p_draft=None, uniforms=None,
+                        rng=(0, 0), out_tokens=None, n_accepted=None, top_k=0, top_p=1.0):
+    """verify_step with the library's own scratch (no workspace argument)."""
+    acc = None
+    if out_tokens is not None:
+        acc = AcceptIO(_ptr(p_draft, torch.float32, "p_draft"), _ptr(uniforms, torch.float32, "uniforms"),
+                       Philox(*rng), _ptr(out_tokens, torch.int32, "out_tokens"),
+                       _ptr(n_accepted, torch.int32, "n_accepted"))
+    check(lib.sps_verify_step_noalloc(model.handle, kv.handle, _ptr(tokens, torch.int32, "tokens"), kv.B, K,
+                                      sampling_of(temperature, top_k, top_p), _ptr(logits, torch.float32, "logits"),
+                                      _ptr(q, torch.float32, "q"), ctypes.byref(acc) if acc else None, _stream()),
+          "sps_verify_step_noalloc")
 
 
 def accept_resample(p_draft, q_target, draft_tokens, uniforms=None, rng=(0, 0), out_tokens=None,
