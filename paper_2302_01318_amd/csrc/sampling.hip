@@ -25,6 +25,11 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
   const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), o);
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
+  const uint32_t lo = __shfl(static_cast<uint32_t>(v), src);
+  const uint32_t hi = __shfl(static_cast<uint32_t>(v >> 32), src);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += shfl_xor_u64(v, o);
@@ -42,11 +47,16 @@ __device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
 
 // Branch-free (selects only), so that loops over a row keep their loads in
 // flight together: floor(x 2^32) for x in (0, 1), 2^32 for x >= 1, 0 for
-// x <= 0 or NaN.
+// x <= 0 or NaN. Integer arithmetic on the fp32 encoding: for 0 < x < 1
+// with biased exponent e and 24-bit significand m (no implicit one when
+// e = 0), x 2^32 = m 2^(e - 118), so the floor is a shift of m.
 __device__ __forceinline__ uint64_t fixed_weight(float x) {
-  const double d = x > 0.f ? fmin(static_cast<double>(x), 1.0) : 0.0;
-  const double f = fmin(d * 4294967296.0, 4294967295.0);        // d = 1 adds the missing unit below
-  return static_cast<uint64_t>(static_cast<uint32_t>(f)) + (d >= 1.0 ? 1u : 0u);
+  const uint32_t b = __float_as_uint(x);
+  const int e = static_cast<int>((b >> 23) & 0xFF);
+  const uint32_t m = (b & 0x7FFFFFu) | (e ? 0x800000u : 0u);
+  const int sh = e - 118;                                      // <= 8 for x < 1
+  const uint64_t w = sh >= 0 ? static_cast<uint64_t>(m << (sh & 31)) : sh > -32 ? m >> (-sh & 31) : 0u;
+  return x >= 1.f ? (1ull << 32) : x > 0.f ? w : 0u;
 }
 
 __device__ __forceinline__ uint64_t grid_threshold(float u, uint64_t W) {
@@ -214,10 +224,11 @@ struct CutScratch {
   uint64_t hist[256];
   uint64_t prefix, need;
   uint64_t wsum[16];
-  uint64_t bins[kCutBuckets];
+  uint64_t bins[kCutBuckets];       // per bucket: count of keys
+  uint64_t wbins[kCutBuckets];      // per bucket: their weight
   uint64_t cand[kCutCand];
-  uint64_t above;
-  int nb, ncand;
+  uint64_t above, above_w;
+  int nb, ncand, weighted;
 };
 
 // The row's draw weights for the cut-off, in LDS (dynamic shared memory of
@@ -307,71 +318,97 @@ __device__ __forceinline__ uint64_t radix_select(const RowKeys& rk, uint64_t lo,
   return P;
 }
 
-// The same select in two passes where it can: a histogram of the keys >=
-// lo over kCutBuckets weight buckets (counts, or WEIGHTED the weights) finds
-// the bucket holding the answer and what the buckets above it hold; the
-// keys of that bucket are gathered (at most kCutCand) and every candidate
-// counts (sums) the candidates above it, so exactly one sees the total
-// reach `need` at itself. Returns false, leaving the answer to the radix
-// passes, when the bucket holds more than kCutCand keys (a flat or nearly
-// flat run of weights).
-template <bool WEIGHTED>
-__device__ __forceinline__ bool bucket_select(const RowKeys& rk, uint64_t lo, uint64_t need, CutScratch& sc,
-                                              uint64_t* out) {
+// The select in two passes where it can. One pass histograms the keys >= lo
+// over kCutBuckets weight buckets, counting them and summing their weights.
+// The target is `need` keys counted from the top, or (NUCLEUS) a weight:
+// floor(floor(top_p 2^24) W / 2^24) of the histogram's total W, the nucleus
+// threshold on what keys >= lo hold (when that is 0, the one top key). One
+// wave finds the bucket where the total from the top reaches the target and
+// what the buckets above it hold; the keys of that bucket are gathered (at
+// most kCutCand) and every candidate counts (sums) the candidates above it,
+// so exactly one sees the total reach the target at itself: that key is tau.
+// *kept = the weight of the keys >= tau. Returns false, leaving the answer to
+// the radix passes, when the bucket holds more than kCutCand keys (a flat or
+// nearly flat run of weights).
+template <bool NUCLEUS>
+__device__ __forceinline__ bool bucket_select(const RowKeys& rk, uint64_t lo, uint64_t need, float top_p,
+                                              CutScratch& sc, uint64_t* tau, uint64_t* kept) {
   const int tid = threadIdx.x, bd = blockDim.x;
-  for (int b = tid; b < kCutBuckets; b += bd) sc.bins[b] = 0;
+  for (int b = tid; b < kCutBuckets; b += bd) {
+    sc.bins[b] = 0;
+    sc.wbins[b] = 0;
+  }
   if (tid == 0) sc.ncand = 0;
   __syncthreads();
   // Consecutive entries of a thread that fall in one bucket add once (a flat
-  // row: one atomic per thread instead of one per entry).
+  // row: two atomics per thread instead of two per entry).
   int cur = -1;
-  uint64_t run = 0;
+  uint64_t rc = 0, rw = 0;
   for (int i = tid; i < rk.V; i += bd) {
     const uint64_t key = rk.key(i);
     if (key < lo) continue;
     const uint64_t w = key >> 24;
     const int b = cut_bucket(w);
-    const uint64_t v = WEIGHTED ? w : 1;
     if (b != cur) {
-      if (run) atomicAdd(reinterpret_cast<unsigned long long*>(&sc.bins[cur]), run);
+      if (rc) atomicAdd(reinterpret_cast<unsigned long long*>(&sc.bins[cur]), rc);
+      if (rw) atomicAdd(reinterpret_cast<unsigned long long*>(&sc.wbins[cur]), rw);
       cur = b;
-      run = 0;
+      rc = rw = 0;
     }
-    run += v;
+    rc += 1;
+    rw += w;
   }
-  if (run) atomicAdd(reinterpret_cast<unsigned long long*>(&sc.bins[cur]), run);
+  if (rc) atomicAdd(reinterpret_cast<unsigned long long*>(&sc.bins[cur]), rc);
+  if (rw) atomicAdd(reinterpret_cast<unsigned long long*>(&sc.wbins[cur]), rw);
   __syncthreads();
+  bool weighted = false;
   if (tid < 64) {
     // Lane l owns kPer buckets from the top; the first lane whose inclusive
-    // total reaches `need` walks its buckets.
+    // total reaches the target walks its buckets.
     constexpr int kPer = (kCutBuckets + 63) / 64;
-    uint64_t h[kPer], tot = 0;
+    uint64_t hc[kPer], hw[kPer], tc = 0, tw = 0;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const int b = kCutBuckets - 1 - (tid * kPer + j);
-      h[j] = b >= 0 ? sc.bins[b] : 0;
-      tot += h[j];
+      hc[j] = b >= 0 ? sc.bins[b] : 0;
+      hw[j] = b >= 0 ? sc.wbins[b] : 0;
+      tc += hc[j];
+      tw += hw[j];
     }
-    const uint64_t inc = wave_incl_scan_u64(tot);
+    const uint64_t ic = wave_incl_scan_u64(tc), iw = wave_incl_scan_u64(tw);
+    if (NUCLEUS) {
+      const uint64_t W = shfl_u64(iw, 63);
+      const uint64_t target = grid_threshold(top_p, W);
+      weighted = target != 0;
+      need = weighted ? target : 1;
+    }
+    const uint64_t inc = weighted ? iw : ic;
     const uint64_t hit = __ballot(inc >= need);
     if (tid == __ffsll(static_cast<long long>(hit)) - 1) {
-      uint64_t c = inc - tot;
+      uint64_t c = inc - (weighted ? tw : tc), cw = iw - tw;
       int jb = kPer - 1;
 #pragma unroll
       for (int j = 0; j < kPer; ++j) {
-        if (c + h[j] >= need) {
+        const uint64_t h = weighted ? hw[j] : hc[j];
+        if (c + h >= need) {
           jb = j;
           break;
         }
-        c += h[j];
+        c += h;
+        cw += hw[j];
       }
       sc.nb = kCutBuckets - 1 - (tid * kPer + jb);
       sc.above = c;
+      sc.above_w = cw;
+      sc.need = need;
+      sc.weighted = weighted;                  // which total the candidates count
     }
   }
   __syncthreads();
   const int nb = sc.nb;
   const uint64_t above = sc.above;
+  need = sc.need;
+  weighted = sc.weighted != 0;
   for (int i = tid; i < rk.V; i += bd) {
     const uint64_t key = rk.key(i);
     if (key >= lo && cut_bucket(key >> 24) == nb) {
@@ -387,22 +424,24 @@ __device__ __forceinline__ bool bucket_select(const RowKeys& rk, uint64_t lo, ui
     uint64_t sum = 0;
     for (int u = 0; u < n; ++u) {
       const uint64_t ku = sc.cand[u];
-      sum += ku > k ? (WEIGHTED ? ku >> 24 : 1) : 0;
+      sum += ku > k ? (weighted ? ku >> 24 : 1) : 0;
     }
-    const uint64_t v = WEIGHTED ? k >> 24 : 1;
+    const uint64_t v = weighted ? k >> 24 : 1;
     if (above + sum < need && above + sum + v >= need) sc.prefix = k;   // exactly one candidate
   }
   __syncthreads();
-  *out = sc.prefix;
+  const uint64_t t_key = sc.prefix;
+  uint64_t w = 0;
+  for (int t = tid; t < n; t += bd) w += sc.cand[t] >= t_key ? sc.cand[t] >> 24 : 0;
+  w = wave_sum_u64(w);
+  if ((tid & 63) == 0) sc.wsum[tid >> 6] = w;
+  __syncthreads();
+  uint64_t s = sc.above_w;
+  for (int v = 0; v < static_cast<int>(bd >> 6); ++v) s += sc.wsum[v];
+  *tau = t_key;
+  *kept = s;
   __syncthreads();                         // sc reusable by the next select
   return true;
-}
-
-template <bool WEIGHTED>
-__device__ __forceinline__ uint64_t cut_select(const RowKeys& rk, uint64_t lo, uint64_t need, CutScratch& sc) {
-  uint64_t key;
-  if (bucket_select<WEIGHTED>(rk, lo, need, sc, &key)) return key;
-  return radix_select<WEIGHTED>(rk, lo, need, sc);
 }
 
 // LDS bytes row_cutoff needs for a row of V entries.
@@ -439,14 +478,24 @@ __device__ __forceinline__ void row_cutoff(PF pf, int V, int top_k, float top_p,
     }
   }
   __syncthreads();
-  uint64_t tau = 1;
-  if (top_k >= 1 && top_k < V) tau = cut_select<false>(rk, 1, static_cast<uint64_t>(top_k), sc);
+  // Top-k, then nucleus among what top-k kept; each select also gives the
+  // weight kept at its key (the radix fallback sums it in one more pass).
+  uint64_t tau = 1, S = 0;
+  bool have_s = false;
+  if (top_k >= 1 && top_k < V) {
+    have_s = bucket_select<false>(rk, 1, static_cast<uint64_t>(top_k), 1.f, sc, &tau, &S);
+    if (!have_s) tau = radix_select<false>(rk, 1, static_cast<uint64_t>(top_k), sc);
+  }
   if (top_p < 1.f) {
-    const uint64_t target = grid_threshold(top_p, kept_weight(rk, tau, sc));
-    const uint64_t tp = target == 0 ? cut_select<false>(rk, tau, 1, sc) : cut_select<true>(rk, tau, target, sc);
+    uint64_t tp;
+    have_s = bucket_select<true>(rk, tau, 0, top_p, sc, &tp, &S);
+    if (!have_s) {
+      const uint64_t target = grid_threshold(top_p, kept_weight(rk, tau, sc));
+      tp = target == 0 ? radix_select<false>(rk, tau, 1, sc) : radix_select<true>(rk, tau, target, sc);
+    }
     tau = tp > tau ? tp : tau;
   }
-  const uint64_t S = kept_weight(rk, tau, sc);
+  if (!have_s) S = kept_weight(rk, tau, sc);
   st.tau = tau;
   st.s = S == 0 ? 0.f : __ull2float_rn(S) * 2.3283064365386963e-10f;   // * 2^-32, exact
 }
