@@ -83,6 +83,100 @@ def measured_mfma(weights="bf16"):
     return {k: t[k] for k in ("mfma_busy_pct", "mfma_executed_tflops", "useful_tflops") if k in t}
 
 
+def measured_trace(weights="bf16"):
+    """Average GEMM launch duration from a rocprofv3 kernel trace of the
+    benchmark (see the profiles/ file), if taken on the current GEMM source."""
+    try:
+        with open(_profile_file("trace", weights)) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("gemm_source_sha256_16") != source_digest(GEMM_SOURCES):
+        return None
+    return {k: t[k] for k in ("avg_launch_us", "achieved", "frac", "stream_read_gbs", "source") if k in t}
+
+
+def _counter_rows(path):
+    """rocprofv3 counter-collection CSV: {dispatch id: {name, grid, counters, seconds}}."""
+    import csv
+    import re
+    d = {}
+    for r in csv.DictReader(open(path)):
+        k = int(r["Dispatch_Id"])
+        e = d.setdefault(k, {"name": re.sub(r"\(.*", "", r["Kernel_Name"]).replace("void ", "").replace("sps::", ""),
+                             "grid": int(r["Grid_Size"]),
+                             "seconds": (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9})
+        e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return d
+
+
+def ingest_profiles(args):
+    """Write profiles/gemm_{traffic,mfma,trace}[_fp8].json from rocprofv3
+    output of this benchmark at its default workload (70B, K = 4, B = 1,
+    ctx 2048, --weights as given), with the hash of the GEMM sources they
+    were taken on (bench.py reports them only while it matches):
+      traffic: FETCH_SIZE and WRITE_SIZE counter CSVs (two runs), scaled by
+               the 1 GiB calibration copy + the embedding copy the benchmark
+               performs;
+      mfma:    a CSV of SQ_INSTS_VALU_MFMA_MOPS_BF16, SQ_VALU_MFMA_BUSY_CYCLES
+               and GRBM_GUI_ACTIVE;
+      trace:   a --kernel-trace CSV: the average gemm_kernel duration, and the
+               streaming-read rate from the stream_read_kernel dispatches."""
+    import csv
+    import re
+    from paper_2302_01318_amd import configs
+    shape = configs.SEVENTY_B.with_(dtype=args.weights)
+    alg = gemm_bytes_per_launch(shape, 5)
+    dig = source_digest(GEMM_SOURCES)
+    kind, paths = args.ingest[0], args.ingest[1:]
+    base = {"workload": "70B-shaped verify step, K=4, B=1, ctx 2048 (321 GEMM launches per step)",
+            "weights": args.weights, "gemm_source_sha256_16": dig}
+    if kind == "traffic":
+        fe, wr = _counter_rows(paths[0]), _counter_rows(paths[1])
+        cbytes = (1 << 30) + shape.vocab * shape.d_model * 2          # calibration copy + embedding copy
+        cp = [k for k in fe if "copyBuffer" in fe[k]["name"] and fe[k]["grid"] == 131072]
+        fs = cbytes / (sum(fe[k]["FETCH_SIZE"] for k in cp) * 1024)
+        ws = cbytes / (sum(wr[k]["WRITE_SIZE"] for k in cp) * 1024)
+        g = [k for k in fe if fe[k]["name"].startswith("gemm_kernel")]
+        per = sum(fe[k]["FETCH_SIZE"] * 1024 * fs + wr[k]["WRITE_SIZE"] * 1024 * ws for k in g) / len(g)
+        out = dict(base, kernel="gemm_kernel, all launches of a step", fetch_scale=round(fs, 4),
+                   write_scale=round(ws, 4), hbm_bytes_per_launch=int(round(per)),
+                   algorithmic_bytes_per_launch=int(round(alg)), launches=len(g),
+                   source="profiles/gemm_hbm_traffic_70b.md")
+    elif kind == "mfma":
+        d = _counter_rows(paths[0])
+        busy = act = fl = dur = 0.0
+        for r in d.values():
+            if r["name"].startswith("gemm_kernel") and "SQ_VALU_MFMA_BUSY_CYCLES" in r:
+                busy += r["SQ_VALU_MFMA_BUSY_CYCLES"]
+                act += r["GRBM_GUI_ACTIVE"] / 8 * 1024          # 8 XCDs, 1024 SIMDs
+                fl += r["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
+                dur += r["seconds"]
+        n = sum(1 for r in d.values() if r["name"].startswith("gemm_kernel") and "SQ_VALU_MFMA_BUSY_CYCLES" in r)
+        HD, F_rows = shape.n_heads * shape.head_dim, shape.d_ff * (2 if shape.ffn == "swiglu" else 1)
+        elems = shape.n_layers * (4 * HD * shape.d_model + F_rows * shape.d_model + shape.d_model * shape.d_ff) + \
+            shape.vocab * shape.d_model
+        useful = 2.0 * 5 * elems / (4 * shape.n_layers + 1) * n          # 5 real rows, every weight once
+        out = dict(base, kernel="gemm_kernel, all launches of a step", mfma_busy_pct=round(100 * busy / act, 2),
+                   mfma_executed_tflops=round(fl / dur / 1e12, 1), useful_tflops=round(useful / dur / 1e12, 1),
+                   peak_tflops_bf16_dense=2500.0, launches=n, source="profiles/gemm_mfma_util_70b.md")
+    else:
+        rows = list(csv.DictReader(open(paths[0])))
+        dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+        g = [dur(r) for r in rows if re.search(r"gemm_kernel", r["Kernel_Name"])]
+        sr = [dur(r) for r in rows if "stream_read_kernel" in r["Kernel_Name"]]
+        avg = sum(g) / len(g)
+        out = dict(base, kernel="gemm_kernel, every dispatch of the run", dispatches=len(g),
+                   avg_launch_us=round(avg * 1e6, 2), achieved=round(alg / avg / 1e9, 1),
+                   frac=round(alg / avg / 1e9 / HBM_PEAK_GBS, 4),
+                   stream_read_gbs=round(STREAM_READ_BYTES / sorted(sr)[len(sr) // 2] / 1e9, 1) if sr else None,
+                   algorithmic_bytes_per_launch=int(round(alg)), source="profiles/verify_step_70b_kernel_trace.md")
+    path = _profile_file(kind, args.weights)
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+
+
 def stream_read_rate(sps, torch, buf, nbytes=STREAM_READ_BYTES, reps=10):
     """GB/s of the library's plain streaming read over the first `nbytes` of
     `buf` (the attainable HBM read rate on this device), median of `reps`."""
@@ -116,6 +210,22 @@ def verify_bytes(shape, B, K, ctx):
     kv_write = shape.n_layers * M * 2 * HD * es
     logits = 2 * M * shape.vocab * 4
     return weights + gains + embed_rows + kv_read + kv_write + logits
+
+
+def gemm_bytes_per_launch(shape, M):
+    """Algorithmic bytes of one weight-streaming GEMM launch averaged over
+    the launches of one forward at M rows: every weight (and FP8 row scale)
+    once, the fp32 input activations and the fp32 outputs once -- the figure
+    sps_profile_gemm_end accumulates per launch."""
+    wes = 1 if shape.dtype == "fp8" else shape.act_bytes()
+    HD, d, F = shape.n_heads * shape.head_dim, shape.d_model, shape.d_ff
+    F_rows = 2 * F if shape.ffn == "swiglu" else F
+
+    def one(rows_w, K, n_valid):
+        return rows_w * K * wes + (4 * rows_w if shape.dtype == "fp8" else 0) + 4 * M * K + 4 * M * n_valid
+
+    layer = one(3 * HD, d, 3 * HD) + one(d, HD, d) + one(F_rows, d, F) + one(d, F, d)
+    return (shape.n_layers * layer + one(shape.vocab, d, shape.vocab)) / (4 * shape.n_layers + 1)
 
 
 def model_shapes(configs, args):
@@ -570,9 +680,15 @@ def main():
                     help="comma-separated draft logit perturbations for --k-study (default: the configured ones)")
     ap.add_argument("--k-study-K", default=None, help="comma-separated K values for --k-study")
     ap.add_argument("--reps", type=int, default=None, help="generations per point for --k-study")
+    ap.add_argument("--ingest", nargs="+", default=None, metavar=("KIND", "CSV"),
+                    help="write profiles/gemm_KIND[_fp8].json from rocprofv3 CSVs of this benchmark: "
+                         "'traffic FETCH.csv WRITE.csv', 'mfma COUNTERS.csv' or 'trace KERNEL_TRACE.csv'")
     ap.add_argument("--no-roofline-pass", action="store_true",
                     help="skip the second pass that times every GEMM launch with events")
     args = ap.parse_args()
+    if args.ingest:
+        ingest_profiles(args)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures the verify step on one GPU; there is no multi-GPU path "
               "(requested --gpus %d)" % args.gpus, file=sys.stderr)
@@ -663,7 +779,8 @@ def main():
                     "frac": round(g_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(args.weights),
                     "launches_per_step": g_n // args.steps, "avg_launch_us": round(g_avg_ms * 1e3, 2),
                     "bytes_per_launch": g_bytes / g_n,
-                    "frac_of_stream_read": round(g_gbs / read_gbs, 4), "mfma": measured_mfma(args.weights)}
+                    "frac_of_stream_read": round(g_gbs / read_gbs, 4), "mfma": measured_mfma(args.weights),
+                    "trace": measured_trace(args.weights)}
     del kv, ws
     torch.cuda.empty_cache()     # the end-to-end caches differ in size from the timing cache
 
