@@ -8,8 +8,9 @@
 // HBM, sets the speed. Here:
 //
 //  * a work-group of 4 waves owns 4 NTW consecutive n-tiles (NTW = 2, or 4
-//    at 14 M tiles, where each fragment read from LDS then feeds four MFMAs
-//    instead of two) and one contiguous range of the k-tiles; wave w
+//    for bf16 weights at 14 and 16 M tiles, where each activation fragment
+//    read from LDS then feeds four MFMAs) and one contiguous range of the
+//    k-tiles; wave w
 //    multiplies n-tiles NTW w .. NTW w + NTW - 1 by all MT M tiles;
 //  * per chunk of KC k-tiles the work-group copies the chunk's activations
 //    once into LDS with global_load_lds (16 B per lane, whole 128-byte
@@ -252,21 +253,23 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
 
 // The main loop with the weights, too, copied into LDS: activation chunks
 // double-buffered as in wide_mainloop, weight chunks in a ring of
-// kWideStages buffers filled kWideStages - 2 chunks ahead of the chunk whose
-// activations are copied. Step c copies the activations of chunk c + 1 and
-// then the weights of chunk c + kWideStages - 1 (each only if that chunk is
-// one of this work-group's), so when step c starts, the copies issued after
-// chunk c's activations are at most the weights of chunk c + kWideStages - 2:
+// kS = wide_stages(MT, W8) buffers filled kS - 2 chunks ahead of the chunk
+// whose activations are copied. Step c copies the activations of chunk c + 1
+// and then the weights of chunk c + kS - 1 (each only if that chunk is one of
+// this work-group's), so when step c starts, the copies issued after chunk
+// c's activations are at most the weights of chunk c + kS - 2:
 // waiting until only those are outstanding (vmcnt), then a barrier, makes
 // chunk c's activations and weights visible to every wave while later
-// weights stay in flight. A buffer is refilled only after the barrier that
-// follows the last reads of the chunk it held.
+// weights stay in flight. With two stages (kS = 2) the weights of chunk c
+// follow its activations and the wait drains every copy. A buffer is
+// refilled only after the barrier that follows the last reads of the chunk
+// it held.
 template <int MT, int KC, int NTW, bool W8>
 __device__ __forceinline__ void wide_mainloop_staged(const GemmParams& p, int g, int c0, int c1,
                                                      bf16x8 (*s_a)[64], bf16x8 (*s_w)[64],
                                                      f32x4 (&acc)[NTW][MT]) {
   using T = bf16;
-  constexpr int kS = kWideStages;
+  constexpr int kS = wide_stages(MT, W8);
   constexpr int kBuf = MT * KC;                              // activation fragments per chunk
   constexpr int kWF = W8 ? KC / 2 : KC;                      // weight fragments per n-tile and chunk
   constexpr int kWSlots = kWideWaves * NTW * kWF;            // weight fragments per stage
@@ -274,7 +277,7 @@ __device__ __forceinline__ void wide_mainloop_staged(const GemmParams& p, int g,
   constexpr int kWLoads = NTW * kWF;
   constexpr uint32_t kFragBytes = 64 * 16;
   static_assert(KC == 2, "activation blocks hold the two k-tiles of a chunk");
-  static_assert(kS >= 3 && kALoads + (kS - 1) * kWLoads <= 63, "copies in flight fit the vmcnt counter");
+  static_assert(kS >= 2 && kALoads + (kS - 1) * kWLoads <= 63, "copies in flight fit the vmcnt counter");
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int ntw = g * kWideWaves * NTW + wave * NTW;        // first n-tile of this wave
@@ -366,7 +369,7 @@ __device__ __forceinline__ void wide_mainloop_staged(const GemmParams& p, int g,
     if (c0 + kS - 2 < c1) issue_w(c0 + kS - 2, kS - 2);
     for (int c = c0; c < c1; ++c) {
       const int bb = (c - c0) & 1, st = (c - c0) % kS;
-      if (c + kS - 2 < c1)
+      if (kS >= 3 && c + kS - 2 < c1)
         __builtin_amdgcn_s_waitcnt(vmcnt_only(kWLoads));   // chunk c + kS - 2's weights may stay in flight
       else
         __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
@@ -443,7 +446,7 @@ template <int MT, int KC, int NTW, int EPI, bool W8>
 __global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, NTW>())))
 void gemm_wide_kernel(const GemmParams p, int chunks) {
   __shared__ bf16x8 s_a[2 * MT * KC][64];          // two chunks of activation fragments
-  __shared__ bf16x8 s_w[wide_staged(MT, W8) ? kWideStages * kWideWaves * NTW * (W8 ? KC / 2 : KC) : 1][64];
+  __shared__ bf16x8 s_w[wide_staged(MT, W8) ? wide_stages(MT, W8) * kWideWaves * NTW * (W8 ? KC / 2 : KC) : 1][64];
   // One norm group's output tile reuses the chunk buffers, dead after the
   // loop, and so do the row scales where they fit behind it.
   constexpr int kTile = kNormTiles * MT * 128;     // floats
@@ -485,7 +488,7 @@ template <int MT, int KC, int NTW, bool W8>
 __global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, NTW>())))
 void gemm_wide_split_kernel(const GemmParams p, int S, int chunks) {
   __shared__ bf16x8 s_a[2 * MT * KC][64];
-  __shared__ bf16x8 s_w[wide_staged(MT, W8) ? kWideStages * kWideWaves * NTW * (W8 ? KC / 2 : KC) : 1][64];
+  __shared__ bf16x8 s_w[wide_staged(MT, W8) ? wide_stages(MT, W8) * kWideWaves * NTW * (W8 ? KC / 2 : KC) : 1][64];
   const int G = (p.NT + kWideWaves * NTW - 1) / (kWideWaves * NTW);
   const int g = blockIdx.x % G, s = blockIdx.x / G;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -535,7 +538,7 @@ __global__ __launch_bounds__(kWideWaves * 64) void gemm_wide_reduce_kernel(const
 // ---------------------------------------------------------------------------
 // Launch planning.
 // ---------------------------------------------------------------------------
-template <int MT, bool W8, int KC = wide_kc(MT, W8), int NTW = wide_ntw(MT)>
+template <int MT, bool W8, int KC = wide_kc(MT, W8), int NTW = wide_ntw(MT, W8)>
 static hipError_t wide_launch(const GemmParams& p, const WidePlan& w, hipStream_t st) {
   const dim3 block(kWideWaves * 64);
   if (w.NTW != NTW || w.KC != KC || w.w8 != W8) return hipErrorInvalidValue;

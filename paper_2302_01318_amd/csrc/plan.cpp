@@ -21,7 +21,7 @@ WidePlan wide_plan(int NT, int KT, int M, bool w8) {
     if (v >= mt) { w.MT = v; break; }
   w.w8 = w8;
   w.KC = wide_kc(w.MT, w8);
-  w.NTW = wide_ntw(w.MT);
+  w.NTW = wide_ntw(w.MT, w8);
   w.G = (NT + kWideWaves * w.NTW - 1) / (kWideWaves * w.NTW);
   w.chunks = (KT + w.KC - 1) / w.KC;
   // Split count: the work-groups a CU holds at once (LDS of the split
@@ -33,7 +33,7 @@ WidePlan wide_plan(int NT, int KT, int M, bool w8) {
   // half-empty second round, 16 % slower), 2 for 250 at two per CU.
   const bool staged = wide_staged(w.MT, w8);
   const long lds = 2L * w.MT * w.KC * 1024 +
-                   (staged ? static_cast<long>(kWideStages) * kWideWaves * w.NTW * (w8 ? w.KC / 2 : w.KC) * 1024 : 0);
+                   (staged ? static_cast<long>(wide_stages(w.MT, w8)) * kWideWaves * w.NTW * (w8 ? w.KC / 2 : w.KC) * 1024 : 0);
   const int occ = std::max(1, std::min(static_cast<int>(kLdsBytes / lds), waves_per_simd(w.MT)));
   const long slots = static_cast<long>(kCUs) * occ;
   long best = -1;

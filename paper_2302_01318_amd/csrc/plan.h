@@ -29,12 +29,17 @@ constexpr int kActRowsF32 = 16;
 // Wide GEMM (bf16 activations, more than 8 rows; gemm_wide.hip).
 constexpr int kWideWaves = 4;          // waves per work-group
 constexpr int kNormTiles = 8;          // n-tiles per norm group (128 columns)
-constexpr int kWideStages = 4;         // LDS weight stages of the staged loop
 constexpr int kWideMT[] = {2, 3, 4, 5, 6, 8, 10, 12, 14, 16, 18, 20};   // compiled M-tile counts
 
-// n-tiles per wave. (With register-held weights, 4 at 14 M tiles ran the
-// 70B W_1 and W_2 22-24 % faster than 2; the staged loop at 2 beats both.)
-constexpr int wide_ntw(int) { return 2; }
+// n-tiles per wave: 2, and 4 for bf16 weights at 14 and 16 M tiles (16
+// n-tiles per work-group halve the activation copies per weight byte, which
+// with the weights share each CU's outstanding L2 requests: 70B steps at
+// B = 16, K = 6 3.6-5 % faster, K = 7 2-3 %). At 18 and 20 M tiles the 288+
+// accumulators per wave spill, and FP8 codes measured no gain (10 M tiles)
+// or a loss (18). (With register-held weights, 4 at 14 M tiles ran the 70B
+// W_1 and W_2 22-24 % faster than 2; the staged loop beats both.)
+constexpr bool wide_four(int MT, bool w8) { return !w8 && (MT == 14 || MT == 16); }
+constexpr int wide_ntw(int MT, bool w8) { return wide_four(MT, w8) ? 4 : 2; }
 
 // Where the weights go through LDS too (wide_mainloop_staged): from 14 M
 // tiles for bf16 weights, where one wave per SIMD with register-held weights
@@ -42,6 +47,14 @@ constexpr int wide_ntw(int) { return 2; }
 // keeps only 4 KiB per wave in flight. Below, the register path with two to
 // three work-groups per CU is faster.
 constexpr bool wide_staged(int MT, bool w8) { return MT >= (w8 ? 8 : 14); }
+
+// LDS weight stages of the staged loop: 4, so each chunk's weights have two
+// steps to land (the wait for a chunk's activations also waits for every
+// copy issued before them, so a fifth stage would add no time), or 2 with 4
+// n-tiles per wave, whose 32 KiB stages leave room for no more beside the
+// activation buffers: the weights then land with the activations, one step
+// ahead.
+constexpr int wide_stages(int MT, bool w8) { return wide_four(MT, w8) ? 2 : 4; }
 
 // Waves per SIMD the register allocation must allow (the compiler would
 // otherwise hoist every LDS fragment read of a chunk into registers).
