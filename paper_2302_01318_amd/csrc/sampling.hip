@@ -47,16 +47,13 @@ __device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
 
 // Branch-free (selects only), so that loops over a row keep their loads in
 // flight together: floor(x 2^32) for x in (0, 1), 2^32 for x >= 1, 0 for
-// x <= 0 or NaN. Integer arithmetic on the fp32 encoding: for 0 < x < 1
-// with biased exponent e and 24-bit significand m (no implicit one when
-// e = 0), x 2^32 = m 2^(e - 118), so the floor is a shift of m.
+// x <= 0 or NaN. In double precision, where x 2^32 is exact and the
+// conversion truncates. (Shifting the fp32 significand gives the same
+// integers but made the draft draw ~40 % slower: 45 against 32 us.)
 __device__ __forceinline__ uint64_t fixed_weight(float x) {
-  const uint32_t b = __float_as_uint(x);
-  const int e = static_cast<int>((b >> 23) & 0xFF);
-  const uint32_t m = (b & 0x7FFFFFu) | (e ? 0x800000u : 0u);
-  const int sh = e - 118;                                      // <= 8 for x < 1
-  const uint64_t w = sh >= 0 ? static_cast<uint64_t>(m << (sh & 31)) : sh > -32 ? m >> (-sh & 31) : 0u;
-  return x >= 1.f ? (1ull << 32) : x > 0.f ? w : 0u;
+  const double d = x > 0.f ? fmin(static_cast<double>(x), 1.0) : 0.0;
+  const double f = fmin(d * 4294967296.0, 4294967295.0);        // d = 1 adds the missing unit below
+  return static_cast<uint64_t>(static_cast<uint32_t>(f)) + (d >= 1.0 ? 1u : 0u);
 }
 
 __device__ __forceinline__ uint64_t grid_threshold(float u, uint64_t W) {
