@@ -34,10 +34,11 @@ constexpr int kWideMT[] = {2, 3, 4, 5, 6, 8, 10, 12, 14, 16, 18, 20};   // compi
 // n-tiles per wave: 2, and 4 for bf16 weights at 14 and 16 M tiles (16
 // n-tiles per work-group halve the activation copies per weight byte, which
 // with the weights share each CU's outstanding L2 requests: 70B steps at
-// B = 16, K = 6 3.6-5 % faster, K = 7 2-3 %). At 18 and 20 M tiles the 288+
-// accumulators per wave spill, and FP8 codes measured no gain (10 M tiles)
-// or a loss (18). (With register-held weights, 4 at 14 M tiles ran the 70B
-// W_1 and W_2 22-24 % faster than 2; the staged loop beats both.)
+// B = 16, K = 6 2.5-5 % faster; K = 7 within the run-to-run spread). At 18
+// and 20 M tiles the 288+ accumulators per wave spill, and FP8 codes
+// measured no gain (10 M tiles) or a loss (18). (With register-held
+// weights, 4 at 14 M tiles ran the 70B W_1 and W_2 22-24 % faster than 2;
+// the staged loop beats both.)
 constexpr bool wide_four(int MT, bool w8) { return !w8 && (MT == 14 || MT == 16); }
 constexpr int wide_ntw(int MT, bool w8) { return wide_four(MT, w8) ? 4 : 2; }
 
@@ -48,12 +49,12 @@ constexpr int wide_ntw(int MT, bool w8) { return wide_four(MT, w8) ? 4 : 2; }
 // three work-groups per CU is faster.
 constexpr bool wide_staged(int MT, bool w8) { return MT >= (w8 ? 8 : 14); }
 
-// LDS weight stages of the staged loop: 4, so each chunk's weights have two
-// steps to land (the wait for a chunk's activations also waits for every
-// copy issued before them, so a fifth stage would add no time), or 2 with 4
-// n-tiles per wave, whose 32 KiB stages leave room for no more beside the
-// activation buffers: the weights then land with the activations, one step
-// ahead.
+// LDS weight stages of the staged loop: 4 (3 and 5 measured the same: the
+// wait for a chunk's activations also waits for every copy issued before
+// them, so each chunk's weights get two steps to land however deep the
+// ring), or 2 with 4 n-tiles per wave, whose 32 KiB stages leave no room for
+// a third beside the activation buffers at 16 M tiles (at 14 a third
+// measured no faster): the weights then land with the activations.
 constexpr int wide_stages(int MT, bool w8) { return wide_four(MT, w8) ? 2 : 4; }
 
 // Waves per SIMD the register allocation must allow (the compiler would
