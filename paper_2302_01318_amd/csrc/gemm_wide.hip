@@ -7,16 +7,16 @@
 // weight byte through the vector caches, and above MT = 1 that traffic, not
 // HBM, sets the speed. Here:
 //
-//  * a work-group of 4 waves owns 4 NTW consecutive n-tiles (NTW = 2, or 4
-//    for bf16 weights at 14 and 16 M tiles, where each activation fragment
-//    read from LDS then feeds four MFMAs) and one contiguous range of the
-//    k-tiles; wave w
-//    multiplies n-tiles NTW w .. NTW w + NTW - 1 by all MT M tiles;
+//  * a work-group of WV waves (4, or 8 where bf16 weights are staged
+//    through LDS) owns WV NTW consecutive n-tiles (NTW = 2) and one
+//    contiguous range of the k-tiles; wave w multiplies n-tiles
+//    NTW w .. NTW w + NTW - 1 by all MT M tiles;
 //  * per chunk of KC k-tiles the work-group copies the chunk's activations
 //    once into LDS with global_load_lds (16 B per lane, whole 128-byte
-//    lines per instruction: act_piece_src), so the four waves share them,
+//    lines per instruction: act_piece_src), so all the waves share them,
 //    and every wave streams its own weight fragments from HBM into
-//    registers (from 16 M tiles through LDS as well: the staged loop);
+//    registers (from 14 M tiles, 8 with FP8 codes, through LDS as well:
+//    the staged loop);
 //  * where N is too small to give every CU a work-group (the d_model-wide
 //    outputs), the k range is split S ways (split-K): each split writes its
 //    fp32 partial tile to the workspace and a second kernel sums the splits
@@ -48,7 +48,7 @@ constexpr int vmcnt_only(int n) { return (n & 15) | ((n >> 4) & 3) << 14 | 7 << 
 // hi rows after folding the lo rows in), in register order.
 template <int MT, int NTW> constexpr int wide_part_floats() { return NTW * MT * 128; }
 
-template <int MT, int NTW> constexpr int wide_waves_per_simd() { return waves_per_simd(MT); }
+template <int MT, bool W8> constexpr int wide_waves_per_simd() { return waves_per_simd(MT, W8); }
 
 // Weight registers of one chunk: bf16 fragments, or the raw FP8 code loads
 // (one per k-tile pair) that become fragments right before their MFMAs.
@@ -105,13 +105,20 @@ __device__ __forceinline__ int act_slot(int lane, int u) {
   return (pl * 4 + (r & 3)) * 8 + ((u * 4 + g) ^ r ^ pl);
 }
 
-// Accumulate chunks [c0, c1) of column group g into acc, then fold the
-// lo-plane rows (lanes 32-63) into their hi rows (lanes 0-31). Double
+// The lo-plane rows of an accumulator tile (lanes 32-63) added into their
+// hi rows (lanes 0-31), which then hold the output rows.
+__device__ __forceinline__ void fold_lo(f32x4& a) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) a[r] += __shfl_xor(a[r], 32);
+}
+
+// Accumulate chunks [c0, c1) of column group g into acc (the caller folds
+// the lo-plane rows into the hi rows with fold_lo). Double
 // buffered: while a chunk's MFMAs run, the next chunk's activation
 // fragments are already on their way into the other LDS buffer (s_a holds
 // 2 * MT * KC fragments) and its weight fragments into the other register
 // set; one barrier per chunk.
-template <int MT, int KC, int NTW, bool W8>
+template <int MT, int KC, int NTW, int WV, bool W8>
 __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0, int c1, bf16x8 (*s_a)[64],
                                               f32x4 (&acc)[NTW][MT]) {
   static_assert(KC % 2 == 0, "chunks hold whole k-tile pairs (activation blocks, FP8 codes)");
@@ -120,7 +127,7 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
   constexpr int kTile = 512;                       // elements per 16 x 32 tile
   constexpr int kBuf = MT * KC;                    // fragments per LDS buffer
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int ntw = g * kWideWaves * NTW + wave * NTW;   // first n-tile of this wave
+  const int ntw = g * WV * NTW + wave * NTW;          // first n-tile of this wave
   const int KT = p.KT;
   const T* W = static_cast<const T*>(p.W);
 
@@ -145,7 +152,7 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
   // + pair) + h; pairs wholly past KT are skipped (their MFMAs are).
   auto issue_a = [&](int c, int bb) {
     const int kb = c * KC;
-    for (int f = wave; f < kBuf; f += kWideWaves) {
+    for (int f = wave; f < kBuf; f += WV) {
       const int h = f & 1, pr = (f >> 1) % (KC / 2), mt = (f >> 1) / (KC / 2);
       if (kb + 2 * pr < KT)
         __builtin_amdgcn_global_load_lds(act_piece_src(p, lane, mt, h, kb + 2 * pr),
@@ -243,12 +250,6 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
     if (c + 1 < c1) step(c + 1, 1, b1, b0);
   }
   __syncthreads();                                 // LDS free for the caller (epilogue tile)
-#pragma unroll
-  for (int j = 0; j < NTW; ++j)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[j][mt][r] += __shfl_xor(acc[j][mt][r], 32);
 }
 
 // The main loop with the weights, too, copied into LDS: activation chunks
@@ -264,7 +265,7 @@ __device__ __forceinline__ void wide_mainloop(const GemmParams& p, int g, int c0
 // follow its activations and the wait drains every copy. A buffer is
 // refilled only after the barrier that follows the last reads of the chunk
 // it held.
-template <int MT, int KC, int NTW, bool W8>
+template <int MT, int KC, int NTW, int WV, bool W8>
 __device__ __forceinline__ void wide_mainloop_staged(const GemmParams& p, int g, int c0, int c1,
                                                      bf16x8 (*s_a)[64], bf16x8 (*s_w)[64],
                                                      f32x4 (&acc)[NTW][MT]) {
@@ -272,15 +273,15 @@ __device__ __forceinline__ void wide_mainloop_staged(const GemmParams& p, int g,
   constexpr int kS = wide_stages(MT, W8);
   constexpr int kBuf = MT * KC;                              // activation fragments per chunk
   constexpr int kWF = W8 ? KC / 2 : KC;                      // weight fragments per n-tile and chunk
-  constexpr int kWSlots = kWideWaves * NTW * kWF;            // weight fragments per stage
-  constexpr int kALoads = (kBuf + kWideWaves - 1) / kWideWaves;
+  constexpr int kWSlots = WV * NTW * kWF;                    // weight fragments per stage
+  constexpr int kALoads = (kBuf + WV - 1) / WV;
   constexpr int kWLoads = NTW * kWF;
   constexpr uint32_t kFragBytes = 64 * 16;
   static_assert(KC == 2, "activation blocks hold the two k-tiles of a chunk");
   static_assert(kS >= 2 && kALoads + (kS - 1) * kWLoads <= 63, "copies in flight fit the vmcnt counter");
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int ntw = g * kWideWaves * NTW + wave * NTW;        // first n-tile of this wave
+  const int ntw = g * WV * NTW + wave * NTW;                // first n-tile of this wave
   const int KT = p.KT;
   // This lane's 16 bytes of weight fragment (n-tile j, unit k) at
   // wbase[j] + 1 KiB k, a unit being a k-tile (bf16) or a k-tile pair (FP8
@@ -304,8 +305,8 @@ __device__ __forceinline__ void wide_mainloop_staged(const GemmParams& p, int g,
   auto issue_a = [&](int c, int bb) {
 #pragma unroll
     for (int i = 0; i < kALoads; ++i) {
-      const int f = wave + i * kWideWaves;
-      if (kBuf % kWideWaves && f >= kBuf) break;       // uneven split: this wave's count is one lower
+      const int f = wave + i * WV;
+      if (kBuf % WV && f >= kBuf) break;               // uneven split: this wave's count is one lower
       lds_copy16_untracked(act_piece_src(p, lane, f >> 1, f & 1, c * KC), a_lds + (bb * kBuf + f) * kFragBytes);
     }
   };
@@ -382,12 +383,6 @@ __device__ __forceinline__ void wide_mainloop_staged(const GemmParams& p, int g,
     }
   }
   __syncthreads();                                 // LDS free for the caller (epilogue tile)
-#pragma unroll
-  for (int j = 0; j < NTW; ++j)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[j][mt][r] += __shfl_xor(acc[j][mt][r], 32);
 }
 
 // Row scales of the input RMSNorm for rows mt0 * 8 .. (mt0 + NMT) * 8 - 1
@@ -395,7 +390,7 @@ __device__ __forceinline__ void wide_mainloop_staged(const GemmParams& p, int g,
 template <int NMT>
 __device__ __forceinline__ void wide_row_scales(const GemmParams& p, int mt0, float* s_rs) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int i = wave; i < NMT * 8; i += kWideWaves) {
+  for (int i = wave; i < NMT * 8; i += static_cast<int>(blockDim.x >> 6)) {
     const float v = norm_scale(p, mt0 * 8 + i, lane);
     if (lane == 0) s_rs[i] = v;
   }
@@ -410,7 +405,7 @@ __device__ __forceinline__ void wide_epilogue_group(const GemmParams& p, int gs,
   using T = bf16;
   const int M = p.M, r0 = mt0 * 8;
   if (gs * kNormTiles >= p.NT) return;             // whole group past the last n-tile
-  for (int e = threadIdx.x; e < kNormTiles * NMT * 128; e += kWideWaves * 64) {
+  for (int e = threadIdx.x; e < kNormTiles * NMT * 128; e += blockDim.x) {
     const int jj = e / (NMT * 128), mtl = (e >> 7) % NMT, i = (e >> 4) & 7, col = e & 15;
     const int m = r0 + mtl * 8 + i, nt = gs * kNormTiles + jj;
     if (m >= M || nt >= p.NT) {
@@ -428,7 +423,7 @@ __device__ __forceinline__ void wide_epilogue_group(const GemmParams& p, int gs,
   if (EPI == kEpiResid) {
     // Sums of squares of the group's 128 columns per row, in a fixed order.
     __syncthreads();
-    for (int r = threadIdx.x; r < NMT * 8; r += kWideWaves * 64) {
+    for (int r = threadIdx.x; r < NMT * 8; r += blockDim.x) {
       const int m = r0 + r;
       if (m >= M) continue;
       const int mtl = r >> 3, i = r & 7;
@@ -440,27 +435,31 @@ __device__ __forceinline__ void wide_epilogue_group(const GemmParams& p, int gs,
   }
 }
 
-// One work-group per column group (4 NTW n-tiles) over the whole k range,
+// One work-group per column group (WV NTW n-tiles) over the whole k range,
 // epilogue fused: the folded tile goes to LDS one norm group at a time.
-template <int MT, int KC, int NTW, int EPI, bool W8>
-__global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, NTW>())))
+template <int MT, int KC, int NTW, int WV, int EPI, bool W8>
+__global__ __launch_bounds__(WV * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, W8>())))
 void gemm_wide_kernel(const GemmParams p, int chunks) {
   __shared__ bf16x8 s_a[2 * MT * KC][64];          // two chunks of activation fragments
-  __shared__ bf16x8 s_w[wide_staged(MT, W8) ? wide_stages(MT, W8) * kWideWaves * NTW * (W8 ? KC / 2 : KC) : 1][64];
+  __shared__ bf16x8 s_w[wide_staged(MT, W8) ? wide_stages(MT, W8) * WV * NTW * (W8 ? KC / 2 : KC) : 1][64];
   // One norm group's output tile reuses the chunk buffers, dead after the
   // loop, and so do the row scales where they fit behind it.
   constexpr int kTile = kNormTiles * MT * 128;     // floats
   static_assert(kTile * sizeof(float) <= sizeof(s_a), "epilogue tile must fit the chunk buffers");
   constexpr bool kRsInA = (kTile + MT * 8) * sizeof(float) <= sizeof(s_a);
   __shared__ float s_rs_own[kRsInA ? 1 : MT * 8];
-  constexpr int kGroups = kWideWaves * NTW / kNormTiles;   // norm groups per work-group
-  constexpr int kWavesPerGroup = kWideWaves / kGroups;
+  constexpr int kGroups = WV * NTW / kNormTiles;   // norm groups per work-group
+  constexpr int kWavesPerGroup = WV / kGroups;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   f32x4 acc[NTW][MT];
   if constexpr (wide_staged(MT, W8))
-    wide_mainloop_staged<MT, KC, NTW, W8>(p, blockIdx.x, 0, chunks, s_a, s_w, acc);
+    wide_mainloop_staged<MT, KC, NTW, WV, W8>(p, blockIdx.x, 0, chunks, s_a, s_w, acc);
   else
-    wide_mainloop<MT, KC, NTW, W8>(p, blockIdx.x, 0, chunks, s_a, acc);
+    wide_mainloop<MT, KC, NTW, WV, W8>(p, blockIdx.x, 0, chunks, s_a, acc);
+#pragma unroll
+  for (int j = 0; j < NTW; ++j)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) fold_lo(acc[j][mt]);
   float* ep = reinterpret_cast<float*>(&s_a[0][0]);
   float* s_rs = kRsInA ? ep + kTile : s_rs_own;
 #pragma unroll
@@ -484,48 +483,51 @@ void gemm_wide_kernel(const GemmParams p, int chunks) {
 
 // Split s of column group g (work-group g + s G): chunks [s C / S, (s+1) C / S)
 // into the partial buffer.
-template <int MT, int KC, int NTW, bool W8>
-__global__ __launch_bounds__(kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, NTW>())))
+template <int MT, int KC, int NTW, int WV, bool W8>
+__global__ __launch_bounds__(WV * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, W8>())))
 void gemm_wide_split_kernel(const GemmParams p, int S, int chunks) {
   __shared__ bf16x8 s_a[2 * MT * KC][64];
-  __shared__ bf16x8 s_w[wide_staged(MT, W8) ? wide_stages(MT, W8) * kWideWaves * NTW * (W8 ? KC / 2 : KC) : 1][64];
-  const int G = (p.NT + kWideWaves * NTW - 1) / (kWideWaves * NTW);
+  __shared__ bf16x8 s_w[wide_staged(MT, W8) ? wide_stages(MT, W8) * WV * NTW * (W8 ? KC / 2 : KC) : 1][64];
+  const int G = (p.NT + WV * NTW - 1) / (WV * NTW);
   const int g = blockIdx.x % G, s = blockIdx.x / G;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c0 = static_cast<int>(static_cast<long>(s) * chunks / S);
   const int c1 = static_cast<int>(static_cast<long>(s + 1) * chunks / S);
   f32x4 acc[NTW][MT];
   if constexpr (wide_staged(MT, W8))
-    wide_mainloop_staged<MT, KC, NTW, W8>(p, g, c0, c1, s_a, s_w, acc);
+    wide_mainloop_staged<MT, KC, NTW, WV, W8>(p, g, c0, c1, s_a, s_w, acc);
   else
-    wide_mainloop<MT, KC, NTW, W8>(p, g, c0, c1, s_a, acc);
-  if (lane < 32) {
-    float* mine = p.part + ((static_cast<size_t>(s) * G + g) * kWideWaves + wave) * wide_part_floats<MT, NTW>();
+    wide_mainloop<MT, KC, NTW, WV, W8>(p, g, c0, c1, s_a, acc);
+  // Fold and store one tile at a time (folding every tile first would keep
+  // all the shuffled copies live at once).
+  float* mine = p.part + ((static_cast<size_t>(s) * G + g) * WV + wave) * wide_part_floats<MT, NTW>() + lane * 4;
 #pragma unroll
-    for (int j = 0; j < NTW; ++j)
+  for (int j = 0; j < NTW; ++j)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-        *reinterpret_cast<f32x4*>(mine + ((j * MT + mt) * 32 + lane) * 4) = acc[j][mt];
-  }
+    for (int mt = 0; mt < MT; ++mt) {
+      fold_lo(acc[j][mt]);
+      if (lane < 32) *reinterpret_cast<f32x4*>(mine + (j * MT + mt) * 128) = acc[j][mt];
+      __builtin_amdgcn_sched_barrier(0);
+    }
 }
 
 // Sum of the S partials of norm group gs = blockIdx.x, M tile mt =
 // blockIdx.y, in split order, then the epilogue of that tile. Thread t sums
 // lane t % 32 of n-tile 8 gs + t / 32, which the split kernel's work-group
-// (8 gs + t / 32) / (4 NTW) holds in wave ((8 gs + t / 32) % (4 NTW)) / NTW:
+// (8 gs + t / 32) / (WV NTW) holds in wave ((8 gs + t / 32) % (WV NTW)) / NTW:
 // one coalesced 16 B load per split.
-template <int MT, int NTW, int EPI>
-__global__ __launch_bounds__(kWideWaves * 64) void gemm_wide_reduce_kernel(const GemmParams p, int S) {
+template <int MT, int NTW, int WV, int EPI>
+__global__ __launch_bounds__(kNormTiles * 32) void gemm_wide_reduce_kernel(const GemmParams p, int S) {
   __shared__ float ep[kNormTiles * 128];
   __shared__ float s_rs[8];
-  constexpr int kNg = kWideWaves * NTW;
+  constexpr int kNg = WV * NTW;
   const int G = (p.NT + kNg - 1) / kNg;
   const int gs = blockIdx.x, mt = blockIdx.y;
   const int t = threadIdx.x, jj = t >> 5, ln = t & 31;
   const int nt = gs * kNormTiles + jj, g = nt / kNg, wave = (nt % kNg) / NTW, j = nt % NTW;
-  const float* src = p.part + (static_cast<size_t>(g) * kWideWaves + wave) * wide_part_floats<MT, NTW>() +
+  const float* src = p.part + (static_cast<size_t>(g) * WV + wave) * wide_part_floats<MT, NTW>() +
                      ((j * MT + mt) * 32 + ln) * 4;
-  const size_t split = static_cast<size_t>(G) * kWideWaves * wide_part_floats<MT, NTW>();
+  const size_t split = static_cast<size_t>(G) * WV * wide_part_floats<MT, NTW>();
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int s = 0; s < S; ++s) acc += *reinterpret_cast<const f32x4*>(src + s * split);
 #pragma unroll
@@ -538,31 +540,31 @@ __global__ __launch_bounds__(kWideWaves * 64) void gemm_wide_reduce_kernel(const
 // ---------------------------------------------------------------------------
 // Launch planning.
 // ---------------------------------------------------------------------------
-template <int MT, bool W8, int KC = wide_kc(MT, W8), int NTW = wide_ntw(MT, W8)>
+template <int MT, bool W8, int KC = wide_kc(MT, W8), int NTW = wide_ntw(MT, W8), int WV = wide_waves(MT, W8)>
 static hipError_t wide_launch(const GemmParams& p, const WidePlan& w, hipStream_t st) {
-  const dim3 block(kWideWaves * 64);
-  if (w.NTW != NTW || w.KC != KC || w.w8 != W8) return hipErrorInvalidValue;
+  const dim3 block(WV * 64), rblock(kNormTiles * 32);
+  if (w.NTW != NTW || w.KC != KC || w.WV != WV || w.w8 != W8) return hipErrorInvalidValue;
   if (w.S > 1) {
-    hipLaunchKernelGGL((gemm_wide_split_kernel<MT, KC, NTW, W8>), dim3(w.G * w.S), block, 0, st, p, w.S, w.chunks);
+    hipLaunchKernelGGL((gemm_wide_split_kernel<MT, KC, NTW, WV, W8>), dim3(w.G * w.S), block, 0, st, p, w.S, w.chunks);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const dim3 rgrid(wide_groups(p.NT), MT);
     switch (p.epi) {
-      case kEpiStore: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, kEpiStore>), rgrid, block, 0, st, p, w.S); break;
-      case kEpiGelu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, kEpiGelu>), rgrid, block, 0, st, p, w.S); break;
-      case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, kEpiSwiglu>), rgrid, block, 0, st, p, w.S); break;
-      case kEpiResid: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, kEpiResid>), rgrid, block, 0, st, p, w.S); break;
-      default: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, kEpiQkv>), rgrid, block, 0, st, p, w.S); break;
+      case kEpiStore: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, WV, kEpiStore>), rgrid, rblock, 0, st, p, w.S); break;
+      case kEpiGelu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, WV, kEpiGelu>), rgrid, rblock, 0, st, p, w.S); break;
+      case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, WV, kEpiSwiglu>), rgrid, rblock, 0, st, p, w.S); break;
+      case kEpiResid: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, WV, kEpiResid>), rgrid, rblock, 0, st, p, w.S); break;
+      default: hipLaunchKernelGGL((gemm_wide_reduce_kernel<MT, NTW, WV, kEpiQkv>), rgrid, rblock, 0, st, p, w.S); break;
     }
     return hipGetLastError();
   }
   const dim3 grid(w.G);
   switch (p.epi) {
-    case kEpiStore: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiStore, W8>), grid, block, 0, st, p, w.chunks); break;
-    case kEpiGelu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiGelu, W8>), grid, block, 0, st, p, w.chunks); break;
-    case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiSwiglu, W8>), grid, block, 0, st, p, w.chunks); break;
-    case kEpiResid: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiResid, W8>), grid, block, 0, st, p, w.chunks); break;
-    default: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, kEpiQkv, W8>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiStore: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, WV, kEpiStore, W8>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiGelu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, WV, kEpiGelu, W8>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiSwiglu: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, WV, kEpiSwiglu, W8>), grid, block, 0, st, p, w.chunks); break;
+    case kEpiResid: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, WV, kEpiResid, W8>), grid, block, 0, st, p, w.chunks); break;
+    default: hipLaunchKernelGGL((gemm_wide_kernel<MT, KC, NTW, WV, kEpiQkv, W8>), grid, block, 0, st, p, w.chunks); break;
   }
   return hipGetLastError();
 }

@@ -22,7 +22,8 @@ WidePlan wide_plan(int NT, int KT, int M, bool w8) {
   w.w8 = w8;
   w.KC = wide_kc(w.MT, w8);
   w.NTW = wide_ntw(w.MT, w8);
-  w.G = (NT + kWideWaves * w.NTW - 1) / (kWideWaves * w.NTW);
+  w.WV = wide_waves(w.MT, w8);
+  w.G = (NT + w.WV * w.NTW - 1) / (w.WV * w.NTW);
   w.chunks = (KT + w.KC - 1) / w.KC;
   // Split count: the work-groups a CU holds at once (LDS of the split
   // kernel, waves per SIMD the registers allow) give the launch's slots; a
@@ -33,8 +34,9 @@ WidePlan wide_plan(int NT, int KT, int M, bool w8) {
   // half-empty second round, 16 % slower), 2 for 250 at two per CU.
   const bool staged = wide_staged(w.MT, w8);
   const long lds = 2L * w.MT * w.KC * 1024 +
-                   (staged ? static_cast<long>(wide_stages(w.MT, w8)) * kWideWaves * w.NTW * (w8 ? w.KC / 2 : w.KC) * 1024 : 0);
-  const int occ = std::max(1, std::min(static_cast<int>(kLdsBytes / lds), waves_per_simd(w.MT)));
+                   (staged ? static_cast<long>(wide_stages(w.MT, w8)) * w.WV * w.NTW * (w8 ? w.KC / 2 : w.KC) * 1024 : 0);
+  const int by_regs = 4 * waves_per_simd(w.MT, w8) / w.WV;   // work-groups per CU the registers allow
+  const int occ = std::max(1, std::min(static_cast<int>(kLdsBytes / lds), by_regs));
   const long slots = static_cast<long>(kCUs) * occ;
   long best = -1;
   w.S = 1;
@@ -48,7 +50,7 @@ WidePlan wide_plan(int NT, int KT, int M, bool w8) {
 }
 
 size_t wide_part_bytes(const WidePlan& w) {
-  return w.S > 1 ? static_cast<size_t>(w.S) * w.G * kWideWaves * w.NTW * w.MT * 128 * sizeof(float) : 0;
+  return w.S > 1 ? static_cast<size_t>(w.S) * w.G * w.WV * w.NTW * w.MT * 128 * sizeof(float) : 0;
 }
 
 int wide_groups(int NT) { return (NT + kNormTiles - 1) / kNormTiles; }

@@ -27,20 +27,12 @@ constexpr int kActRowsBf16 = 8;
 constexpr int kActRowsF32 = 16;
 
 // Wide GEMM (bf16 activations, more than 8 rows; gemm_wide.hip).
-constexpr int kWideWaves = 4;          // waves per work-group
 constexpr int kNormTiles = 8;          // n-tiles per norm group (128 columns)
 constexpr int kWideMT[] = {2, 3, 4, 5, 6, 8, 10, 12, 14, 16, 18, 20};   // compiled M-tile counts
 
-// n-tiles per wave: 2, and 4 for bf16 weights at 14 and 16 M tiles (16
-// n-tiles per work-group halve the activation copies per weight byte, which
-// with the weights share each CU's outstanding L2 requests: 70B steps at
-// B = 16, K = 6 2.5-5 % faster; K = 7 within the run-to-run spread). At 18
-// and 20 M tiles the 288+ accumulators per wave spill, and FP8 codes
-// measured no gain (10 M tiles) or a loss (18). (With register-held
-// weights, 4 at 14 M tiles ran the 70B W_1 and W_2 22-24 % faster than 2;
-// the staged loop beats both.)
-constexpr bool wide_four(int MT, bool w8) { return !w8 && (MT == 14 || MT == 16); }
-constexpr int wide_ntw(int MT, bool w8) { return wide_four(MT, w8) ? 4 : 2; }
+// n-tiles per wave. (With register-held weights, 4 at 14 M tiles ran the
+// 70B W_1 and W_2 22-24 % faster than 2; the staged loop beats both.)
+constexpr int wide_ntw(int, bool) { return 2; }
 
 // Where the weights go through LDS too (wide_mainloop_staged): from 14 M
 // tiles for bf16 weights, where one wave per SIMD with register-held weights
@@ -49,17 +41,29 @@ constexpr int wide_ntw(int MT, bool w8) { return wide_four(MT, w8) ? 4 : 2; }
 // three work-groups per CU is faster.
 constexpr bool wide_staged(int MT, bool w8) { return MT >= (w8 ? 8 : 14); }
 
+// Waves per work-group: 4, and 8 (two per SIMD, 16 n-tiles per group)
+// where bf16 weights go through LDS: the activation copies per weight byte
+// halve, which with the weights share each CU's outstanding L2 requests,
+// and each SIMD has a second wave to issue while one waits (70B steps at
+// B = 16: K = 6 53.9 -> 53.3 ms, K = 8 66.0 -> 59.6 ms, against 4-wave
+// groups; 4 n-tiles per wave in 4 waves instead spills its 288
+// accumulators from 18 M tiles). FP8 codes keep 4 waves.
+constexpr int wide_waves(int MT, bool w8) { return !w8 && wide_staged(MT, w8) ? 8 : 4; }
+
 // LDS weight stages of the staged loop: 4 (3 and 5 measured the same: the
 // wait for a chunk's activations also waits for every copy issued before
 // them, so each chunk's weights get two steps to land however deep the
-// ring), or 2 with 4 n-tiles per wave, whose 32 KiB stages leave no room for
-// a third beside the activation buffers at 16 M tiles (at 14 a third
-// measured no faster): the weights then land with the activations.
-constexpr int wide_stages(int MT, bool w8) { return wide_four(MT, w8) ? 2 : 4; }
+// ring), or with 8 waves, whose 32 KiB stages leave no room for more beside
+// the activation buffers, 2: the weights then land with the activations.
+constexpr int wide_stages(int MT, bool w8) { return wide_waves(MT, w8) == 8 ? 2 : 4; }
 
 // Waves per SIMD the register allocation must allow (the compiler would
-// otherwise hoist every LDS fragment read of a chunk into registers).
-constexpr int waves_per_simd(int MT) { return MT > 12 ? 1 : MT <= 6 ? 3 : 2; }
+// otherwise hoist every LDS fragment read of a chunk into registers): with
+// 4-wave work-groups, 1 from 14 M tiles (one work-group per CU), else 2-3;
+// 8-wave work-groups need two.
+constexpr int waves_per_simd(int MT, bool w8) {
+  return wide_waves(MT, w8) == 8 ? 2 : MT > 12 ? 1 : MT <= 6 ? 3 : 2;
+}
 
 // k-tiles per chunk, whole pairs (activation blocks, FP8 codes): the two
 // chunk buffers (2 MT KC KiB of LDS) leave room for two to three
@@ -78,9 +82,10 @@ constexpr int kPerLane = 32;
 constexpr size_t kRowStatBytes = 24;   // sizeof(RowStat), sampling.hip
 
 // ---- launch plans ------------------------------------------------------
-// Wide GEMM: M tiles, k-tiles per chunk, n-tiles per wave, column groups
-// (4 NTW n-tiles each), k splits and chunks of one launch.
-struct WidePlan { int MT, KC, NTW, G, S, chunks; bool w8; };
+// Wide GEMM: M tiles, k-tiles per chunk, n-tiles per wave, waves per
+// work-group, column groups (WV NTW n-tiles each), k splits and chunks of
+// one launch.
+struct WidePlan { int MT, KC, NTW, WV, G, S, chunks; bool w8; };
 WidePlan wide_plan(int NT, int KT, int M, bool w8);   // w8: FP8 weight codes
 size_t wide_part_bytes(const WidePlan& w);           // workspace for the split-K partials
 int wide_groups(int NT);                             // norm groups (8 n-tiles each)
