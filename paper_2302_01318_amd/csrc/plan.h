@@ -42,34 +42,41 @@ constexpr int wide_ntw(int, bool) { return 2; }
 constexpr bool wide_staged(int MT, bool w8) { return MT >= (w8 ? 8 : 14); }
 
 // Waves per work-group: 4, and 8 (two per SIMD, 16 n-tiles per group)
-// where bf16 weights go through LDS: the activation copies per weight byte
-// halve, which with the weights share each CU's outstanding L2 requests,
-// and each SIMD has a second wave to issue while one waits (70B steps at
-// B = 16: K = 6 53.9 -> 53.3 ms, K = 8 66.0 -> 59.6 ms, against 4-wave
-// groups; 4 n-tiles per wave in 4 waves instead spills its 288
-// accumulators from 18 M tiles). FP8 codes keep 4 waves.
-constexpr int wide_waves(int MT, bool w8) { return !w8 && wide_staged(MT, w8) ? 8 : 4; }
+// from 8 M tiles with bf16 weights and wherever FP8 codes go through LDS:
+// the activation copies per weight byte halve, which with the weights
+// share each CU's outstanding L2 requests, and each SIMD has a second wave
+// to issue while one waits. 70B steps at B = 16 against 4-wave groups: bf16
+// K = 3 / 4 / 5 44.1 / 48.8 / 52.1 -> 43.4 / 48.1 / 50.3 ms, K = 6 53.9 ->
+// 52.6 ms, K = 8 66.0 -> 59.6 ms; FP8 K = 6 / 8 50.9 / 58.0 -> 46.7 /
+// 53.7 ms. (4 n-tiles per wave in 4 waves instead spills its 288
+// accumulators from 18 M tiles.)
+constexpr int wide_waves(int MT, bool w8) { return (w8 ? wide_staged(MT, w8) : MT >= 8) ? 8 : 4; }
 
-// LDS weight stages of the staged loop: 4 (3 and 5 measured the same: the
-// wait for a chunk's activations also waits for every copy issued before
-// them, so each chunk's weights get two steps to land however deep the
-// ring), or with 8 waves, whose 32 KiB stages leave no room for more beside
-// the activation buffers, 2: the weights then land with the activations.
-constexpr int wide_stages(int MT, bool w8) { return wide_waves(MT, w8) == 8 ? 2 : 4; }
+// LDS weight stages of the staged loop: 4 (3 and 5 measured the same with
+// 4-wave groups: the wait for a chunk's activations also waits for every
+// copy issued before them, so each chunk's weights get two steps to land
+// however deep the ring). The 32 KiB bf16 stages of 8-wave groups leave
+// room beside the activation buffers for 3 at 14 M tiles (weights two
+// steps ahead, 1.7 % faster than 2) and 2 above (the weights then land
+// with the activations); 8-wave FP8 stages are 16 KiB, so 4.
+constexpr int wide_stages(int MT, bool w8) {
+  return w8 || wide_waves(MT, w8) == 4 ? 4 : MT == 14 ? 3 : 2;
+}
 
 // Waves per SIMD the register allocation must allow (the compiler would
-// otherwise hoist every LDS fragment read of a chunk into registers): with
-// 4-wave work-groups, 1 from 14 M tiles (one work-group per CU), else 2-3;
-// 8-wave work-groups need two.
+// otherwise hoist every LDS fragment read of a chunk into registers): two
+// for 8-wave work-groups (one group per CU), else 3 up to 6 M tiles (three
+// 4-wave groups per CU) and 1 from 14 (FP8 codes below 8 M tiles are the
+// only 4-wave groups past 6).
 constexpr int waves_per_simd(int MT, bool w8) {
   return wide_waves(MT, w8) == 8 ? 2 : MT > 12 ? 1 : MT <= 6 ? 3 : 2;
 }
 
 // k-tiles per chunk, whole pairs (activation blocks, FP8 codes): the two
-// chunk buffers (2 MT KC KiB of LDS) leave room for two to three
-// work-groups per CU up to 12 M tiles (one from 14, where registers allow
-// one wave per SIMD; from 16 the staged loop also needs LDS for its weight
-// ring) and hold a norm group's output tile (4 MT KiB).
+// chunk buffers (2 MT KC KiB of LDS) leave room for the work-groups a CU
+// holds (three 4-wave groups up to 6 M tiles, one 8-wave group from 8;
+// the staged loop also needs LDS for its weight ring) and hold a norm
+// group's output tile (4 MT KiB).
 constexpr int wide_kc(int MT, bool w8) { return wide_staged(MT, w8) ? 2 : MT <= 10 ? 4 : 2; }
 
 // Decode attention: positions per wave (two 32-position blocks).
