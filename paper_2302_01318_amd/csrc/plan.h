@@ -48,8 +48,10 @@ constexpr bool wide_staged(int MT, bool w8) { return MT >= (w8 ? 8 : 14); }
 // to issue while one waits. 70B steps at B = 16 against 4-wave groups: bf16
 // K = 3 / 4 / 5 44.1 / 48.8 / 52.1 -> 43.4 / 48.1 / 50.3 ms, K = 6 53.9 ->
 // 52.6 ms, K = 8 66.0 -> 59.6 ms; FP8 K = 6 / 8 50.9 / 58.0 -> 46.7 /
-// 53.7 ms. (4 n-tiles per wave in 4 waves instead spills its 288
-// accumulators from 18 M tiles.)
+// 53.7 ms. Below 8 M tiles, where three 4-wave groups share a CU, 8-wave
+// groups measured 2-12 % slower (bf16 and FP8, B = 4 and B = 16 at K <= 2).
+// (4 n-tiles per wave in 4 waves instead spills its 288 accumulators from
+// 18 M tiles.)
 constexpr int wide_waves(int MT, bool w8) { return (w8 ? wide_staged(MT, w8) : MT >= 8) ? 8 : 4; }
 
 // LDS weight stages of the staged loop: 4 (3 and 5 measured the same with
