@@ -110,17 +110,19 @@ def test_small_bf16_many_rows(sps):
 
 @pytest.mark.parametrize("B,K", [(12, 8), (16, 8)])
 def test_small_bf16_large_batch(sps, B, K):
-    # 108 and 144 rows: the widest single GEMM launches (14 and 20 M tiles)
+    # 108 and 144 rows: the widest single GEMM launches (14 and 18 M tiles)
     g = np.random.default_rng(B)
     verify_parity(sps, SMALL.with_(ffn="gelu"), B, K, [int(x) for x in g.integers(0, 200, B)], 40 + B, 2e-2,
                   check_kv=False)
 
 
-@pytest.mark.parametrize("B,K", [(16, 8), (25, 4), (4, 8), (12, 7), (11, 9)])
+@pytest.mark.parametrize("B,K", [(16, 8), (25, 4), (4, 8), (12, 7), (11, 9), (8, 7), (16, 4)])
 def test_small_bf16_odd_depth_wide(sps, B, K):
     """Contraction depths of 5, 6 and 9 k-tiles (d_model 160, three 64-wide
-    heads, d_ff 288) at 144, 125, 36, 96 and 110 rows (18, 16, 5, 12 and 14
-    M tiles): wide-GEMM chunks whose last k-tile pair is half past the end."""
+    heads, d_ff 288) at 144, 125, 36, 96, 110, 64 and 80 rows (18, 16, 5,
+    12, 14, 8 and 10 M tiles: 4-wave groups, 8-wave groups with
+    register-held weights, 8-wave groups with staged weights): wide-GEMM
+    chunks whose last k-tile pair is half past the end."""
     g = np.random.default_rng(B + 900)
     verify_parity(sps, SMALL.with_(d_model=160, d_ff=288, ffn="swiglu"), B, K,
                   [int(x) for x in g.integers(0, 150, B)], 90 + B, 2e-2, check_kv=False)
