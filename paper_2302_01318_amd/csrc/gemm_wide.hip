@@ -481,15 +481,18 @@ void gemm_wide_kernel(const GemmParams p, int chunks) {
   }
 }
 
-// Split s of column group g (work-group g + s G): chunks [s C / S, (s+1) C / S)
-// into the partial buffer.
+// Split s of column group g (work-group s + g S): chunks [s C / S, (s+1) C / S)
+// into the partial buffer. Work-group b runs on XCD b % 8, so with the split
+// index fastest every XCD streams the activations of one split (S dividing 8;
+// two or three splits for S = 3, 6) and its L2 holds that slice for all the
+// column groups it runs, instead of every split's slice.
 template <int MT, int KC, int NTW, int WV, bool W8>
 __global__ __launch_bounds__(WV * 64) __attribute__((amdgpu_waves_per_eu(wide_waves_per_simd<MT, W8>())))
 void gemm_wide_split_kernel(const GemmParams p, int S, int chunks) {
   __shared__ bf16x8 s_a[2 * MT * KC][64];
   __shared__ bf16x8 s_w[wide_staged(MT, W8) ? wide_stages(MT, W8) * WV * NTW * (W8 ? KC / 2 : KC) : 1][64];
   const int G = (p.NT + WV * NTW - 1) / (WV * NTW);
-  const int g = blockIdx.x % G, s = blockIdx.x / G;
+  const int s = blockIdx.x % S, g = blockIdx.x / S;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c0 = static_cast<int>(static_cast<long>(s) * chunks / S);
   const int c1 = static_cast<int>(static_cast<long>(s + 1) * chunks / S);
@@ -513,8 +516,8 @@ void gemm_wide_split_kernel(const GemmParams p, int S, int chunks) {
 
 // Sum of the S partials of norm group gs = blockIdx.x, M tile mt =
 // blockIdx.y, in split order, then the epilogue of that tile. Thread t sums
-// lane t % 32 of n-tile 8 gs + t / 32, which the split kernel's work-group
-// (8 gs + t / 32) / (WV NTW) holds in wave ((8 gs + t / 32) % (WV NTW)) / NTW:
+// lane t % 32 of n-tile 8 gs + t / 32, which column group (8 gs + t / 32) /
+// (WV NTW) of the split kernel holds in wave ((8 gs + t / 32) % (WV NTW)) / NTW:
 // one coalesced 16 B load per split.
 template <int MT, int NTW, int WV, int EPI>
 __global__ __launch_bounds__(kNormTiles * 32) void gemm_wide_reduce_kernel(const GemmParams p, int S) {
