@@ -27,22 +27,63 @@ __host__ __device__ __forceinline__ int rope_pack_index(int f, int DH) {
 
 // Row scale of the input RMSNorm for local row m (1 when the GEMM has no
 // normed input): rs = 1 / sqrt(sum_g ss_in[g][m] / d + eps). One wave sums
-// the groups; every lane returns the result.
-__device__ __forceinline__ float norm_scale(const GemmParams& p, int m, int lane) {
+// the groups, lane l those of index l, l + 64, ... in that order; every lane
+// returns the result. norm_first loads a lane's first group and norm_finish
+// adds the rest and reduces, so that callers can issue the first loads of
+// several rows together.
+__device__ __forceinline__ float norm_first(const GemmParams& p, int m, int lane) {
+  return p.ss_in && m < p.M && lane < p.ng_in ? p.ss_in[static_cast<size_t>(lane) * p.Mtot + p.m0 + m] : 0.f;
+}
+__device__ __forceinline__ float norm_finish(const GemmParams& p, int m, int lane, float s) {
   if (!p.ss_in || m >= p.M) return 1.f;
-  float s = 0.f;
-  for (int g = lane; g < p.ng_in; g += 64) s += p.ss_in[static_cast<size_t>(g) * p.Mtot + p.m0 + m];
+  for (int g = lane + 64; g < p.ng_in; g += 64) s += p.ss_in[static_cast<size_t>(g) * p.Mtot + p.m0 + m];
   s = wave_sum(s);
   return 1.0f / sqrtf(s * p.inv_d + p.eps);
 }
+__device__ __forceinline__ float norm_scale(const GemmParams& p, int m, int lane) {
+  return norm_finish(p, m, lane, norm_first(p, m, lane));
+}
+
+// Inputs of an element's epilogue that live in memory: the old residual
+// value and the norm gain (kEpiResid), the sequence's length and the rotary
+// (cos, sin) of a q / k pair (kEpiQkv). Loading them for several elements
+// before any of their stores lets a thread's loads overlap: in a loop of
+// whole elements the compiler keeps each load behind the previous element's
+// stores, which may alias it.
+struct EpiIn {
+  float a, b;
+  int len;
+};
+template <int EPI>
+__device__ __forceinline__ EpiIn epilogue_inputs(const GemmParams& p, int gm, int nt, int col) {
+  EpiIn in{0.f, 0.f, 0};
+  const int n = nt * 16 + col;
+  if (EPI == kEpiResid) {
+    if (n < p.n_valid) {
+      in.a = p.h[static_cast<size_t>(gm) * p.n_valid + n];
+      in.b = p.gain[n];
+    }
+  } else if (EPI == kEpiQkv) {
+    in.len = p.lengths[gm / p.Mps];
+    if (n < 2 * p.H * p.DH && col < 8) {
+      const int f = ((n % p.DH) / 16) * 8 + col;
+      const float2 cs = p.rope[static_cast<size_t>(gm) * (p.DH / 2) + f];   // cos, sin (embed_kernel)
+      in.a = cs.x;
+      in.b = cs.y;
+    }
+  }
+  return in;
+}
 
 // Epilogue of output element (global row gm, packed column 16 nt + col) with
-// value v (already scaled by the row's norm scale). v2 is the value of
-// column 16 nt + col + 8 when col < 8: the SwiGLU up projection of a gate
-// column, or the rotate-half partner of a q / k dim. Returns h^2 of the new
-// residual value for kEpiResid (0 for columns past n_valid), else 0.
+// value v (already scaled by the row's norm scale) and its memory inputs in.
+// v2 is the value of column 16 nt + col + 8 when col < 8: the SwiGLU up
+// projection of a gate column, or the rotate-half partner of a q / k dim.
+// Returns h^2 of the new residual value for kEpiResid (0 for columns past
+// n_valid), else 0.
 template <typename T, int EPI>
-__device__ __forceinline__ float epilogue_element(const GemmParams& p, int gm, int nt, int col, float v, float v2) {
+__device__ __forceinline__ float epilogue_apply(const GemmParams& p, int gm, int nt, int col, float v, float v2,
+                                                const EpiIn& in) {
   if (EPI == kEpiStore) {
     const int n = nt * 16 + col;
     if (n < p.n_valid) p.out[static_cast<size_t>(gm) * p.ldo + n] = v;
@@ -57,25 +98,23 @@ __device__ __forceinline__ float epilogue_element(const GemmParams& p, int gm, i
   } else if (EPI == kEpiResid) {
     const int n = nt * 16 + col;
     if (n < p.n_valid) {
-      float* hp = p.h + static_cast<size_t>(gm) * p.n_valid + n;
-      const float hn = *hp + v;
-      *hp = hn;
-      store_act(static_cast<T*>(p.u), p.uplane, static_cast<size_t>(gm) * p.ldu + n, hn * p.gain[n]);
+      const float hn = in.a + v;
+      p.h[static_cast<size_t>(gm) * p.n_valid + n] = hn;
+      store_act(static_cast<T*>(p.u), p.uplane, static_cast<size_t>(gm) * p.ldu + n, hn * in.b);
       return hn * hn;
     }
   } else {  // kEpiQkv
     const int n = nt * 16 + col;
     const int HD = p.H * p.DH;
     const int b = gm / p.Mps, jr = gm % p.Mps;
-    const int pos = p.lengths[b] + p.pos_offset + jr;
+    const int pos = in.len + p.pos_offset + jr;
     const bool ok = pos >= 0 && pos < p.T_cap;
     if (!ok && n == 0) atomicOr(p.err, kErrCapacity);
     if (n < 2 * HD) {                        // q or k: rotate the pair held by columns col, col + 8
       if (col < 8) {
         const int hh = (n % HD) / p.DH, pi = n % p.DH;
         const int f = (pi / 16) * 8 + col;
-        const float2 cs = p.rope[static_cast<size_t>(gm) * (p.DH / 2) + f];   // cos, sin (embed_kernel)
-        const float c = cs.x, s = cs.y;
+        const float c = in.a, s = in.b;
         const float y1 = v * c - v2 * s, y2 = v2 * c + v * s;
         const int half = p.DH / 2;
         if (n < HD) {
@@ -95,6 +134,12 @@ __device__ __forceinline__ float epilogue_element(const GemmParams& p, int gm, i
     }
   }
   return 0.f;
+}
+
+// One element's whole epilogue (loads, then epilogue_apply).
+template <typename T, int EPI>
+__device__ __forceinline__ float epilogue_element(const GemmParams& p, int gm, int nt, int col, float v, float v2) {
+  return epilogue_apply<T, EPI>(p, gm, nt, col, v, v2, epilogue_inputs<EPI>(p, gm, nt, col));
 }
 
 }  // namespace sps

@@ -386,13 +386,22 @@ __device__ __forceinline__ void wide_mainloop_staged(const GemmParams& p, int g,
 }
 
 // Row scales of the input RMSNorm for rows mt0 * 8 .. (mt0 + NMT) * 8 - 1
-// into s_rs (the caller synchronises before use).
-template <int NMT>
+// into s_rs (the caller synchronises before use); NW waves, wave w takes
+// rows w, w + NW, ..., their first loads issued together.
+template <int NMT, int NW>
 __device__ __forceinline__ void wide_row_scales(const GemmParams& p, int mt0, float* s_rs) {
+  constexpr int kR = (NMT * 8 + NW - 1) / NW;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int i = wave; i < NMT * 8; i += static_cast<int>(blockDim.x >> 6)) {
-    const float v = norm_scale(p, mt0 * 8 + i, lane);
-    if (lane == 0) s_rs[i] = v;
+  float v[kR];
+#pragma unroll
+  for (int k = 0; k < kR; ++k) v[k] = norm_first(p, mt0 * 8 + wave + k * NW, lane);
+#pragma unroll
+  for (int k = 0; k < kR; ++k) {
+    const int i = wave + k * NW;
+    if (i < NMT * 8) {
+      const float r = norm_finish(p, mt0 * 8 + i, lane, v[k]);
+      if (lane == 0) s_rs[i] = r;
+    }
   }
 }
 
@@ -403,22 +412,51 @@ template <int NMT, int EPI>
 __device__ __forceinline__ void wide_epilogue_group(const GemmParams& p, int gs, int mt0, float* ep,
                                                     const float* s_rs) {
   using T = bf16;
-  const int M = p.M, r0 = mt0 * 8;
+  constexpr int kN = kNormTiles * NMT * 128;       // elements of the group
+  constexpr int kB = 4;                            // elements per thread whose inputs load together
+  const int M = p.M, r0 = mt0 * 8, bd = blockDim.x;
   if (gs * kNormTiles >= p.NT) return;             // whole group past the last n-tile
-  for (int e = threadIdx.x; e < kNormTiles * NMT * 128; e += blockDim.x) {
-    const int jj = e / (NMT * 128), mtl = (e >> 7) % NMT, i = (e >> 4) & 7, col = e & 15;
-    const int m = r0 + mtl * 8 + i, nt = gs * kNormTiles + jj;
-    if (m >= M || nt >= p.NT) {
-      if (EPI == kEpiResid) ep[e] = 0.f;
-      continue;
+  for (int e0 = threadIdx.x; e0 < kN; e0 += kB * bd) {
+    // Loads only (every product waits for its operands, so the arithmetic
+    // follows below), then each element's arithmetic and stores.
+    float x[kB], x2[kB], sc[kB], sc2[kB];
+    EpiIn in[kB];
+    bool ok[kB];
+#pragma unroll
+    for (int b = 0; b < kB; ++b) {
+      const int e = e0 + b * bd;
+      const int jj = e / (NMT * 128), mtl = (e >> 7) % NMT, i = (e >> 4) & 7, col = e & 15;
+      const int m = r0 + mtl * 8 + i, nt = gs * kNormTiles + jj;
+      ok[b] = e < kN && m < M && nt < p.NT;
+      x[b] = x2[b] = 0.f;
+      sc[b] = sc2[b] = 1.f;
+      in[b] = EpiIn{0.f, 0.f, 0};
+      if (ok[b]) {
+        const bool pair = (EPI == kEpiSwiglu || EPI == kEpiQkv) && col < 8;
+        x[b] = ep[e];
+        if (pair) x2[b] = ep[e + 8];
+        if (p.wscale) {                            // FP8 row scales (NULL for bf16 weights)
+          sc[b] = p.wscale[nt * 16 + col];
+          if (pair) sc2[b] = p.wscale[nt * 16 + col + 8];
+        }
+        in[b] = epilogue_inputs<EPI>(p, p.m0 + m, nt, col);
+      }
     }
-    const float rs = s_rs[mtl * 8 + i];
-    const float* sc = p.wscale;                    // FP8 row scales (NULL for bf16 weights)
-    const float v = ep[e] * rs * (sc ? sc[nt * 16 + col] : 1.f);
-    const float v2 = (EPI == kEpiSwiglu || EPI == kEpiQkv) && col < 8 ? ep[e + 8] * rs * (sc ? sc[nt * 16 + col + 8] : 1.f)
-                                                                      : 0.f;
-    const float sq = epilogue_element<T, EPI>(p, p.m0 + m, nt, col, v, v2);
-    if (EPI == kEpiResid) ep[e] = sq;              // only this thread reads element e here
+#pragma unroll
+    for (int b = 0; b < kB; ++b) {
+      const int e = e0 + b * bd;
+      if (e >= kN) continue;
+      if (!ok[b]) {
+        if (EPI == kEpiResid) ep[e] = 0.f;
+        continue;
+      }
+      const int jj = e / (NMT * 128), mtl = (e >> 7) % NMT, i = (e >> 4) & 7, col = e & 15;
+      const float rs = s_rs[mtl * 8 + i];
+      const float v = x[b] * rs * sc[b];
+      const float v2 = (EPI == kEpiSwiglu || EPI == kEpiQkv) && col < 8 ? x2[b] * rs * sc2[b] : 0.f;
+      const float sq = epilogue_apply<T, EPI>(p, p.m0 + r0 + mtl * 8 + i, gs * kNormTiles + jj, col, v, v2, in[b]);
+      if (EPI == kEpiResid) ep[e] = sq;            // only this thread reads element e here
+    }
   }
   if (EPI == kEpiResid) {
     // Sums of squares of the group's 128 columns per row, in a fixed order.
@@ -474,7 +512,7 @@ void gemm_wide_kernel(const GemmParams p, int chunks) {
           for (int r = 0; r < 4; ++r)
             ep[(((jw + j) * MT + mt) * 8 + (lane >> 4) * 4 + r) * 16 + (lane & 15)] = acc[j][mt][r];
     }
-    if (h == 0) wide_row_scales<MT>(p, 0, s_rs);   // after the first dump: fewer live registers
+    if (h == 0) wide_row_scales<MT, WV>(p, 0, s_rs);   // after the first dump: fewer live registers
     __syncthreads();
     wide_epilogue_group<MT, EPI>(p, blockIdx.x * kGroups + h, 0, ep, s_rs);
     if (h + 1 < kGroups) __syncthreads();          // ep is rewritten for the next group
@@ -531,11 +569,20 @@ __global__ __launch_bounds__(kNormTiles * 32) void gemm_wide_reduce_kernel(const
   const float* src = p.part + (static_cast<size_t>(g) * WV + wave) * wide_part_floats<MT, NTW>() +
                      ((j * MT + mt) * 32 + ln) * 4;
   const size_t split = static_cast<size_t>(G) * WV * wide_part_floats<MT, NTW>();
+  // Every split's load in flight at once (a loop over S would wait for each),
+  // and the row scales' loads beside them; the sum stays in split order.
+  // (Splits past S re-read the last one's slot, an L1 hit, so no load sits
+  // behind a branch.)
+  f32x4 part[kMaxSplits];
+#pragma unroll
+  for (int s = 0; s < kMaxSplits; ++s) part[s] = *reinterpret_cast<const f32x4*>(src + min(s, S - 1) * split);
+  wide_row_scales<1, kNormTiles * 32 / 64>(p, mt, s_rs);   // the block's waves
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < S; ++s) acc += *reinterpret_cast<const f32x4*>(src + s * split);
+#pragma unroll
+  for (int s = 0; s < kMaxSplits; ++s)
+    if (s < S) acc += part[s];
 #pragma unroll
   for (int r = 0; r < 4; ++r) ep[(jj * 8 + (ln >> 4) * 4 + r) * 16 + (ln & 15)] = acc[r];
-  wide_row_scales<1>(p, mt, s_rs);
   __syncthreads();
   wide_epilogue_group<1, EPI>(p, gs, mt, ep, s_rs);
 }
@@ -591,7 +638,7 @@ static hipError_t wide_dispatch(const GemmParams& p, const WidePlan& w, hipStrea
 }
 
 hipError_t launch_gemm_wide(const GemmParams& p, const WidePlan& w, hipStream_t st) {
-  if (w.S > 1 && !p.part) return hipErrorInvalidValue;
+  if ((w.S > 1 && !p.part) || w.S > kMaxSplits) return hipErrorInvalidValue;
   if (w.w8 != (p.wscale != nullptr) || (w.w8 && p.KT % 2)) return hipErrorInvalidValue;
   return w.w8 ? wide_dispatch<true>(p, w, st) : wide_dispatch<false>(p, w, st);
 }

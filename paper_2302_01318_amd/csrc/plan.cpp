@@ -40,7 +40,7 @@ WidePlan wide_plan(int NT, int KT, int M, bool w8) {
   const long slots = static_cast<long>(kCUs) * occ;
   long best = -1;
   w.S = 1;
-  for (int S : {1, 2, 3, 4, 6, 8}) {
+  for (int S : {1, 2, 3, 4, 6, kMaxSplits}) {
     if (S > 1 && S > w.chunks / 2) break;
     const long rounds = (static_cast<long>(w.G) * S + slots - 1) / slots;
     const long cost = rounds * ((w.chunks + S - 1) / S + 8);

@@ -29,6 +29,7 @@ constexpr int kActRowsF32 = 16;
 // Wide GEMM (bf16 activations, more than 8 rows; gemm_wide.hip).
 constexpr int kNormTiles = 8;          // n-tiles per norm group (128 columns)
 constexpr int kWideMT[] = {2, 3, 4, 5, 6, 8, 10, 12, 14, 16, 18, 20};   // compiled M-tile counts
+constexpr int kMaxSplits = 8;          // largest k split of a wide launch (the reduction holds one load per split)
 
 // n-tiles per wave. (With register-held weights, 4 at 14 M tiles ran the
 // 70B W_1 and W_2 22-24 % faster than 2; the staged loop beats both.)

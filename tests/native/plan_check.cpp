@@ -107,7 +107,7 @@ static void check_wide_plans() {
           const WidePlan p = wide_plan(NT, KT, M, w8 != 0);
           CHECK(p.MT * kActRowsBf16 >= M, "wide plan NT %d KT %d M %d: %d M tiles", NT, KT, M, p.MT);
           CHECK((p.WV == 4 || p.WV == 8) && p.G * p.WV * p.NTW >= NT, "wide plan NT %d: %d groups", NT, p.G);
-          CHECK(p.chunks * p.KC >= KT && p.S >= 1 && p.S <= 8, "wide plan KT %d: chunks %d S %d", KT, p.chunks, p.S);
+          CHECK(p.chunks * p.KC >= KT && p.S >= 1 && p.S <= kMaxSplits, "wide plan KT %d: chunks %d S %d", KT, p.chunks, p.S);
           CHECK(!w8 || p.KC % 2 == 0, "FP8 plan with odd chunk");
           const size_t pb = wide_part_bytes(p);
           CHECK(p.S == 1 ? pb == 0 : pb == static_cast<size_t>(p.S) * p.G * p.WV * p.NTW * p.MT * 512,
