@@ -172,14 +172,17 @@ void sps_model_destroy(sps_model_t model);
 /* ---- KV cache -------------------------------------------------------- */
 
 /* Bytes of a KV cache for B sequences of capacity T_cap positions
- * (T_cap % 32 == 0). Layout per (layer, sequence, head): keys in 16-position
- * x 32-dim MFMA tiles, values in 32-position x 16-dim tiles (see DESIGN). */
+ * (T_cap % 32 == 0, 32 <= T_cap <= 2^22; 0 otherwise). Layout per (layer,
+ * sequence, head): keys in 16-position x 32-dim MFMA tiles, values in
+ * 32-position x 16-dim tiles, both in the register order of the attention
+ * kernel's MFMA operands. */
 size_t sps_kv_bytes(const sps_config* cfg, int32_t B, int32_t T_cap);
 
 /* Create a handle over `kv_buf` (sps_kv_bytes bytes) and `lengths`, a device
  * int32 [B] array of committed lengths that the caller initialises. A draft
  * and a target cache of the same batch share one `lengths` array: positions
- * are the same token positions in both. */
+ * are the same token positions in both. SPS_E_SHAPE for a T_cap that is not
+ * a multiple of 32 in [32, 2^22]. */
 sps_status sps_kv_create(const sps_config* cfg, int32_t B, int32_t T_cap, void* kv_buf,
                          int32_t* lengths, sps_kv_t* out /*host*/);
 void sps_kv_destroy(sps_kv_t kv);
@@ -198,7 +201,7 @@ sps_status sps_kv_read(sps_kv_t kv, int32_t layer, int32_t b, int32_t pos0, int3
  * up to max_tokens_per_seq new tokens each against a cache of capacity
  * T_cap: any call with B sequences and at most that many tokens per sequence
  * (a verify step takes K + 1, a draft step 2) fits. 0 for an invalid config,
- * T_cap < 32, or a request no call admits (max_tokens_per_seq > 64 or
+ * T_cap outside [32, 2^22], or a request no call admits (max_tokens_per_seq > 64 or
  * B * max_tokens_per_seq > 160). */
 size_t sps_workspace_bytes(const sps_config* cfg, int32_t B, int32_t max_tokens_per_seq,
                            int32_t T_cap);

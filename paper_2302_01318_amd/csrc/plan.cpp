@@ -205,7 +205,7 @@ WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
 }
 
 size_t workspace_bytes(const sps_config* cfg, int B, int max_tokens_per_seq, int T_cap) {
-  if (!valid_config(cfg) || B < 1 || max_tokens_per_seq < 1 || T_cap < 32) return 0;
+  if (!valid_config(cfg) || B < 1 || max_tokens_per_seq < 1 || T_cap < 32 || T_cap > kMaxTCap) return 0;
   // No call runs more tokens per sequence or more rows than this.
   if (max_tokens_per_seq > kMaxTokensPerSeq || static_cast<long>(B) * max_tokens_per_seq > kMaxRows) return 0;
   return make_ws(make_layout(cfg), B, max_tokens_per_seq, T_cap).total;

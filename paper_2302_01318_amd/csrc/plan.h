@@ -16,6 +16,7 @@ namespace sps {
 constexpr int kMaxTokensPerSeq = 64;   // new tokens per sequence in one forward
 constexpr int kMaxRows = 160;          // B * tokens per sequence in one forward
 constexpr int kMaxK = 63;              // lookahead
+constexpr int kMaxTCap = 1 << 22;      // KV capacity (positions): keeps grid extents and partial counts far inside their ranges
 
 // ---- GPU and kernel geometry -------------------------------------------
 constexpr int kCUs = 256;              // compute units of the MI355X

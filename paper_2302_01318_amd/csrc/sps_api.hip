@@ -389,7 +389,7 @@ sps_status sps_model_create(const sps_config* cfg, void* packed, sps_model_t* ou
 void sps_model_destroy(sps_model_t model) { delete model; }
 
 size_t sps_kv_bytes(const sps_config* cfg, int32_t B, int32_t T_cap) {
-  if (!valid_config(cfg) || B < 1 || T_cap < 32 || T_cap % 32) return 0;
+  if (!valid_config(cfg) || B < 1 || T_cap < 32 || T_cap % 32 || T_cap > sps::kMaxTCap) return 0;
   const Layout L = make_layout(cfg);
   return static_cast<size_t>(L.L) * 2 * B * L.H * static_cast<size_t>(T_cap) * L.DH * L.es;
 }
@@ -400,7 +400,7 @@ sps_status sps_kv_create(const sps_config* cfg, int32_t B, int32_t T_cap, void* 
   *out = nullptr;
   if (!valid_config(cfg)) return SPS_E_SHAPE;
   if (!kv_buf || !lengths || B < 1) return SPS_E_INVALID;
-  if (T_cap < 32 || T_cap % 32) return SPS_E_SHAPE;
+  if (T_cap < 32 || T_cap % 32 || T_cap > sps::kMaxTCap) return SPS_E_SHAPE;
   sps_kv_s* kv = new (std::nothrow) sps_kv_s;
   if (!kv) return SPS_E_CAPACITY;
   kv->cfg = *cfg;

@@ -142,7 +142,9 @@ static void check_extremes() {
   CHECK(workspace_bytes(&c, 1, INT_MAX, 2112) == 0, "huge token count admitted");
   CHECK(workspace_bytes(&c, INT_MAX, 1, 2112) == 0, "huge batch admitted");
   CHECK(workspace_bytes(&c, 1, 65, 2112) == 0, "65 tokens per sequence admitted");
-  CHECK(workspace_bytes(&c, 1, 64, INT_MAX) > 0, "largest capacity refused");
+  CHECK(workspace_bytes(&c, 1, 64, kMaxTCap) > 0, "largest capacity refused");
+  CHECK(workspace_bytes(&c, 1, 64, kMaxTCap + 32) == 0, "capacity past the largest admitted");
+  CHECK(workspace_bytes(&c, 1, 64, INT_MAX) == 0, "INT_MAX capacity admitted");
   CHECK(workspace_bytes(&c, 1, 5, 31) == 0, "capacity below 32 admitted");
   sps_sampling s{1.f, 0, 1.f};
   CHECK(check_sampling(s, 32000) == SPS_OK, "plain sampling refused");

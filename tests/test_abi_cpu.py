@@ -56,6 +56,14 @@ def test_config_validation_and_sizes(sps):
     assert sps.lib.sps_kv_bytes(ctypes.byref(good), 1, 100) == 0          # T_cap % 32
     assert sps.lib.sps_kv_bytes(ctypes.byref(good), 1, 2304) == 80 * 2 * 64 * 2304 * 128 * 2
     assert sps.lib.sps_workspace_bytes(ctypes.byref(good), 0, 5, 2304) == 0
+    # KV capacity at most 2^22 positions
+    assert sps.lib.sps_kv_bytes(ctypes.byref(good), 1, 1 << 22) == 80 * 2 * 64 * (1 << 22) * 128 * 2
+    assert sps.lib.sps_kv_bytes(ctypes.byref(good), 1, (1 << 22) + 32) == 0
+    assert sps.lib.sps_workspace_bytes(ctypes.byref(good), 1, 5, (1 << 22) + 32) == 0
+    assert sps.lib.sps_workspace_bytes(ctypes.byref(good), 1, 5, 1 << 22) > 0
+    h = ctypes.c_void_p()
+    assert sps.lib.sps_kv_create(ctypes.byref(good), 1, (1 << 22) + 32, ctypes.c_void_p(1), ctypes.c_void_p(1),
+                                 ctypes.byref(h)) == 2 and not h.value
 
 
 def test_fp8_config_and_slots(sps):
