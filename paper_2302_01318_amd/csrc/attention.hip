@@ -98,12 +98,13 @@ __device__ __forceinline__ void load_block(const T* __restrict__ kr, const T* __
 }
 
 // Work-group of the grid (G, H, B) with dispatch-order index L (x fastest):
-// every (sequence b, head h) has G position groups. With last_last, the
-// first (G - 1) H B work-groups take groups 0 .. G - 2 of each (sequence,
-// head) in turn and the last H B work-groups their last group; otherwise
-// work-group L takes group L % G of (sequence, head) L / G.
-__device__ __forceinline__ void attn_group(bool last_last, int* h, int* b, int* g) {
-  if (!last_last) {
+// every (sequence b, head h) has G position groups. With short_first, the
+// first H B work-groups take the last group of each (sequence, head), partly
+// filled or empty, and the rest groups 0 .. G - 2 of each (sequence, head) in
+// turn, neighbouring regions of its cache; otherwise work-group L takes
+// group L % G of (sequence, head) L / G.
+__device__ __forceinline__ void attn_group(bool short_first, int* h, int* b, int* g) {
+  if (!short_first) {
     *g = static_cast<int>(blockIdx.x);
     *h = static_cast<int>(blockIdx.y);
     *b = static_cast<int>(blockIdx.z);
@@ -111,14 +112,14 @@ __device__ __forceinline__ void attn_group(bool last_last, int* h, int* b, int* 
   }
   const long G = gridDim.x, H = gridDim.y;
   const long L = blockIdx.x + G * (blockIdx.y + H * static_cast<long>(blockIdx.z));
-  const long nfull = (G - 1) * H * gridDim.z;
+  const long nlast = H * gridDim.z;
   long hb;
-  if (L < nfull) {
-    hb = L / (G - 1);
-    *g = static_cast<int>(L % (G - 1));
-  } else {
-    hb = L - nfull;
+  if (L < nlast) {
+    hb = L;
     *g = static_cast<int>(G - 1);
+  } else {
+    hb = (L - nlast) / (G - 1);              // G > 1 here: L < G H B
+    *g = static_cast<int>((L - nlast) % (G - 1));
   }
   *h = static_cast<int>(hb % H);
   *b = static_cast<int>(hb / H);
@@ -131,24 +132,21 @@ __device__ __forceinline__ void attn_group(bool last_last, int* h, int* b, int* 
 // to 16 new tokens per sequence, every verify and draft step) the four
 // waves' partials are merged in LDS and the work-group writes one partial
 // per 4 WP positions; with more query tiles (prefill chunks) every wave
-// writes its own. Work-groups take the groups of one (sequence, head) in
-// position order, neighbouring regions of its cache; with last_last (set
-// where the full groups are at most two per CU) every (sequence, head)'s
-// last group, partly filled or empty, runs after all the others, so the full
-// ones spread evenly over the CUs (7B at ctx 2048: 256 full groups, one per
-// CU, beside 32 short ones).
+// writes its own. With short_first (set by short_first_order) the short
+// last groups run first and finish while the full groups start, instead of
+// landing as a third work-group beside two full ones on some CUs.
 template <typename T, int DH, int QT, int WP, int KP = 1, bool NTL = false>
 __global__ __launch_bounds__(256) void attn_partial_kernel(const T* __restrict__ q, const T* __restrict__ kc,
                                                            const T* __restrict__ vc,
                                                            const int32_t* __restrict__ lengths, int pos_offset,
-                                                           int Mps, int H, int T_cap, int NP, bool last_last,
+                                                           int Mps, int H, int T_cap, int NP, bool short_first,
                                                            float c_log2,
                                                            float* __restrict__ part) {
   constexpr bool kMerge = QT == 1;
   constexpr int kPre = KP;   // blocks whose loads are issued together
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int h, b, g;
-  attn_group(last_last, &h, &b, &g);
+  attn_group(short_first, &h, &b, &g);
   const int r16 = lane & 15, grp = lane >> 4;
   const int len = lengths[b] + pos_offset;        // position of query 0
   int nkv = len + Mps;
@@ -298,12 +296,13 @@ __global__ __launch_bounds__(DH) void attn_combine_kernel(const float* __restric
 
 
 // Whether the partial kernel runs every (sequence, head)'s last position
-// group after the others: measured per kernel trace, 7B at ctx 2048 (256
-// full groups) 11.5 -> 10.3 us, 70B at ctx 2048 (512) and the 3072-wide draft
-// (192) unchanged; with 2048 full groups (70B at B = 4 or ctx 8192) the
-// other order is 2.5-4 % faster.
-static bool last_last(int groups, int H, int B) {
-  return static_cast<long>(groups - 1) * H * B <= 2L * kCUs;
+// group first: where every CU gets one or two full groups. Per kernel trace:
+// 7B at ctx 2048 (256 full groups) 11.5 -> 10.3 us, 70B at ctx 2048 (512)
+// 16.1 -> 15.7 us; the 3072-wide draft (192 full groups, fewer than the
+// CUs) 8.0 -> 8.4 us, and with 2048 (70B at B = 4 or ctx 8192) no gain.
+static bool short_first_order(int groups, int H, int B) {
+  const long full = static_cast<long>(groups - 1) * H * B;
+  return full >= kCUs && full <= 2L * kCUs;
 }
 
 // Decode launches (up to 16 new tokens per sequence): WP positions per wave,
@@ -316,7 +315,7 @@ static hipError_t attn_decode_t(const void* q, const void* kc, const void* vc, c
   const int groups = (T_cap + 4 * WP - 1) / (4 * WP);
   hipLaunchKernelGGL((attn_partial_kernel<T, DH, 1, WP, KP, NTL>), dim3(groups, H, B), dim3(256), 0, st,
                      static_cast<const T*>(q), static_cast<const T*>(kc), static_cast<const T*>(vc), lengths,
-                     pos_offset, Mps, H, T_cap, groups, last_last(groups, H, B), c_log2, part);
+                     pos_offset, Mps, H, T_cap, groups, short_first_order(groups, H, B), c_log2, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3(B * Mps, H), dim3(DH), 0, st, part, lengths, pos_offset,
@@ -347,10 +346,10 @@ static hipError_t attn_t(const void* q, const void* kc, const void* vc, const in
   const int NP = attn_partials(T_cap);
   if (Mps <= 32)
     hipLaunchKernelGGL((attn_partial_kernel<T, DH, 2, kWavePos>), grid, dim3(256), 0, st, qq, kk, vv, lengths,
-                       pos_offset, Mps, H, T_cap, NP, last_last(groups, H, B), c_log2, part);
+                       pos_offset, Mps, H, T_cap, NP, short_first_order(groups, H, B), c_log2, part);
   else
     hipLaunchKernelGGL((attn_partial_kernel<T, DH, 4, kWavePos>), grid, dim3(256), 0, st, qq, kk, vv, lengths,
-                       pos_offset, Mps, H, T_cap, NP, last_last(groups, H, B), c_log2, part);
+                       pos_offset, Mps, H, T_cap, NP, short_first_order(groups, H, B), c_log2, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3(B * Mps, H), dim3(DH), 0, st, part, lengths, pos_offset,
