@@ -83,9 +83,11 @@ hipError_t launch_kv_copy(int dtype, int to_cache, void* kc, void* vc, int H, in
 // Sampling.
 // Row statistics (stats, row_stat_bytes() each, may be NULL) and, if probs
 // != NULL, the probabilities after temperature and the top-k / nucleus
-// modifiers (top_k <= 0 or >= V: off; top_p >= 1: off).
+// modifiers (top_k <= 0 or >= V: off; top_p >= 1: off). With stats and cut
+// (rows x cut_row_bytes(V) bytes of scratch) given, rows with a modifier are
+// cut over several CUs; otherwise one work-group per row does everything.
 hipError_t launch_row_softmax(const float* logits, int rows, int V, float temperature, int top_k, float top_p,
-                              void* stats, float* probs, int* err, hipStream_t st);
+                              void* stats, float* probs, char* cut, int* err, hipStream_t st);
 hipError_t launch_accept_probs(const float* p, const float* q, const int32_t* drafts,
                                const float* unif, uint64_t seed, uint64_t loop, int B, int K,
                                int V, int32_t* out, int32_t* n_acc, int* err, hipStream_t st);
@@ -93,9 +95,13 @@ hipError_t launch_accept_logits(const float* p, const float* logits, const void*
                                 float temperature, const int32_t* tokens, const float* unif,
                                 uint64_t seed, uint64_t loop, int B, int K, int V, int32_t* out,
                                 int32_t* n_acc, int* err, hipStream_t st);
+// Draft step t: p_t of each sequence's last row into p_out and x~_{t+1}
+// drawn from it. stats (B rows) and cut (B x cut_row_bytes(V)), if given,
+// are scratch for a cut over several CUs when a modifier is on.
 hipError_t launch_draft_sample(const float* logits, int Mps, int B, int V, float temperature,
                                int top_k, float top_p, float* p_out, int K, int t, int32_t* tokens,
-                               const int32_t* ctx, uint64_t seed, uint64_t loop, int* err, hipStream_t st);
+                               const int32_t* ctx, uint64_t seed, uint64_t loop, void* stats, char* cut, int* err,
+                               hipStream_t st);
 hipError_t launch_commit(int32_t* lengths, const int32_t* tokens, const int32_t* out,
                          const int32_t* n_acc, int B, int K, int32_t* ctx, int32_t* seq_out,
                          int32_t* n_out, int cap, hipStream_t st);

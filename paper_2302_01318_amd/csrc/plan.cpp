@@ -177,6 +177,12 @@ size_t forward_part_bytes(const Layout& L, int M) {
   return part;
 }
 
+size_t cut_row_bytes(int V) {
+  if (V > modifier_max_vocab()) return 0;
+  // histogram, 16 softmax partials (256 bytes), bucket ids
+  return align256(static_cast<size_t>(kCutBuckets) * 2 * sizeof(uint64_t)) + 256 + align256(static_cast<size_t>(V) * 2);
+}
+
 WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
   WsLayout w{};
   const size_t M = static_cast<size_t>(B) * Mps;
@@ -199,6 +205,7 @@ WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap) {
   w.ss_b = o; o = align256(o + ng * M * 4);
   w.logits = o; o = align256(o + M * L.V * 4);
   w.stats = o; o = align256(o + M * kRowStatBytes);
+  w.cut = o; o = align256(o + M * cut_row_bytes(L.V));   // top-k / nucleus scratch per row
   w.gpart = o; o = align256(o + part);
   w.total = o;
   return w;

@@ -91,6 +91,7 @@ constexpr int kAttnWavePos = 64;
 constexpr int kSampleThreads = 1024;
 constexpr int kPerLane = 32;
 constexpr size_t kRowStatBytes = 24;   // sizeof(RowStat), sampling.hip
+constexpr int kCutBuckets = 1 + 33 * 16;   // weight buckets of the top-k / nucleus cut-off (sampling.hip)
 
 // ---- launch plans ------------------------------------------------------
 // Wide GEMM: M tiles, k-tiles per chunk, n-tiles per wave, waves per
@@ -129,7 +130,7 @@ Layout make_layout(const sps_config* c);   // c must be valid
 
 // Offsets of the forward's scratch buffers within the workspace.
 struct WsLayout {
-  size_t h, x, o, q, rope, apart, act, ss_a, ss_b, logits, stats, gpart, total;
+  size_t h, x, o, q, rope, apart, act, ss_a, ss_b, logits, stats, cut, gpart, total;
 };
 
 // The workspace of a call that runs forwards of B sequences with any number
@@ -140,6 +141,11 @@ WsLayout make_ws(const Layout& L, int B, int Mps, int T_cap);
 
 // sps_workspace_bytes: 0 for an invalid request (see sps.h).
 size_t workspace_bytes(const sps_config* cfg, int B, int max_tokens_per_seq, int T_cap);
+
+// Per-row scratch of the top-k / nucleus cut-off over several CUs: the
+// row's bucket histogram (counts, weights) and a bucket id per entry; 0
+// where the vocabulary is past what the cut-off handles.
+size_t cut_row_bytes(int V);
 
 // Bytes of split-K partials the launches of one forward over M rows write.
 size_t forward_part_bytes(const Layout& L, int M);

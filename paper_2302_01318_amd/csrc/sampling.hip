@@ -11,6 +11,8 @@
 // it 64 consecutive entries at a time; the 16 segment totals give every
 // segment its exclusive prefix, and only the wave whose segment holds the
 // threshold scans it again to find the index.
+#include <algorithm>
+
 #include "common.h"
 #include "launch.h"
 #include "philox.h"
@@ -109,6 +111,53 @@ __device__ __forceinline__ float prob_final(float z, const RowStat& st, float in
 }
 __device__ __forceinline__ bool row_modified(const RowStat& st) { return st.s > 0.f; }
 
+// Softmax partials of row_stat (rows of up to kPerLane nt entries): thread
+// t of nt takes entries t + k nt, k < kPerLane, all loads in flight
+// together, and returns the max of x = z / T and the sum of exp(x - max)
+// over them (in k order) and whether one is NaN or +Inf; wave_soft_merge
+// combines a wave's partials by butterfly, soft_merge one partial into
+// another. row_stat and the cut-off's partial kernel both use these, so a
+// row's statistics are the same bits in either.
+struct SoftPart {
+  float m, s;
+  bool bad;
+};
+__device__ __forceinline__ SoftPart thread_soft_part(const float* __restrict__ z, int V, float inv_t, unsigned t,
+                                                     unsigned nt) {
+  SoftPart p{-INFINITY, 0.f, false};
+  float x[kPerLane];
+#pragma unroll
+  for (int k = 0; k < kPerLane; ++k)   // all loads first (clamped: none behind a branch)
+    x[k] = z[min(t + k * nt, static_cast<unsigned>(V - 1))];
+#pragma unroll
+  for (int k = 0; k < kPerLane; ++k) {
+    x[k] = t + k * nt < static_cast<unsigned>(V) ? __fmul_rn(x[k], inv_t) : -INFINITY;
+    p.bad |= !(x[k] < INFINITY);
+    p.m = fmaxf(p.m, x[k]);
+  }
+  if (p.m > -INFINITY) {
+#pragma unroll
+    for (int k = 0; k < kPerLane; ++k) p.s += expf(x[k] - p.m);
+  }
+  return p;
+}
+// (Explicit roundings: a contracted multiply-add could be formed differently
+// where the merge is inlined, and the partials' consumers must reproduce
+// row_stat's bits.)
+__device__ __forceinline__ void soft_merge(float& m, float& s2, float om, float os) {
+  const float nm = fmaxf(m, om);
+  if (nm == -INFINITY) return;
+  s2 = __fadd_rn(__fmul_rn(s2, expf(m - nm)), __fmul_rn(os, expf(om - nm)));
+  m = nm;
+}
+__device__ __forceinline__ void wave_soft_merge(float& m, float& s2) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float om = __shfl_xor(m, o), os = __shfl_xor(s2, o);
+    soft_merge(m, s2, om, os);
+  }
+}
+
 // red: __shared__ float[32], ired: __shared__ int[16].
 __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, float temperature, float* red,
                                           int* ired) {
@@ -149,20 +198,10 @@ __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, 
   float mx = -INFINITY, sm = 0.f;
   bool bad = false;
   if (V <= kPerLane * static_cast<int>(blockDim.x)) {
-    float x[kPerLane];
-#pragma unroll
-    for (int k = 0; k < kPerLane; ++k)   // all loads first (clamped: none behind a branch)
-      x[k] = z[min(threadIdx.x + k * blockDim.x, static_cast<unsigned>(V - 1))];
-#pragma unroll
-    for (int k = 0; k < kPerLane; ++k) {
-      x[k] = threadIdx.x + k * blockDim.x < static_cast<unsigned>(V) ? __fmul_rn(x[k], inv_t) : -INFINITY;
-      bad |= !(x[k] < INFINITY);
-      mx = fmaxf(mx, x[k]);
-    }
-    if (mx > -INFINITY) {
-#pragma unroll
-      for (int k = 0; k < kPerLane; ++k) sm += expf(x[k] - mx);
-    }
+    const SoftPart p = thread_soft_part(z, V, inv_t, threadIdx.x, blockDim.x);
+    mx = p.m;
+    sm = p.s;
+    bad = p.bad;
   } else {
     for (int i = threadIdx.x; i < V; i += blockDim.x) {
       const float x = __fmul_rn(z[i], inv_t);
@@ -175,23 +214,13 @@ __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, 
       }
     }
   }
-  auto merge = [](float& m, float& s2, float om, float os) {
-    const float nm = fmaxf(m, om);
-    if (nm == -INFINITY) return;
-    s2 = s2 * expf(m - nm) + os * expf(om - nm);
-    m = nm;
-  };
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float om = __shfl_xor(mx, o), os = __shfl_xor(sm, o);
-    merge(mx, sm, om, os);
-  }
+  wave_soft_merge(mx, sm);
   __syncthreads();
   if ((threadIdx.x & 63) == 0) { red[threadIdx.x >> 6] = mx; red[16 + (threadIdx.x >> 6)] = sm; }
   __syncthreads();
   mx = red[0];
   sm = red[16];
-  for (int w = 1; w < static_cast<int>(blockDim.x >> 6); ++w) merge(mx, sm, red[w], red[16 + w]);
+  for (int w = 1; w < static_cast<int>(blockDim.x >> 6); ++w) soft_merge(mx, sm, red[w], red[16 + w]);
   st.a = mx;
   st.b = sm;
   if (__syncthreads_or(bad)) {
@@ -207,8 +236,7 @@ __device__ __forceinline__ RowStat row_stat(const float* __restrict__ z, int V, 
 // position e (0..32) of its leading one bit and the next 4 bits. The bucket
 // is monotone in w, so the buckets split the ranking into contiguous key
 // ranges (~6 % of a weight wide).
-constexpr int kCutBuckets = 1 + 33 * 16;
-constexpr int kCutCand = 1024;            // keys of one bucket resolved exactly
+constexpr int kCutCand = 1024;            // keys of one bucket resolved exactly (kCutBuckets: plan.h)
 
 __device__ __forceinline__ int cut_bucket(uint64_t w) {
   if (w == 0) return 0;
@@ -498,7 +526,7 @@ __device__ __forceinline__ void row_cutoff(PF pf, int V, int top_k, float top_p,
 }
 
 // Whether the modifiers change a row (greedy rows are never modified).
-__device__ __forceinline__ bool modifiers_active(float temperature, int top_k, float top_p, int V) {
+__host__ __device__ __forceinline__ bool modifiers_active(float temperature, int top_k, float top_p, int V) {
   return temperature > 0.f && ((top_k >= 1 && top_k < V) || top_p < 1.f);
 }
 
@@ -554,6 +582,462 @@ __global__ __launch_bounds__(kSampleThreads) void row_softmax_kernel(const float
   const float inv_t = temperature == 0.f ? 0.f : 1.0f / temperature;
   if (threadIdx.x == 0 && stats) stats[row] = st;
   if (probs) write_probs(z, V, st, inv_t, probs + static_cast<size_t>(row) * V);
+}
+
+// ---------------------------------------------------------------------------
+// The top-k / nucleus cut-off of the rows of a verify or draft step over
+// several CUs (one work-group per row is instruction-bound at ~290 VALU
+// instructions per vocabulary entry). cut_part_kernel's work-groups are the
+// waves of row_stat, each writing that wave's softmax partial (every
+// consumer merges them in row_stat's order, so the row's probabilities are
+// those of the unmodified row bit for bit), and clear the row's bucket
+// histogram; cut_hist_kernel's work-groups each take one segment of a row: the draw
+// weights, each entry's bucket, and the segment's bucket counts and weights
+// added to the row's histogram (integer atomics: the totals do not depend on
+// the order); cut_select_kernel finds the bucket holding each cut from the
+// histogram, gathers that bucket's keys alone (their weights recomputed) and
+// resolves the cut as bucket_select does, else (more than kCutCand keys in
+// the bucket, a flat run of weights) it runs row_cutoff over the whole row.
+// Row r of a launch is logits row r rstride + roff.
+// ---------------------------------------------------------------------------
+
+// Per-row scratch (cut_row_bytes(V) bytes): bucket counts, bucket weights,
+// the softmax partials of the row_stat waves, then a 16-bit bucket id per
+// entry.
+struct CutPart {
+  float m, s;
+  uint32_t bad, pad;
+};
+constexpr int kStatWaves = kSampleThreads / 64;     // waves of row_stat
+static_assert(kStatWaves * sizeof(CutPart) <= 256, "partials fit their scratch slot");
+struct CutRowScratch {
+  uint64_t* n;
+  uint64_t* w;
+  CutPart* part;
+  uint16_t* bid;
+};
+__device__ __forceinline__ CutRowScratch cut_row(char* base, size_t row_bytes, int r) {
+  constexpr size_t kHist = (static_cast<size_t>(kCutBuckets) * 2 * sizeof(uint64_t) + 255) & ~static_cast<size_t>(255);
+  char* p = base + static_cast<size_t>(r) * row_bytes;
+  return CutRowScratch{reinterpret_cast<uint64_t*>(p), reinterpret_cast<uint64_t*>(p) + kCutBuckets,
+                       reinterpret_cast<CutPart*>(p + kHist), reinterpret_cast<uint16_t*>(p + kHist + 256)};
+}
+
+// Row statistics from the wave partials, merged in wave order as row_stat
+// merges them (the same bits).
+__device__ __forceinline__ RowStat stat_of_parts(const CutPart* __restrict__ part) {
+  float mx = part[0].m, sm = part[0].s;
+  bool bad = part[0].bad != 0;
+  for (int w = 1; w < kStatWaves; ++w) {
+    soft_merge(mx, sm, part[w].m, part[w].s);
+    bad |= part[w].bad != 0;
+  }
+  RowStat st;
+  st.s = 0.f;
+  st.tau = 0;
+  st.nonfinite = bad ? 1u : 0u;
+  st.a = bad ? 0.f : mx;
+  st.b = bad ? -1.f : sm;
+  return st;
+}
+
+__device__ __forceinline__ const float* cut_logits(const float* logits, int r, int rstride, int roff, int V) {
+  return logits + (static_cast<size_t>(r) * rstride + roff) * V;
+}
+
+// Grid (kStatWaves, rows), one wave each: wave w of row_stat's work-group,
+// its partial into the row's scratch; wave 0 also clears the histogram.
+__global__ __launch_bounds__(64) void cut_part_kernel(const float* __restrict__ logits, int V, int rstride, int roff,
+                                                     float temperature, char* __restrict__ cut, size_t cut_bytes) {
+  const int r = blockIdx.y, w = blockIdx.x;
+  SoftPart p = thread_soft_part(cut_logits(logits, r, rstride, roff, V), V, 1.0f / temperature,
+                                w * 64 + threadIdx.x, kSampleThreads);
+  wave_soft_merge(p.m, p.s);
+  const bool bad = __ballot(p.bad) != 0;
+  const CutRowScratch cs = cut_row(cut, cut_bytes, r);
+  if (threadIdx.x == 0) cs.part[w] = CutPart{p.m, p.s, bad ? 1u : 0u, 0u};
+  if (w == 0)
+    for (int b = threadIdx.x; b < kCutBuckets; b += 64) {
+      cs.n[b] = 0;
+      cs.w[b] = 0;
+    }
+}
+
+constexpr int kCutSegThreads = 256;
+
+// Grid (segments, rows): segment s of a row is entries [s seg, (s + 1) seg).
+__global__ __launch_bounds__(kCutSegThreads) void cut_hist_kernel(const float* __restrict__ logits, int V, int rstride,
+                                                                  int roff, float temperature,
+                                                                  RowStat* __restrict__ stats, char* __restrict__ cut,
+                                                                  size_t cut_bytes, int seg) {
+  __shared__ uint64_t hn[kCutBuckets], hw[kCutBuckets];
+  const int r = blockIdx.y, s = blockIdx.x;
+  const CutRowScratch cs = cut_row(cut, cut_bytes, r);
+  const RowStat st = stat_of_parts(cs.part);
+  // The row's statistics as merged here go to stats[r]: the select reads these
+  // bits rather than merging again, so its keys are the ones bucketed here.
+  if (s == 0 && threadIdx.x == 0) stats[r] = st;
+  if (st.nonfinite) return;                        // uniform over the block
+  for (int b = threadIdx.x; b < kCutBuckets; b += blockDim.x) {
+    hn[b] = 0;
+    hw[b] = 0;
+  }
+  __syncthreads();
+  const float* z = cut_logits(logits, r, rstride, roff, V);
+  const float inv_t = 1.0f / temperature;
+  const int i0 = s * seg, i1 = min(V, i0 + seg);
+  for (int i = i0 + static_cast<int>(threadIdx.x); i < i1; i += kCutSegThreads) {
+    const uint64_t w = fixed_weight(prob_of(z[i], st, inv_t, i));
+    const int b = cut_bucket(w);
+    cs.bid[i] = static_cast<uint16_t>(b);
+    atomicAdd(reinterpret_cast<unsigned long long*>(&hn[b]), 1ull);
+    if (w) atomicAdd(reinterpret_cast<unsigned long long*>(&hw[b]), static_cast<unsigned long long>(w));
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < kCutBuckets; b += blockDim.x) {
+    if (hn[b]) atomicAdd(reinterpret_cast<unsigned long long*>(&cs.n[b]), static_cast<unsigned long long>(hn[b]));
+    if (hw[b]) atomicAdd(reinterpret_cast<unsigned long long*>(&cs.w[b]), static_cast<unsigned long long>(hw[b]));
+  }
+}
+
+// A row's bucket ids held in registers: thread t owns the 8 ids of vector
+// t + j kSampleThreads (entries 8 (t + j kSampleThreads) .. + 7), j < kIdVecs,
+// loaded together (V <= 8 kIdVecs kSampleThreads).
+constexpr int kIdVecs = 4;
+typedef uint32_t id8 __attribute__((ext_vector_type(4)));   // eight 16-bit bucket ids
+static_assert(8 * kIdVecs * kSampleThreads >= kPerLane * kSampleThreads, "bucket ids of the largest cut row");
+struct RowIds {
+  id8 v[kIdVecs];
+  __device__ __forceinline__ int id(int j, int e) const {
+    const uint32_t w = v[j][e >> 1];
+    return static_cast<int>(e & 1 ? w >> 16 : w & 0xFFFFu);
+  }
+};
+__device__ __forceinline__ RowIds load_ids(const uint16_t* __restrict__ bid, int V) {
+  RowIds ids;
+  const id8* src = reinterpret_cast<const id8*>(bid);
+  const int nv = (V + 7) / 8;                      // vectors holding entries (the scratch pads to 256 bytes)
+#pragma unroll
+  for (int j = 0; j < kIdVecs; ++j) ids.v[j] = src[min(static_cast<int>(threadIdx.x) + j * kSampleThreads, nv - 1)];
+  return ids;
+}
+
+// The keys of bucket nb (every one of them: nb lies above the previous
+// cut's bucket) into sc.cand; false (uniform) when there are more than
+// kCutCand.
+template <class PF>
+__device__ __forceinline__ bool gather_bucket(PF pf, const RowIds& ids, int V, int nb, CutScratch& sc) {
+  const int tid = threadIdx.x;
+  if (tid == 0) sc.ncand = 0;
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kIdVecs; ++j)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int i = 8 * (tid + j * kSampleThreads) + e;
+      if (i < V && ids.id(j, e) == nb) {
+        const int slot = atomicAdd(&sc.ncand, 1);
+        if (slot < kCutCand) sc.cand[slot] = rank_key(fixed_weight(pf(i)), i);
+      }
+    }
+  __syncthreads();
+  return sc.ncand <= kCutCand;
+}
+
+// One select over the keys >= lo, as bucket_select, from the bucket totals
+// in sc.bins / sc.wbins (all keys of every bucket) instead of a pass over
+// the row. lob is the bucket of lo (-1: lo admits every key); its keys are
+// sc.cand[0 .. nlo), gathered by the previous select, of which only those >=
+// lo count. Sets *tau, *kept (weight of the keys >= tau) and the bucket and
+// candidates now in sc.cand; false (uniform) where the bucket of the cut
+// holds more than kCutCand keys.
+template <bool NUCLEUS, class PF>
+__device__ bool hist_select(PF pf, const RowIds& ids, int V, uint64_t lo, int lob, int nlo,
+                            uint64_t need, float top_p, CutScratch& sc, uint64_t* sub_n, uint64_t* sub_w,
+                            uint64_t* tau, uint64_t* kept, int* nb_out, int* n_out) {
+  const int tid = threadIdx.x, bd = blockDim.x;
+  if (lob >= 0) {
+    // Bucket lob: only its candidates >= lo; the buckets under it: nothing.
+    uint64_t c = 0, w = 0;
+    for (int t = tid; t < nlo; t += bd) {
+      const uint64_t k = sc.cand[t];
+      c += k >= lo ? 1 : 0;
+      w += k >= lo ? k >> 24 : 0;
+    }
+    c = wave_sum_u64(c);
+    w = wave_sum_u64(w);
+    __syncthreads();
+    if ((tid & 63) == 0) {
+      sc.wsum[tid >> 6] = c;
+      sc.hist[tid >> 6] = w;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      uint64_t cc = 0, ww = 0;
+      for (int v = 0; v < bd / 64; ++v) {
+        cc += sc.wsum[v];
+        ww += sc.hist[v];
+      }
+      sc.bins[lob] = cc;
+      sc.wbins[lob] = ww;
+    }
+    for (int b = tid; b < lob; b += bd) {
+      sc.bins[b] = 0;
+      sc.wbins[b] = 0;
+    }
+  }
+  if (tid == 0) sc.nb = -2;
+  __syncthreads();
+  if (tid < 64) {
+    // Lane l owns kPer buckets from the top; the first lane whose inclusive
+    // total reaches the target walks its buckets.
+    constexpr int kPer = (kCutBuckets + 63) / 64;
+    uint64_t hc[kPer], hw[kPer], tc = 0, tw = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int b = kCutBuckets - 1 - (tid * kPer + j);
+      hc[j] = b >= 0 ? sc.bins[b] : 0;
+      hw[j] = b >= 0 ? sc.wbins[b] : 0;
+      tc += hc[j];
+      tw += hw[j];
+    }
+    const uint64_t ic = wave_incl_scan_u64(tc), iw = wave_incl_scan_u64(tw);
+    bool weighted = false;
+    if (NUCLEUS) {
+      const uint64_t W = shfl_u64(iw, 63);
+      const uint64_t target = grid_threshold(top_p, W);
+      weighted = target != 0;
+      need = weighted ? target : 1;
+    }
+    const uint64_t inc = weighted ? iw : ic;
+    const uint64_t hit = __ballot(inc >= need);
+    if (hit && tid == __ffsll(static_cast<long long>(hit)) - 1) {
+      uint64_t c = inc - (weighted ? tw : tc), cw = iw - tw;
+      int jb = kPer - 1;
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        const uint64_t h = weighted ? hw[j] : hc[j];
+        if (c + h >= need) {
+          jb = j;
+          break;
+        }
+        c += h;
+        cw += hw[j];
+      }
+      sc.nb = kCutBuckets - 1 - (tid * kPer + jb);
+      sc.above = c;
+      sc.above_w = cw;
+      sc.need = need;
+      sc.weighted = weighted;
+    }
+  }
+  __syncthreads();
+  const int nb = sc.nb;
+  if (nb < 0 || nb < lob) return false;            // (no bucket reaches the target: not for a valid row)
+  const uint64_t above = sc.above;                 // count / weight above bucket nb; sc.above_w its weight
+  need = sc.need;
+  const bool weighted = sc.weighted != 0;
+  int n = nlo;
+  if (nb != lob) {
+    if (!gather_bucket(pf, ids, V, nb, sc)) return false;
+    n = sc.ncand;
+  }
+  // Second level: the candidates' key range (keys >= lo) in 256 sub-ranges
+  // of 2^sh keys (sub-range (k - kmin) >> sh, monotone in k); one wave finds
+  // the sub-range where the total from the top reaches the target, and only
+  // its candidates, gathered into sc.hist, are compared pairwise (all n of
+  // them where it holds more than 256).
+  uint64_t kmin = ~0ull, kmax = 0;
+  for (int t = tid; t < n; t += bd) {
+    const uint64_t k = sc.cand[t];
+    kmin = k >= lo && k < kmin ? k : kmin;
+    kmax = k >= lo && k > kmax ? k : kmax;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t a = shfl_xor_u64(kmin, o), b = shfl_xor_u64(kmax, o);
+    kmin = a < kmin ? a : kmin;
+    kmax = b > kmax ? b : kmax;
+  }
+  if ((tid & 63) == 0) {
+    sc.wsum[tid >> 6] = kmin;
+    sc.hist[tid >> 6] = kmax;
+  }
+  for (int b = tid; b < 256; b += bd) {
+    sub_n[b] = 0;
+    sub_w[b] = 0;
+  }
+  __syncthreads();
+  kmin = ~0ull;
+  kmax = 0;
+  for (int v = 0; v < bd / 64; ++v) {
+    kmin = sc.wsum[v] < kmin ? sc.wsum[v] : kmin;
+    kmax = sc.hist[v] > kmax ? sc.hist[v] : kmax;
+  }
+  if (kmax < kmin) return false;                   // no candidate >= lo (uniform; not for a valid row)
+  const uint64_t span = kmax - kmin;
+  const int sh = span >> 8 ? 64 - __clzll(static_cast<long long>(span >> 8)) : 0;   // span >> sh < 256
+  for (int t = tid; t < n; t += bd) {
+    const uint64_t k = sc.cand[t];
+    if (k >= lo) {
+      const int sb = static_cast<int>((k - kmin) >> sh);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&sub_n[sb]), 1ull);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&sub_w[sb]), static_cast<unsigned long long>(k >> 24));
+    }
+  }
+  if (tid == 0) {
+    sc.prefix = 0;
+    sc.nb = -1;
+  }
+  __syncthreads();
+  if (tid < 64) {
+    // Lane l owns sub-ranges 255 - 4l .. 252 - 4l; the first lane whose
+    // inclusive total (above the bucket's included) reaches the target walks them.
+    uint64_t hc[4], hw[4], tc = 0, tw = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      hc[j] = sub_n[255 - 4 * tid - j];
+      hw[j] = sub_w[255 - 4 * tid - j];
+      tc += hc[j];
+      tw += hw[j];
+    }
+    const uint64_t ic = wave_incl_scan_u64(tc), iw = wave_incl_scan_u64(tw);
+    const uint64_t inc = above + (weighted ? iw : ic);
+    const uint64_t hit = __ballot(inc >= need);
+    if (hit && tid == __ffsll(static_cast<long long>(hit)) - 1) {
+      uint64_t c = inc - (weighted ? tw : tc), cw = sc.above_w + iw - tw;
+      int jb = 3;
+#pragma unroll
+      for (int j = 0; j < 3; ++j) {
+        const uint64_t h = weighted ? hw[j] : hc[j];
+        if (c + h >= need) {
+          jb = j;
+          break;
+        }
+        c += h;
+        cw += hw[j];
+      }
+      sc.nb = 255 - 4 * tid - jb;                  // the sub-range
+      sc.above = c;                                // count / weight above it
+      sc.above_w = cw;                             // weight above it
+      sc.ncand = 0;
+    }
+  }
+  __syncthreads();
+  const int sbt = sc.nb;
+  if (sbt < 0) return false;
+  const uint64_t above2 = sc.above;
+  for (int t = tid; t < n; t += bd) {
+    const uint64_t k = sc.cand[t];
+    if (k >= lo && static_cast<int>((k - kmin) >> sh) == sbt) {
+      const int slot = atomicAdd(&sc.ncand, 1);
+      if (slot < 256) sc.hist[slot] = k;
+    }
+  }
+  __syncthreads();
+  const int m = sc.ncand;
+  const bool small = m <= 256;
+  const uint64_t* list = small ? sc.hist : sc.cand;
+  const int nl = small ? m : n;
+  for (int t = tid; t < nl; t += bd) {
+    const uint64_t k = list[t];
+    if (k < lo || static_cast<int>((k - kmin) >> sh) != sbt) continue;
+    uint64_t sum = 0;
+    for (int u = 0; u < nl; ++u) {
+      const uint64_t ku = list[u];
+      sum += ku > k && static_cast<int>((ku - kmin) >> sh) == sbt ? (weighted ? ku >> 24 : 1) : 0;
+    }
+    const uint64_t v = weighted ? k >> 24 : 1;
+    if (above2 + sum < need && above2 + sum + v >= need) sc.prefix = k;   // exactly one candidate
+  }
+  __syncthreads();
+  const uint64_t t_key = sc.prefix;
+  if (t_key == 0) return false;
+  uint64_t w = 0;
+  for (int t = tid; t < nl; t += bd) {
+    const uint64_t k = list[t];
+    w += k >= t_key && static_cast<int>((k - kmin) >> sh) == sbt ? k >> 24 : 0;
+  }
+  w = wave_sum_u64(w);
+  if ((tid & 63) == 0) sc.wsum[tid >> 6] = w;
+  __syncthreads();
+  uint64_t total = sc.above_w;                     // weight above the sub-range
+  for (int v = 0; v < bd / 64; ++v) total += sc.wsum[v];
+  *tau = t_key;
+  *kept = total;
+  *nb_out = nb;
+  *n_out = n;
+  __syncthreads();                                 // sc reusable by the next select
+  return true;
+}
+
+// grid (rows), kSampleThreads threads, dynamic LDS cutoff_lds_bytes(V) (for
+// the fallback).
+__global__ __launch_bounds__(kSampleThreads) void cut_select_kernel(const float* __restrict__ logits, int V,
+                                                                    int rstride, int roff, float temperature,
+                                                                    int top_k, float top_p,
+                                                                    RowStat* __restrict__ stats,
+                                                                    char* __restrict__ cut, size_t cut_bytes, int* err) {
+  __shared__ CutScratch sc;
+  __shared__ uint64_t sub_n[256], sub_w[256];
+  extern __shared__ uint32_t s_rowkeys[];
+  const int r = blockIdx.x;
+  const CutRowScratch cs = cut_row(cut, cut_bytes, r);
+  const RowIds ids = load_ids(cs.bid, V);          // in flight with the histogram's and the partials' loads
+  for (int b = threadIdx.x; b < kCutBuckets; b += blockDim.x) {
+    sc.bins[b] = cs.n[b];
+    sc.wbins[b] = cs.w[b];
+  }
+  const RowStat base = stats[r];                   // merged by cut_hist_kernel
+  if (base.nonfinite) {                            // uniform: one-hot at index 0, never cut (as row_stat_final)
+    if (threadIdx.x == 0) atomicOr(err, kErrNonFinite);
+    return;
+  }
+  __syncthreads();
+  const float* z = cut_logits(logits, r, rstride, roff, V);
+  const float inv_t = 1.0f / temperature;
+  auto pf = [&](int i) { return prob_of(z[i], base, inv_t, i); };
+  // Top-k, then nucleus among what top-k kept (row_cutoff's order).
+  uint64_t tau = 1, S = 0;
+  int lob = -1, nk = 0;
+  bool ok = true;
+  if (top_k >= 1 && top_k < V)
+    ok = hist_select<false>(pf, ids, V, 1, -1, 0, static_cast<uint64_t>(top_k), 1.f, sc, sub_n, sub_w, &tau, &S, &lob,
+                            &nk);
+  if (ok && top_p < 1.f) {
+    uint64_t tp = 0, Sp = 0;
+    int lp = -1, np = 0;
+    ok = hist_select<true>(pf, ids, V, tau, lob, nk, 0, top_p, sc, sub_n, sub_w, &tp, &Sp, &lp, &np);
+    tau = tp > tau ? tp : tau;
+    S = Sp;
+  }
+  RowStat st = base;
+  if (ok) {
+    st.tau = tau;
+    st.s = S == 0 ? 0.f : __ull2float_rn(S) * 2.3283064365386963e-10f;   // * 2^-32, exact
+  } else {
+    row_cutoff(pf, V, top_k, top_p, st, sc, s_rowkeys);
+  }
+  if (threadIdx.x == 0) stats[r] = st;
+}
+
+// Probabilities of rows (with their cut) into probs[row][V], one segment per
+// work-group: grid (segments, rows).
+__global__ __launch_bounds__(kCutSegThreads) void cut_export_kernel(const float* __restrict__ logits, int V,
+                                                                    float temperature,
+                                                                    const RowStat* __restrict__ stats,
+                                                                    float* __restrict__ probs, int seg) {
+  const int r = blockIdx.y, s = blockIdx.x;
+  const RowStat st = stats[r];
+  const float* z = logits + static_cast<size_t>(r) * V;
+  float* pr = probs + static_cast<size_t>(r) * V;
+  const float inv_t = 1.0f / temperature;
+  const int i0 = s * seg, i1 = min(V, i0 + seg);
+  if (row_modified(st)) {
+    for (int i = i0 + static_cast<int>(threadIdx.x); i < i1; i += kCutSegThreads) pr[i] = prob_final<true>(z[i], st, inv_t, i);
+  } else {
+    for (int i = i0 + static_cast<int>(threadIdx.x); i < i1; i += kCutSegThreads) pr[i] = prob_final<false>(z[i], st, inv_t, i);
+  }
 }
 
 // Segment [b0, b1) of the vocabulary owned by this wave: a multiple of 64
@@ -775,8 +1259,8 @@ __global__ __launch_bounds__(kSampleThreads) void accept_kernel(QS qs, const flo
 // written to p_out[b][t][:], and x~_{t+1} drawn from it into tokens[b][t+1].
 __global__ __launch_bounds__(kSampleThreads) void draft_sample_kernel(
     const float* __restrict__ logits, int Mps, int V, float temperature, int top_k, float top_p,
-    float* __restrict__ p_out, int K, int t, int32_t* __restrict__ tokens, const int32_t* __restrict__ ctx,
-    uint64_t seed, uint64_t loop, int* err) {
+    const RowStat* __restrict__ pre, float* __restrict__ p_out, int K, int t, int32_t* __restrict__ tokens,
+    const int32_t* __restrict__ ctx, uint64_t seed, uint64_t loop, int* err) {
   __shared__ float red[32];
   __shared__ int ired[16];
   __shared__ uint64_t wsum[17];
@@ -787,7 +1271,9 @@ __global__ __launch_bounds__(kSampleThreads) void draft_sample_kernel(
   const float* z = logits + (static_cast<size_t>(b) * Mps + Mps - 1) * V;
   // (A row with a NaN / +Inf logit becomes p_t = one-hot at token 0, a valid
   // draft distribution, so the draw gives token 0 and the flag is raised.)
-  const RowStat st = row_stat_final(z, V, temperature, top_k, top_p, red, ired, sc, s_rowkeys, err);
+  // (pre: the statistics, with the cut, of the row of sequence b, taken by
+  // the cut-off kernels, which also raised the flag for a non-finite row.)
+  const RowStat st = pre ? pre[b] : row_stat_final(z, V, temperature, top_k, top_p, red, ired, sc, s_rowkeys, err);
   const float inv_t = temperature == 0.f ? 0.f : 1.0f / temperature;
   // p_t once into p_out, then the draw from the stored values (visible to
   // the whole block after the barrier).
@@ -841,10 +1327,15 @@ static hipError_t cutoff_lds(const void* kernel, float temperature, int top_k, f
   const bool on = temperature > 0.f && ((top_k >= 1 && top_k < V) || top_p < 1.f);
   *bytes = on ? (cutoff_lds_bytes(V) + 15) / 16 * 16 : 0;
   if (*bytes > 65536) {
-    static bool opted[2] = {false, false};
-    const int which = kernel == reinterpret_cast<const void*>(&row_softmax_kernel) ? 0 : 1;
+    static bool opted[3] = {false, false, false};
+    const int which = kernel == reinterpret_cast<const void*>(&row_softmax_kernel)  ? 0
+                      : kernel == reinterpret_cast<const void*>(&cut_select_kernel) ? 2
+                                                                                     : 1;
     if (!opted[which]) {
-      const hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 140 * 1024);
+      // The largest row the cut-off handles (the kernels' static LDS and this
+      // fit the CU's 160 KiB).
+      const int most = static_cast<int>((cutoff_lds_bytes(modifier_max_vocab()) + 15) / 16 * 16);
+      const hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, most);
       if (e != hipSuccess) return e;
       opted[which] = true;
     }
@@ -852,9 +1343,40 @@ static hipError_t cutoff_lds(const void* kernel, float temperature, int top_k, f
   return hipSuccess;
 }
 
+// The cut-off over several CUs for `rows` rows (logits row r rstride +
+// roff), their statistics into stats[0 .. rows).
+static hipError_t cut_rows(const float* logits, int rows, int rstride, int roff, int V, float temperature, int top_k,
+                           float top_p, RowStat* stats, char* cut, int* err, int* seg_out, int* nseg_out,
+                           hipStream_t st) {
+  const size_t cut_bytes = cut_row_bytes(V);
+  const int nseg = std::max(1, std::min(32, (512 + rows - 1) / rows));   // ~512 work-groups per launch
+  const int seg = (V + nseg - 1) / nseg;
+  size_t lds = 0;
+  hipError_t e = cutoff_lds(reinterpret_cast<const void*>(&cut_select_kernel), temperature, top_k, top_p, V, &lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(cut_part_kernel, dim3(kStatWaves, rows), dim3(64), 0, st, logits, V, rstride, roff, temperature,
+                     cut, cut_bytes);
+  hipLaunchKernelGGL(cut_hist_kernel, dim3((V + seg - 1) / seg, rows), dim3(kCutSegThreads), 0, st, logits, V, rstride,
+                     roff, temperature, stats, cut, cut_bytes, seg);
+  hipLaunchKernelGGL(cut_select_kernel, dim3(rows), dim3(kSampleThreads), lds, st, logits, V, rstride, roff,
+                     temperature, top_k, top_p, stats, cut, cut_bytes, err);
+  *seg_out = seg;
+  *nseg_out = (V + seg - 1) / seg;
+  return hipGetLastError();
+}
+
 hipError_t launch_row_softmax(const float* logits, int rows, int V, float temperature, int top_k, float top_p,
-                              void* stats, float* probs, int* err, hipStream_t st) {
+                              void* stats, float* probs, char* cut, int* err, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
+  if (cut && stats && modifiers_active(temperature, top_k, top_p, V) && V <= modifier_max_vocab()) {
+    int seg = 0, nseg = 0;
+    RowStat* rs = reinterpret_cast<RowStat*>(stats);
+    const hipError_t e = cut_rows(logits, rows, 1, 0, V, temperature, top_k, top_p, rs, cut, err, &seg, &nseg, st);
+    if (e != hipSuccess || !probs) return e;
+    hipLaunchKernelGGL(cut_export_kernel, dim3(nseg, rows), dim3(kCutSegThreads), 0, st, logits, V, temperature, rs,
+                       probs, seg);
+    return hipGetLastError();
+  }
   size_t lds = 0;
   const hipError_t e = cutoff_lds(reinterpret_cast<const void*>(&row_softmax_kernel), temperature, top_k, top_p, V,
                                   &lds);
@@ -884,13 +1406,24 @@ hipError_t launch_accept_logits(const float* p, const float* logits, const void*
 
 hipError_t launch_draft_sample(const float* logits, int Mps, int B, int V, float temperature, int top_k,
                                float top_p, float* p_out, int K, int t, int32_t* tokens, const int32_t* ctx,
-                               uint64_t seed, uint64_t loop, int* err, hipStream_t st) {
+                               uint64_t seed, uint64_t loop, void* stats, char* cut, int* err, hipStream_t st) {
+  if (cut && stats && modifiers_active(temperature, top_k, top_p, V) && V <= modifier_max_vocab()) {
+    // The cut over several CUs, then the draw from the stored statistics.
+    int seg = 0, nseg = 0;
+    RowStat* rs = reinterpret_cast<RowStat*>(stats);
+    const hipError_t e = cut_rows(logits, B, Mps, Mps - 1, V, temperature, top_k, top_p, rs, cut, err, &seg, &nseg,
+                                  st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(draft_sample_kernel, dim3(B), dim3(kSampleThreads), 0, st, logits, Mps, V, temperature, top_k,
+                       top_p, rs, p_out, K, t, tokens, ctx, seed, loop, err);
+    return hipGetLastError();
+  }
   size_t lds = 0;
   const hipError_t e = cutoff_lds(reinterpret_cast<const void*>(&draft_sample_kernel), temperature, top_k, top_p, V,
                                   &lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(draft_sample_kernel, dim3(B), dim3(kSampleThreads), lds, st, logits, Mps, V, temperature, top_k,
-                     top_p, p_out, K, t, tokens, ctx, seed, loop, err);
+                     top_p, static_cast<const RowStat*>(nullptr), p_out, K, t, tokens, ctx, seed, loop, err);
   return hipGetLastError();
 }
 

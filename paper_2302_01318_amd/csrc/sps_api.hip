@@ -482,7 +482,7 @@ sps_status verify_impl(sps_model_t target, sps_kv_t kv, const int32_t* tokens, i
   if (s != SPS_OK) return s;
   const int V = target->cfg.vocab;
   SPS_HIP(sps::launch_row_softmax(logits, B * (K + 1), V, sampling.temperature, sampling.top_k, sampling.top_p,
-                                  stats, q_out, err, st));
+                                  stats, q_out, base + ws.cut, err, st));
   if (acc)
     SPS_HIP(sps::launch_accept_logits(acc->p_draft, logits, stats, sampling.temperature, tokens, acc->uniforms,
                                       acc->rng.seed, acc->rng.loop, B, K, V, acc->out_tokens, acc->n_accepted, err,
@@ -554,7 +554,8 @@ sps_status sps_draft_step(sps_model_t draft, sps_kv_t kv, const int32_t* ctx, in
       s = forward_impl(draft, kv, tokens + t, K + 1, B, 1, t, logits, base, ws, err, st);
     if (s != SPS_OK) return s;
     SPS_HIP(sps::launch_draft_sample(logits, t == 0 ? 2 : 1, B, V, sampling.temperature, sampling.top_k,
-                                     sampling.top_p, p_out, K, t, tokens, ctx, rng.seed, rng.loop, err, st));
+                                     sampling.top_p, p_out, K, t, tokens, ctx, rng.seed, rng.loop, base + ws.stats,
+                                     base + ws.cut, err, st));
   }
   return SPS_OK;
 }
@@ -585,7 +586,7 @@ sps_status sps_softmax(const float* logits, int32_t rows, int32_t V, sps_samplin
   int* err = device_error_ptr();
   if (!err) return SPS_E_HIP;
   SPS_HIP(sps::launch_row_softmax(logits, rows, V, sampling.temperature, sampling.top_k, sampling.top_p, nullptr,
-                                  probs, err, as_stream(stream)));
+                                  probs, nullptr, err, as_stream(stream)));
   return SPS_OK;
 }
 

@@ -47,7 +47,8 @@ static sps_config cfg(int d, int L, int H, int DH, int F, int V, int ffn, int dt
 }
 
 static void check_layout(const WsLayout& w, const char* what) {
-  const size_t r[] = {w.h, w.x, w.o, w.q, w.rope, w.apart, w.act, w.ss_a, w.ss_b, w.logits, w.stats, w.gpart, w.total};
+  const size_t r[] = {w.h, w.x, w.o, w.q, w.rope, w.apart, w.act, w.ss_a, w.ss_b, w.logits, w.stats, w.cut, w.gpart,
+                      w.total};
   for (size_t i = 0; i + 1 < sizeof(r) / sizeof(r[0]); ++i) {
     CHECK(r[i] % 256 == 0, "%s: region %zu not aligned", what, i);
     CHECK(r[i] <= r[i + 1], "%s: region %zu out of order", what, i);
@@ -68,7 +69,7 @@ static void check_call(const Layout& L, int B, int mps, const WsLayout& w, int T
   const size_t M = static_cast<size_t>(B) * mps;
   CHECK(w.x - w.h >= M * L.d * 4 && w.o - w.x >= M * L.d * 4 && w.q - w.o >= M * L.HD * 4 &&
             w.rope - w.q >= M * L.HD * L.es && w.ss_a - w.act >= M * L.F * 4 && w.stats - w.logits >= M * L.V * 4 &&
-            w.gpart - w.stats >= M * kRowStatBytes,
+            w.cut - w.stats >= M * kRowStatBytes && w.gpart - w.cut >= M * cut_row_bytes(L.V),
         "%s: activation regions too small for B %d x %d", what, B, mps);
 }
 

@@ -87,6 +87,49 @@ def test_verify_step_with_modifiers(sps, k, p):
     np.testing.assert_array_equal(nacc.cpu().numpy(), w_n)
 
 
+V32K = configs.ModelShape("v32k", 128, 1, 2, 64, 256, 32000, "gelu", "bf16")
+
+
+@pytest.mark.parametrize("T,k,p", [(1.0, 0, 0.8), (1.0, 50, 1.0), (0.9, 40, 0.9), (50.0, 0, 0.5), (50.0, 3000, 0.9),
+                                   (0.3, 5, 0.95), (1.0, 31999, 1.0)])
+def test_verify_step_with_modifiers_v32000(sps, T, k, p):
+    """The verify step's cut over several CUs at a 32000-token vocabulary:
+    the exported q equals the oracle's cut of the plain softmax of the same
+    logits bit for bit, and accept / resample follows. Temperature 50 makes
+    the rows nearly flat (thousands of equal weights at the cut: the
+    whole-row fallback), 0.3 sharp."""
+    B, K = 2, 4
+    print("verify modifiers V 32000 T", T, "top_k", k, "top_p", p, flush=True)
+    V = V32K.vocab
+    gm, _ = build_pair(V32K, 90, std=0.2)          # logits spread ~2: bucket sizes of a real row
+    n_prior = [40, 57]
+    T_cap = round_up(max(n_prior) + K + 1, 32)
+    kv = sps.KVCache(V32K, B, T_cap)
+    install_prior(V32K, kv, new_cache(V32K, B, T_cap), 91, n_prior)
+    p_raw, _, _ = synth.accept_case(92, B, K, V, 2.0, 0.5)
+    p_mod = omod.modify_rows(p_raw, k, p)
+    g = np.random.default_rng(93)
+    drafts = np.stack([[g.choice(V, p=p_mod[b, t].astype(np.float64) / p_mod[b, t].astype(np.float64).sum())
+                        for t in range(K)] for b in range(B)]).astype(np.int32)
+    toks = np.concatenate([synth.tokens(94, B, 1, V), drafts], axis=1).astype(np.int32)
+    ws = sps.workspace(V32K, B, K + 1, T_cap)
+    logits = torch.empty((B, K + 1, V), device="cuda")
+    q = torch.empty_like(logits)
+    out = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+    nacc = torch.empty(B, dtype=torch.int32, device="cuda")
+    sps.verify_step(gm, kv, torch.from_numpy(toks).cuda(), K, T, ws, logits=logits, q=q,
+                    p_draft=torch.from_numpy(p_mod).cuda(), rng=(95, 1), out_tokens=out, n_accepted=nacc,
+                    top_k=k, top_p=p)
+    torch.cuda.synchronize()
+    assert sps.device_error() == 0
+    q_base = sps.softmax(logits, T).cpu().numpy()
+    qg = q.cpu().numpy()
+    np.testing.assert_array_equal(qg, omod.modify_rows(q_base, k, p))
+    w_out, w_n, _ = oacc.accept_resample(p_mod, qg, drafts, oacc.philox_uniforms(95, 1, B, K))
+    np.testing.assert_array_equal(out.cpu().numpy(), w_out)
+    np.testing.assert_array_equal(nacc.cpu().numpy(), w_n)
+
+
 def draft_run(sps, gd, kv, ctx, K, T, k, p, rng, ws):
     B = ctx.shape[0]
     toks = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
@@ -131,3 +174,26 @@ def test_draft_equal_to_target_accepts_everything_with_modifiers(sps):
         for b in range(2):
             if not bool(done[b]):
                 assert int(a[b]) == 4
+
+
+@pytest.mark.parametrize("T,k,p", [(1.0, 25, 0.85), (50.0, 0, 0.5)])
+def test_draft_step_with_modifiers_v32000(sps, T, k, p):
+    """The draft step's cut over several CUs at a 32000-token vocabulary:
+    its first distribution equals the oracle's cut of the plain one bit for
+    bit, and every drawn token lies in the kept set."""
+    B, K = 2, 3
+    gd, _ = build_pair(V32K, 96, std=0.2)
+    T_cap = 96
+    kv = sps.KVCache(V32K, B, T_cap)
+    install_prior(V32K, kv, new_cache(V32K, B, T_cap), 97, [30, 44])
+    ctx = torch.tensor([[5, 6], [7, 8]], dtype=torch.int32, device="cuda")
+    ws = sps.workspace(V32K, B, 2, T_cap)
+    _, p_plain = draft_run(sps, gd, kv, ctx, K, T, 0, 1.0, (98, 0), ws)
+    toks, p_mod = draft_run(sps, gd, kv, ctx, K, T, k, p, (98, 0), ws)
+    np.testing.assert_array_equal(p_mod[:, 0], omod.modify_rows(p_plain[:, 0], k, p))
+    for b in range(B):
+        for t in range(K):
+            row = p_mod[b, t]
+            if k:
+                assert 1 <= (row > 0).sum() <= k
+            assert row[toks[b, t + 1]] > 0

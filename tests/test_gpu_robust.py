@@ -134,25 +134,27 @@ def test_accept_nonfinite_inputs_bit_exact(sps):
     assert 0 in clean and 7 in clean
 
 
-def _verify(sps, gm, kv, toks, K, T, ws, p, rng):
+def _verify(sps, gm, kv, toks, K, T, ws, p, rng, top_k=0, top_p=1.0):
     B, V = toks.shape[0], gm.shape.vocab
     logits = torch.empty((B, K + 1, V), dtype=torch.float32, device="cuda")
     q = torch.empty_like(logits)
     out = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
     nacc = torch.empty(B, dtype=torch.int32, device="cuda")
     sps.verify_step(gm, kv, toks, K, T, ws, logits=logits, q=q, p_draft=p, rng=rng, out_tokens=out,
-                    n_accepted=nacc)
+                    n_accepted=nacc, top_k=top_k, top_p=top_p)
     torch.cuda.synchronize()
     return logits.cpu().numpy(), q.cpu().numpy(), out.cpu().numpy(), nacc.cpu().numpy()
 
 
-def test_verify_step_nonfinite_logits(sps):
+@pytest.mark.parametrize("top_k,top_p", [(0, 1.0), (20, 0.9)])
+def test_verify_step_nonfinite_logits(sps, top_k, top_p):
     """A NaN embedding row makes the logits of one sequence NaN (attention is
     per sequence; later positions see the NaN key and value, earlier ones
     take 0 x NaN from the masked position in the score product): its
     exported q rows are one-hot at token 0, its outcome is a = 0 and token
     0, the flag is raised, and the other sequences are bit-identical to a
-    clean run."""
+    clean run; with a top-k / nucleus cut too (the cut over several CUs
+    leaves such a row uncut)."""
     shape = configs.TINY_TARGET
     B, K, V = 3, 4, shape.vocab
     w = synth.weights(shape, 70)
@@ -173,8 +175,8 @@ def test_verify_step_nonfinite_logits(sps):
         kv.lengths.copy_(torch.tensor([5, 9, 2], dtype=torch.int32))
         ws = sps.workspace(shape, B, K + 1, 64)
         sps.device_error()
-        runs.append(_verify(sps, gm, kv, cuda(toks, torch.int32), K, 1.0, ws, cuda(p, torch.float32), (3, 1))
-                    + (sps.device_error(),))
+        runs.append(_verify(sps, gm, kv, cuda(toks, torch.int32), K, 1.0, ws, cuda(p, torch.float32), (3, 1),
+                            top_k, top_p) + (sps.device_error(),))
     (l0, q0, o0, n0, f0), (l1, q1, o1, n1, f1) = runs
     assert f0 == 0 and f1 & sps.DEV_NONFINITE
     for b in (0, 2):
@@ -188,10 +190,12 @@ def test_verify_step_nonfinite_logits(sps):
         assert q1[1, j, 0] == 1.0 and not q1[1, j, 1:].any()
 
 
-def test_draft_step_nonfinite_logits(sps):
+@pytest.mark.parametrize("top_k,top_p", [(0, 1.0), (20, 0.9)])
+def test_draft_step_nonfinite_logits(sps, top_k, top_p):
     """A draft whose logits are NaN for one sequence: its p rows are one-hot
     at token 0 (a valid draft distribution), its drafts are token 0, the
-    flag is raised; the other sequence is bit-identical to a clean run."""
+    flag is raised; the other sequence is bit-identical to a clean run (with
+    or without a top-k / nucleus cut)."""
     shape = configs.TINY_DRAFT
     B, K, V = 2, 3, shape.vocab
     w = synth.weights(shape, 80)
@@ -211,7 +215,7 @@ def test_draft_step_nonfinite_logits(sps):
         tokens = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
         p = torch.empty((B, K, V), dtype=torch.float32, device="cuda")
         sps.device_error()
-        sps.draft_step(gm, kv, cuda(ctx, torch.int32), K, 1.0, (4, 2), tokens, p, ws)
+        sps.draft_step(gm, kv, cuda(ctx, torch.int32), K, 1.0, (4, 2), tokens, p, ws, top_k, top_p)
         torch.cuda.synchronize()
         runs.append((tokens.cpu().numpy(), p.cpu().numpy(), sps.device_error()))
     (t0, p0, f0), (t1, p1, f1) = runs
