@@ -1040,6 +1040,137 @@ __global__ __launch_bounds__(kCutSegThreads) void cut_export_kernel(const float*
   }
 }
 
+// ---------------------------------------------------------------------------
+// The draft step's softmax export and draw over several CUs (temperature >
+// 0): draft_p_kernel's work-groups take one segment of a sequence's row
+// each -- the row statistics (stored by the cut-off kernels, or merged from
+// cut_part_kernel's wave partials, the same bits as row_stat), p_t written
+// for the segment and the total of its draw weights; draft_draw_kernel then
+// finds the segment holding the threshold from the totals and scans only
+// that segment. The draw is the one of draft_sample_kernel (integer inverse
+// CDF over the stored probabilities, in index order).
+// ---------------------------------------------------------------------------
+template <bool MOD>
+__device__ __forceinline__ uint64_t segment_probs(const float* __restrict__ z, const RowStat& st, float inv_t, int i0,
+                                                  int i1, float* __restrict__ pr) {
+  uint64_t w = 0;
+  for (int i = i0 + static_cast<int>(threadIdx.x); i < i1; i += kCutSegThreads) {
+    const float x = prob_final<MOD>(z[i], st, inv_t, i);
+    pr[i] = x;
+    w += fixed_weight(x);
+  }
+  return w;
+}
+
+__global__ __launch_bounds__(kCutSegThreads) void draft_p_kernel(const float* __restrict__ logits, int Mps, int V,
+                                                                 float temperature, const RowStat* __restrict__ pre,
+                                                                 char* __restrict__ cut, size_t cut_bytes, int seg,
+                                                                 float* __restrict__ p_out, int K, int t, int* err) {
+  __shared__ uint64_t s_w[kCutSegThreads / 64];
+  const int b = blockIdx.y, s = blockIdx.x;
+  const CutRowScratch cs = cut_row(cut, cut_bytes, b);
+  const RowStat st = pre ? pre[b] : stat_of_parts(cs.part);
+  if (!pre && st.nonfinite && s == 0 && threadIdx.x == 0) atomicOr(err, kErrNonFinite);   // one-hot at token 0
+  const float* z = logits + (static_cast<size_t>(b) * Mps + Mps - 1) * V;
+  float* pr = p_out + (static_cast<size_t>(b) * K + t) * V;
+  const float inv_t = 1.0f / temperature;
+  const int i0 = s * seg, i1 = min(V, i0 + seg);
+  uint64_t w = row_modified(st) ? segment_probs<true>(z, st, inv_t, i0, i1, pr)
+                                : segment_probs<false>(z, st, inv_t, i0, i1, pr);
+  w = wave_sum_u64(w);
+  if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = w;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t tot = 0;
+    for (int v = 0; v < kCutSegThreads / 64; ++v) tot += s_w[v];
+    cs.n[s] = tot;                                 // the histogram's slots: free once the cut is taken
+  }
+}
+
+constexpr int kDrawPer = 8;                        // entries per thread of the segment scan
+
+// One work-group per sequence. Threshold t of the row's total W (as
+// block_draw); the segment whose range of the cumulative weights holds it is
+// scanned with thread r owning kDrawPer consecutive entries per round.
+__global__ __launch_bounds__(kCutSegThreads) void draft_draw_kernel(const char* __restrict__ cut, size_t cut_bytes,
+                                                                    int nseg, int seg, int V,
+                                                                    const float* __restrict__ p_out, int K, int t,
+                                                                    int32_t* __restrict__ tokens,
+                                                                    const int32_t* __restrict__ ctx, uint64_t seed,
+                                                                    uint64_t loop, int* err) {
+  __shared__ uint64_t wsum[17];
+  __shared__ uint64_t s_thr, s_off;
+  __shared__ int s_seg, s_y;
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const CutRowScratch cs = cut_row(const_cast<char*>(cut), cut_bytes, b);
+  const size_t tok = static_cast<size_t>(b) * (K + 1);
+  // Wave 0: the segment totals in order (nseg <= 32), the threshold and the
+  // segment whose range of the cumulative weight holds it, for every wave.
+  if (tid < 64) {
+    const float u = philox_uniform(seed, loop, 0, b, t);
+    const uint64_t tot = tid < nseg ? cs.n[tid] : 0;
+    uint64_t inc = tot;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint64_t o = shfl_up_u64(inc, d);
+      if (tid >= d) inc += o;
+    }
+    const uint64_t W = shfl_u64(inc, 63);
+    const uint64_t thr = grid_threshold(u, W);
+    const uint64_t hit = W ? __ballot(tid < nseg && inc > thr) : 0;
+    const int sstar = hit ? __ffsll(static_cast<long long>(hit)) - 1 : -1;
+    const uint64_t off = shfl_u64(inc - tot, sstar < 0 ? 0 : sstar);   // weight before segment sstar
+    if (tid == 0) {
+      s_thr = thr;
+      s_off = off;
+      s_seg = sstar;
+      s_y = -1;
+    }
+  }
+  __syncthreads();
+  const int sstar = s_seg;
+  const uint64_t thr = s_thr;
+  if (sstar >= 0) {                                // uniform
+    const float* pr = p_out + (static_cast<size_t>(b) * K + t) * V;
+    const int i0 = sstar * seg, i1 = min(V, i0 + seg);
+    uint64_t run = s_off;
+    for (int base = i0; base < i1; base += kCutSegThreads * kDrawPer) {
+      uint64_t w[kDrawPer], lt = 0;
+      const int c0 = base + kDrawPer * tid;
+#pragma unroll
+      for (int k = 0; k < kDrawPer; ++k) {
+        const uint64_t x = fixed_weight(pr[min(c0 + k, i1 - 1)]);
+        w[k] = c0 + k < i1 ? x : 0;
+        lt += w[k];
+      }
+      uint64_t total;
+      const uint64_t ex = run + block_exscan_u64(lt, wsum, &total);
+      if (ex <= thr && thr < ex + lt) {            // exactly one thread
+        uint64_t acc = ex;
+        int hitk = -1;
+#pragma unroll
+        for (int k = 0; k < kDrawPer; ++k) {
+          acc += w[k];
+          if (hitk < 0 && acc > thr) hitk = k;
+        }
+        s_y = c0 + hitk;
+      }
+      __syncthreads();
+      if (s_y >= 0) break;                         // uniform
+      run += total;
+    }
+  }
+  if (tid == 0) {
+    int y = s_y;
+    if (y < 0) {                                   // every weight zero
+      y = 0;
+      atomicOr(err, kErrEmpty);
+    }
+    tokens[tok + t + 1] = y;
+    if (t == 0) tokens[tok] = ctx[2 * b + 1];
+  }
+}
+
 // Segment [b0, b1) of the vocabulary owned by this wave: a multiple of 64
 // entries, the waves' segments in order.
 struct Segment { int b0, b1; };
@@ -1407,15 +1538,31 @@ hipError_t launch_accept_logits(const float* p, const float* logits, const void*
 hipError_t launch_draft_sample(const float* logits, int Mps, int B, int V, float temperature, int top_k,
                                float top_p, float* p_out, int K, int t, int32_t* tokens, const int32_t* ctx,
                                uint64_t seed, uint64_t loop, void* stats, char* cut, int* err, hipStream_t st) {
-  if (cut && stats && modifiers_active(temperature, top_k, top_p, V) && V <= modifier_max_vocab()) {
-    // The cut over several CUs, then the draw from the stored statistics.
-    int seg = 0, nseg = 0;
+  if (cut && stats && temperature > 0.f && V <= modifier_max_vocab()) {
+    // Statistics (and the cut) over several CUs, then p_t and the draw.
+    const size_t cut_bytes = cut_row_bytes(V);
     RowStat* rs = reinterpret_cast<RowStat*>(stats);
-    const hipError_t e = cut_rows(logits, B, Mps, Mps - 1, V, temperature, top_k, top_p, rs, cut, err, &seg, &nseg,
-                                  st);
+    const bool mod = modifiers_active(temperature, top_k, top_p, V);
+    int seg = 0, nseg = 0;
+    hipError_t e = hipSuccess;
+    if (mod) {
+      e = cut_rows(logits, B, Mps, Mps - 1, V, temperature, top_k, top_p, rs, cut, err, &seg, &nseg, st);
+    } else {
+      nseg = std::max(1, std::min(32, (512 + B - 1) / B));
+      seg = (V + nseg - 1) / nseg;
+      nseg = (V + seg - 1) / seg;
+      hipLaunchKernelGGL(cut_part_kernel, dim3(kStatWaves, B), dim3(64), 0, st, logits, V, Mps, Mps - 1, temperature,
+                         cut, cut_bytes);
+      e = hipGetLastError();
+    }
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(draft_sample_kernel, dim3(B), dim3(kSampleThreads), 0, st, logits, Mps, V, temperature, top_k,
-                       top_p, rs, p_out, K, t, tokens, ctx, seed, loop, err);
+    hipLaunchKernelGGL(draft_p_kernel, dim3(nseg, B), dim3(kCutSegThreads), 0, st, logits, Mps, V, temperature,
+                       mod ? static_cast<const RowStat*>(rs) : static_cast<const RowStat*>(nullptr), cut, cut_bytes, seg,
+                       p_out, K, t, err);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(draft_draw_kernel, dim3(B), dim3(kCutSegThreads), 0, st, cut, cut_bytes, nseg, seg, V, p_out, K,
+                       t, tokens, ctx, seed, loop, err);
     return hipGetLastError();
   }
   size_t lds = 0;
