@@ -85,6 +85,34 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // One M tile with at most one output element per thread: the epilogue's
+  // memory inputs (the input norm's group sums of squares, the old residual
+  // and gain or the rotary table and length, FP8 row scales) are loaded
+  // before the weight stream, so that the tail after the last weight load
+  // waits on no memory round but its own stores.
+  constexpr int kMaxRows = MT * kRows;
+  constexpr bool kPre = MT == 1 && NTW * 256 <= WAVES * 64;
+  constexpr int kPreRows = kPre ? (kMaxRows + WAVES - 1) / WAVES : 1;
+  NormPre pre_norm[kPreRows];
+  EpiIn pre_in{0.f, 0.f, 0};
+  float pre_sc = 1.f, pre_sc2 = 1.f;
+  if constexpr (kPre) {
+#pragma unroll
+    for (int i = 0; i < kPreRows; ++i) pre_norm[i] = norm_prefetch(p, wave + i * WAVES, lane);
+    const int e = threadIdx.x;
+    if (e < NTW * 256) {
+      const int j = e >> 8, r = (e >> 6) & 3, ln = e & 63;
+      const int nt = nt0 + j, i = (ln >> 4) * 4 + r, col = ln & 15;
+      if (!(kRows == 8 && i >= 8) && nt < p.NT && i < M) {
+        pre_in = epilogue_inputs<EPI>(p, p.m0 + i, nt, col);
+        if (W8) {
+          pre_sc = p.wscale[nt * 16 + col];
+          if ((EPI == kEpiSwiglu || EPI == kEpiQkv) && col < 8) pre_sc2 = p.wscale[nt * 16 + col + 8];
+        }
+      }
+    }
+  }
+
   if constexpr (W8) {
     // Code tile pair kp of n-tile j: 64 lanes x 16 B at wq[j] + 64 kp.
     const u32x4* wq[NTW];
@@ -177,7 +205,6 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
   }
 
   // Sum the waves' partials in LDS (fixed order), then the epilogue.
-  constexpr int kMaxRows = MT * kRows;
   __shared__ float red[WAVES][NTW][MT][4][64];
   __shared__ float tot[NTW][MT][4][64];
   __shared__ float s_rs[kMaxRows];
@@ -193,9 +220,20 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) red[wave][j][mt][r][lane] = acc[j][mt][r];
   // Row scales of the input RMSNorm.
-  for (int m = wave; m < kMaxRows; m += WAVES) {
-    const float v = norm_scale(p, m, lane);
-    if (lane == 0) s_rs[m] = v;
+  if constexpr (kPre) {
+#pragma unroll
+    for (int i = 0; i < kPreRows; ++i) {
+      const int m = wave + i * WAVES;
+      if (m < kMaxRows) {
+        const float v = norm_from_pre(p, m, lane, pre_norm[i]);
+        if (lane == 0) s_rs[m] = v;
+      }
+    }
+  } else {
+    for (int m = wave; m < kMaxRows; m += WAVES) {
+      const float v = norm_scale(p, m, lane);
+      if (lane == 0) s_rs[m] = v;
+    }
   }
   __syncthreads();
   for (int e = threadIdx.x; e < NTW * MT * 256; e += WAVES * 64) {
@@ -223,12 +261,12 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_kernel(const GemmParams p) {
     if (nt >= p.NT || m >= M) continue;
     const int gm = p.m0 + m;
     const float rs = s_rs[m];
-    const float sc = W8 ? p.wscale[nt * 16 + col] : 1.f;
+    const float sc = !W8 ? 1.f : kPre ? pre_sc : p.wscale[nt * 16 + col];
     const float v = out_value(j, mt, r, ln) * rs * sc;
     const float v2 = (EPI == kEpiSwiglu || EPI == kEpiQkv) && col < 8
-                         ? out_value(j, mt, r, ln + 8) * rs * (W8 ? p.wscale[nt * 16 + col + 8] : 1.f)
+                         ? out_value(j, mt, r, ln + 8) * rs * (!W8 ? 1.f : kPre ? pre_sc2 : p.wscale[nt * 16 + col + 8])
                          : 0.f;
-    const float sq = epilogue_element<T, EPI>(p, gm, nt, col, v, v2);
+    const float sq = epilogue_apply<T, EPI>(p, gm, nt, col, v, v2, kPre ? pre_in : epilogue_inputs<EPI>(p, gm, nt, col));
     if (EPI == kEpiResid && nt * 16 + col < p.n_valid) s_sq[m][j * 16 + col] = sq;
   }
   if (EPI == kEpiResid) {

@@ -44,6 +44,35 @@ __device__ __forceinline__ float norm_scale(const GemmParams& p, int m, int lane
   return norm_finish(p, m, lane, norm_first(p, m, lane));
 }
 
+// The same row scale with a lane's first kNormPre groups loaded ahead (by
+// norm_prefetch, e.g. before a GEMM's main loop, so that the loads' latency
+// hides under the weight stream); norm_from_pre adds them and any further
+// groups in the order norm_scale does, so the result is the same bits.
+constexpr int kNormPre = 4;
+struct NormPre {
+  float v[kNormPre];
+};
+__device__ __forceinline__ NormPre norm_prefetch(const GemmParams& p, int m, int lane) {
+  NormPre r;
+  const bool on = p.ss_in && m < p.M;
+#pragma unroll
+  for (int q = 0; q < kNormPre; ++q) {
+    const int g = lane + 64 * q;
+    r.v[q] = on && g < p.ng_in ? p.ss_in[static_cast<size_t>(g) * p.Mtot + p.m0 + m] : 0.f;
+  }
+  return r;
+}
+__device__ __forceinline__ float norm_from_pre(const GemmParams& p, int m, int lane, const NormPre& r) {
+  if (!p.ss_in || m >= p.M) return 1.f;
+  float s = r.v[0];
+#pragma unroll
+  for (int q = 1; q < kNormPre; ++q)
+    if (lane + 64 * q < p.ng_in) s += r.v[q];
+  for (int g = lane + 64 * kNormPre; g < p.ng_in; g += 64) s += p.ss_in[static_cast<size_t>(g) * p.Mtot + p.m0 + m];
+  s = wave_sum(s);
+  return 1.0f / sqrtf(s * p.inv_d + p.eps);
+}
+
 // Inputs of an element's epilogue that live in memory: the old residual
 // value and the norm gain (kEpiResid), the sequence's length and the rotary
 // (cos, sin) of a q / k pair (kEpiQkv). Loading them for several elements
@@ -134,12 +163,6 @@ __device__ __forceinline__ float epilogue_apply(const GemmParams& p, int gm, int
     }
   }
   return 0.f;
-}
-
-// One element's whole epilogue (loads, then epilogue_apply).
-template <typename T, int EPI>
-__device__ __forceinline__ float epilogue_element(const GemmParams& p, int gm, int nt, int col, float v, float v2) {
-  return epilogue_apply<T, EPI>(p, gm, nt, col, v, v2, epilogue_inputs<EPI>(p, gm, nt, col));
 }
 
 }  // namespace sps
