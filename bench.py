@@ -96,6 +96,16 @@ def measured_trace(weights="bf16"):
     return {k: t[k] for k in ("avg_launch_us", "achieved", "frac", "stream_read_gbs", "source") if k in t}
 
 
+def profiled_figures(shape_name, weights, B, K, ctx):
+    """The rocprofv3 figures of profiles/ (traffic, MFMA utilisation, traced
+    launch average) for a run of the workload they were taken on -- the
+    70B-shaped verify step at K = 4, B = 1, ctx 2048, in the run's weight
+    format -- and None for any other workload, whose launches differ."""
+    if shape_name != "70b" or (B, K, ctx) != (1, 4, 2048):
+        return {"traffic": None, "mfma": None, "trace": None}
+    return {"traffic": measured_traffic(weights), "mfma": measured_mfma(weights), "trace": measured_trace(weights)}
+
+
 def _counter_rows(path):
     """rocprofv3 counter-collection CSV: {dispatch id: {name, grid, counters, seconds}}."""
     import csv
@@ -776,13 +786,14 @@ def main():
         g_avg_ms = g_ms / g_n
         g_gbs = (g_bytes / g_n) / (g_avg_ms * 1e-3) / 1e9
         log("gemm: %d launches, avg %.1f us, %.1f GB/s" % (g_n, g_avg_ms * 1e3, g_gbs))
+        prof = profiled_figures(args.shape, args.weights, B, K, ctx)
         roofline = {"bound": "hbm", "kernel": "gemm_kernel (weight-streaming skinny GEMM, all linear layers)",
                     "achieved": round(g_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(g_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(args.weights),
+                    "frac": round(g_gbs / HBM_PEAK_GBS, 4), "traffic": prof["traffic"],
                     "launches_per_step": g_n // args.steps, "avg_launch_us": round(g_avg_ms * 1e3, 2),
                     "bytes_per_launch": g_bytes / g_n,
-                    "frac_of_stream_read": round(g_gbs / read_gbs, 4), "mfma": measured_mfma(args.weights),
-                    "trace": measured_trace(args.weights)}
+                    "frac_of_stream_read": round(g_gbs / read_gbs, 4), "mfma": prof["mfma"],
+                    "trace": prof["trace"]}
     del kv, ws
     torch.cuda.empty_cache()     # the end-to-end caches differ in size from the timing cache
 

@@ -36,3 +36,15 @@ def test_verify_bytes_at_the_quoted_shapes():
     # FP8 projections: one byte per weight plus a scale per output row.
     b70_8 = bench.verify_bytes(s70.with_(dtype="fp8"), 1, 4, 2048)
     assert 69e9 < b70_8 < 71e9, b70_8
+
+
+def test_profile_figures_only_for_the_profiled_workload():
+    # profiles/ holds counters and traces of the 70B verify step at K = 4,
+    # B = 1, ctx 2048; another shape or workload must not report them.
+    import bench
+    for args in (("7b", "bf16", 1, 4, 2048), ("70b", "bf16", 16, 8, 2048), ("70b", "bf16", 1, 4, 8192),
+                 ("70b", "fp8", 4, 4, 2048)):
+        assert bench.profiled_figures(*args) == {"traffic": None, "mfma": None, "trace": None}, args
+    got = bench.profiled_figures("70b", "bf16", 1, 4, 2048)
+    assert got["traffic"] == bench.measured_traffic("bf16")
+    assert got["trace"] == bench.measured_trace("bf16")
