@@ -72,6 +72,50 @@ def test_draft_step_stays_inside_its_workspace(sps):
     assert bool(((tokens >= 0) & (tokens < V)).all())
 
 
+@pytest.mark.parametrize("B,top_p", [(40, 1.0), (64, 1.0), (64, 0.9)])
+def test_draft_draw_at_large_batch(sps, B, top_p):
+    """The draft draw over 32000-token rows at B = 40 and 64, where a row is
+    cut into 13 and 8 segments and the chosen segment is scanned in two
+    rounds: every drawn token equals the oracle's integer inverse-CDF draw
+    from the exported p row with the same Philox uniform, every exported row
+    is a distribution, and with nucleus 0.9 the first row of each sequence
+    is the oracle's cut of the unmodified run's row, bit for bit."""
+    from oracle import modifiers as omod
+    from oracle import philox as ophil
+    shape = configs.DRAFT_70B.with_(n_layers=1)
+    K, T_cap, V = 3, 64, shape.vocab
+    print("draft draw B", B, "top_p", top_p, flush=True)
+    gm = sps.Model(shape, synth.weights(shape, 42))
+    kv = sps.KVCache(shape, B, T_cap)
+    ws = sps.workspace(shape, B, 2, T_cap)
+    ctx = cuda(synth.tokens(43, B, 2, V), torch.int32)
+    seed, loop = 44, 5
+
+    def run(p_nuc):
+        kv.buf.zero_()
+        kv.lengths.fill_(8)
+        tokens = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+        p = torch.empty((B, K, V), dtype=torch.float32, device="cuda")
+        sps.draft_step(gm, kv, ctx, K, 1.0, (seed, loop), tokens, p, ws, 0, p_nuc)
+        torch.cuda.synchronize()
+        assert sps.device_error() == 0
+        return tokens.cpu().numpy(), p.cpu().numpy()
+
+    got_t, got_p = run(top_p)
+    np.testing.assert_array_equal(got_t[:, 0], ctx.cpu().numpy()[:, 1])
+    ud = ophil.uniforms(seed, loop, ophil.PURPOSE_DRAFT, B, K)
+    for b in range(B):
+        for t in range(K):
+            row = got_p[b, t]
+            assert np.isfinite(row).all() and (row >= 0).all()
+            assert abs(float(row.astype(np.float64).sum()) - 1.0) < 1e-4
+            y, ok = osamp.categorical(osamp.to_weights(row), ud[b, t])
+            assert ok and got_t[b, t + 1] == y, (b, t, y, got_t[b, t + 1])
+    if top_p < 1.0:
+        _, p_plain = run(1.0)
+        np.testing.assert_array_equal(got_p[:, 0], omod.modify_rows(p_plain[:, 0], 0, top_p))
+
+
 # ----------------------------------------------------------- non-finite --
 
 def test_softmax_nonfinite_rows(sps):
