@@ -97,7 +97,9 @@ hipError_t launch_accept_logits(const float* p, const float* logits, const void*
                                 int32_t* n_acc, int* err, hipStream_t st);
 // Draft step t: p_t of each sequence's last row into p_out and x~_{t+1}
 // drawn from it. stats (B rows) and cut (B x cut_row_bytes(V)), if given,
-// are scratch for a cut over several CUs when a modifier is on.
+// are scratch for the statistics, the cut (when a modifier is on), the
+// export and the draw over several CUs at temperature > 0 and V up to the
+// cut-off's largest row; otherwise one work-group per sequence does all.
 hipError_t launch_draft_sample(const float* logits, int Mps, int B, int V, float temperature,
                                int top_k, float top_p, float* p_out, int K, int t, int32_t* tokens,
                                const int32_t* ctx, uint64_t seed, uint64_t loop, void* stats, char* cut, int* err,

@@ -1474,25 +1474,34 @@ static hipError_t cutoff_lds(const void* kernel, float temperature, int top_k, f
   return hipSuccess;
 }
 
+// Segments of a row for the kernels that take one segment per work-group:
+// about 512 work-groups per launch, at most 32 per row (the draw scans the
+// segment totals with one wave); every segment non-empty.
+static void cut_segments(int rows, int V, int* seg, int* nseg) {
+  const int n = std::max(1, std::min(32, (512 + rows - 1) / rows));
+  *seg = (V + n - 1) / n;
+  *nseg = (V + *seg - 1) / *seg;
+}
+
 // The cut-off over several CUs for `rows` rows (logits row r rstride +
 // roff), their statistics into stats[0 .. rows).
 static hipError_t cut_rows(const float* logits, int rows, int rstride, int roff, int V, float temperature, int top_k,
                            float top_p, RowStat* stats, char* cut, int* err, int* seg_out, int* nseg_out,
                            hipStream_t st) {
   const size_t cut_bytes = cut_row_bytes(V);
-  const int nseg = std::max(1, std::min(32, (512 + rows - 1) / rows));   // ~512 work-groups per launch
-  const int seg = (V + nseg - 1) / nseg;
+  int seg = 0, nseg = 0;
+  cut_segments(rows, V, &seg, &nseg);
   size_t lds = 0;
   hipError_t e = cutoff_lds(reinterpret_cast<const void*>(&cut_select_kernel), temperature, top_k, top_p, V, &lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(cut_part_kernel, dim3(kStatWaves, rows), dim3(64), 0, st, logits, V, rstride, roff, temperature,
                      cut, cut_bytes);
-  hipLaunchKernelGGL(cut_hist_kernel, dim3((V + seg - 1) / seg, rows), dim3(kCutSegThreads), 0, st, logits, V, rstride,
+  hipLaunchKernelGGL(cut_hist_kernel, dim3(nseg, rows), dim3(kCutSegThreads), 0, st, logits, V, rstride,
                      roff, temperature, stats, cut, cut_bytes, seg);
   hipLaunchKernelGGL(cut_select_kernel, dim3(rows), dim3(kSampleThreads), lds, st, logits, V, rstride, roff,
                      temperature, top_k, top_p, stats, cut, cut_bytes, err);
   *seg_out = seg;
-  *nseg_out = (V + seg - 1) / seg;
+  *nseg_out = nseg;
   return hipGetLastError();
 }
 
@@ -1548,9 +1557,7 @@ hipError_t launch_draft_sample(const float* logits, int Mps, int B, int V, float
     if (mod) {
       e = cut_rows(logits, B, Mps, Mps - 1, V, temperature, top_k, top_p, rs, cut, err, &seg, &nseg, st);
     } else {
-      nseg = std::max(1, std::min(32, (512 + B - 1) / B));
-      seg = (V + nseg - 1) / nseg;
-      nseg = (V + seg - 1) / seg;
+      cut_segments(B, V, &seg, &nseg);
       hipLaunchKernelGGL(cut_part_kernel, dim3(kStatWaves, B), dim3(64), 0, st, logits, V, Mps, Mps - 1, temperature,
                          cut, cut_bytes);
       e = hipGetLastError();
