@@ -20,7 +20,7 @@ about as often as the paper's trained drafts (and on an unrelated random
 pair beside it), and the CPU oracle timed on a bounded sample.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--K 4] [--B 1] [--ctx 2048]
-    python bench.py --sweep | --accept-grid | --k-study | --draft-step | --cpu-oracle
+    python bench.py --sweep | --accept-grid | --k-study | --draft-step | --softmax | --cpu-oracle
 """
 import argparse
 import json
@@ -659,6 +659,27 @@ def accept_grid(args):
                     "the oracle (numpy, as it stands) on host copies of the same inputs, one call"}
 
 
+def softmax_rows(args):
+    """sps_softmax alone (one work-group per row) on 5 rows of 32000 logits
+    ~ N(0, 2^2), the verify step's row count at K = 4: plain, nucleus 0.8
+    and top-k 50 at --temperature; four input sets used in turn."""
+    import torch
+    from paper_2302_01318_amd import sps
+    rows, V = 5, 32000
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(args.seed)
+    sets = [torch.randn((rows, V), generator=gen, device="cuda") * 2.0 for _ in range(4)]
+    out = torch.empty((rows, V), device="cuda")
+    res = []
+    for name, k, p in (("plain", 0, 1.0), ("nucleus 0.8", 0, 0.8), ("top-k 50", 50, 1.0)):
+        ms = timed(lambda i: sps.softmax(sets[i % 4], args.temperature, k, p, out), 50, 5)
+        assert sps.device_error() == 0
+        res.append({"setting": name, "top_k": k, "top_p": p, "us": round(ms * 1e3, 2)})
+        print("softmax %s: %.2f us" % (name, ms * 1e3), file=sys.stderr, flush=True)
+    return {"metric": "sps_softmax us per call", "rows": rows, "V": V, "temperature": args.temperature,
+            "softmax": res}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -683,6 +704,8 @@ def main():
     ap.add_argument("--accept-grid", action="store_true", help="accept/resample alone over the B x K grid")
     ap.add_argument("--cpu-oracle", action="store_true",
                     help="the oracle's CPU time: tiny pair end to end, 7B and 70B verify (extrapolated)")
+    ap.add_argument("--softmax", action="store_true",
+                    help="sps_softmax alone on 5 x 32000 rows: plain, nucleus 0.8, top-k 50")
     ap.add_argument("--draft-step", action="store_true",
                     help="the draft side alone: K draft tokens per step (draft weights per --weights)")
     ap.add_argument("--k-study", action="store_true",
@@ -709,9 +732,10 @@ def main():
     if args.cpu_oracle:
         print(json.dumps(cpu_oracle(args)), flush=True)
         return
-    if args.sweep or args.accept_grid or args.k_study or args.draft_step:
+    if args.sweep or args.accept_grid or args.k_study or args.draft_step or args.softmax:
         res = (sweep(args) if args.sweep else accept_grid(args) if args.accept_grid else
-               draft_step_bench(args) if args.draft_step else k_study(args))
+               draft_step_bench(args) if args.draft_step else softmax_rows(args) if args.softmax else
+               k_study(args))
         print(json.dumps(res), flush=True)
         return
 

@@ -287,9 +287,12 @@ def philox_uniforms(seed, loop, purpose, B, n, device="cuda"):
     return out
 
 
-def softmax(logits, temperature, top_k=0, top_p=1.0):
+def softmax(logits, temperature, top_k=0, top_p=1.0, out=None):
     rows, V = logits.reshape(-1, logits.shape[-1]).shape
-    out = torch.empty_like(logits)
+    if out is None:
+        out = torch.empty_like(logits)
+    elif out.shape != logits.shape:
+        raise ValueError("out has shape %s, logits %s" % (tuple(out.shape), tuple(logits.shape)))
     check(lib.sps_softmax(_ptr(logits, torch.float32, "logits"), rows, V, sampling_of(temperature, top_k, top_p),
                           _ptr(out),
                           _stream()), "sps_softmax")
