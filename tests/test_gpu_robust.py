@@ -78,8 +78,9 @@ def test_draft_draw_at_large_batch(sps, B, top_p):
     cut into 13 and 8 segments and the chosen segment is scanned in two
     rounds: every drawn token equals the oracle's integer inverse-CDF draw
     from the exported p row with the same Philox uniform, every exported row
-    is a distribution, and with nucleus 0.9 the first row of each sequence
-    is the oracle's cut of the unmodified run's row, bit for bit."""
+    is a distribution, a rerun gives the same bits, and with nucleus 0.9 the
+    first row of each sequence is the oracle's cut of the unmodified run's
+    row, bit for bit."""
     from oracle import modifiers as omod
     from oracle import philox as ophil
     shape = configs.DRAFT_70B.with_(n_layers=1)
@@ -103,6 +104,10 @@ def test_draft_draw_at_large_batch(sps, B, top_p):
 
     got_t, got_p = run(top_p)
     np.testing.assert_array_equal(got_t[:, 0], ctx.cpu().numpy()[:, 1])
+    # A rerun is bit-identical (the histograms' atomics add integers).
+    again_t, again_p = run(top_p)
+    np.testing.assert_array_equal(again_t, got_t)
+    assert again_p.tobytes() == got_p.tobytes()
     ud = ophil.uniforms(seed, loop, ophil.PURPOSE_DRAFT, B, K)
     for b in range(B):
         for t in range(K):
