@@ -260,8 +260,12 @@ def device_model(sps, synth, shape, seed):
 E2E_CODE_PERT = 0.5       # draft logit perturbation of the end-to-end coupled pair
 
 
-def coupled_model(sps, synth, shape, model_seed, code_pert, st):
-    m = sps.Model(shape)
+def coupled_model(sps, synth, shape, model_seed, code_pert, st, into=None):
+    """One model of the coupled pair; packed into the buffers of `into` (a
+    model of the same shape) when given. Reusing the buffers matters for
+    timing: a generation right after the 70B target was freed and a new one
+    allocated ran 28.0 instead of 27.3 ms per loop (the next one 27.3)."""
+    m = into if into is not None else sps.Model(shape)
     for (name, layer), t in synth.coupled_device_weights(shape, st["pair_seed"], model_seed, st["layer_std"],
                                                          code_pert, st["logit_std"], st["rank"]):
         m.pack(name, layer, t)
@@ -569,7 +573,7 @@ def k_study(args):
     reps = args.reps or st["reps"]
     n_new, plen = st["n_new"], st["prompt"]
 
-    coupled = lambda shp, seed, pert: coupled_model(sps, synth, shp, seed, pert, st)
+    coupled = lambda shp, seed, pert, into=None: coupled_model(sps, synth, shp, seed, pert, st, into)
 
     target = coupled(shape, args.seed + 1, 0.0)
     gen = torch.Generator(device="cuda")
@@ -580,8 +584,11 @@ def k_study(args):
 
     def generations(draft, K):
         g = sps.Generator(target, draft, 1, T_cap, K)
-        g.prefill(prompts[0])                 # untimed warm-up: first launches load code objects
-        g.run(2 * (K + 1), args.temperature, args.seed + 999, top_k=args.top_k, top_p=args.top_p)
+        # Untimed warm-up on the timed runs' code path (accepted_log included:
+        # its per-loop device ops are kernels too): first launches load code
+        # objects.
+        g.prefill(prompts[0])
+        g.run(2 * (K + 1), args.temperature, args.seed + 999, accepted_log=[], top_k=args.top_k, top_p=args.top_p)
         times, accepted, loops = [], [], 0
         for r in range(reps):
             g.prefill(prompts[r])
@@ -608,8 +615,9 @@ def k_study(args):
     ars = generations(None, 0)
     log("ArS: %.2f ms/token" % ars["ms_per_token"])
     rows = []
+    draft = None
     for i, sd in enumerate(perts):
-        draft = coupled(dshape, args.seed + 2 + i, sd)
+        draft = coupled(dshape, args.seed + 2 + i, sd, draft)   # one set of draft buffers (see coupled_model)
         for K in Ks:
             r = generations(draft, K)
             r["code_pert"] = sd
@@ -618,8 +626,8 @@ def k_study(args):
             log("draft pert %.2f K %d: accepted %.2f per loop, %.2f ms/token, %.2fx ArS, time-to-%d p50 %.3f "
                 "p90 %.3f s" % (sd, K, r["mean_accepted"], r["ms_per_token"], r["speedup_vs_ars"], n_new,
                                 r["time_s"]["p50"], r["time_s"]["p90"]))
-        del draft
-        torch.cuda.empty_cache()
+    del draft
+    torch.cuda.empty_cache()
     return {"k_study": rows, "ars": ars, "layer_std": st["layer_std"], "prompt": plen,
             "n_new": n_new, "temperature": args.temperature, "top_k": args.top_k, "top_p": args.top_p,
             "target_weights": shape.dtype, "draft_weights": dshape.dtype,
@@ -835,11 +843,13 @@ def main():
             out = {}
             for name, d_, k in (("sps", dm, K), ("ars", None, 0))[:2 if ars else 1]:
                 g = sps.Generator(tgt, d_, B, Tc, k)
-                # An untimed short generation first: the first launch of each
-                # kernel loads its code object (up to ~0.16 s), which would
-                # otherwise land inside the timed run.
+                # An untimed short generation first, on the timed run's code
+                # path (accepted_log included: its per-loop device ops are
+                # kernels too): the first launch of each kernel loads its code
+                # object (up to ~0.16 s), which would otherwise land inside the
+                # timed run.
                 g.prefill(prompt)
-                g.run(2 * (k + 1), T, args.seed + 999, top_k=top_k, top_p=top_p)
+                g.run(2 * (k + 1), T, args.seed + 999, accepted_log=[], top_k=top_k, top_p=top_p)
                 g.prefill(prompt)
                 torch.cuda.synchronize()
                 acc_log = []
@@ -861,24 +871,22 @@ def main():
         torch.cuda.synchronize()
         log("draft packed: %.1f GB in %.1f s" % (draft.packed.numel() / 1e9, time.time() - t0))
         e2e["unrelated"] = pair_run(target, draft, "unrelated pair")
-        del draft, target
-        torch.cuda.empty_cache()
         st = configs.K_STUDY
-        coupled = lambda shp, seed, pert: coupled_model(sps, synth, shp, seed, pert, st)
-        target = coupled(shape, args.seed + 1, 0.0)
-        draft = coupled(dshape, args.seed + 2, E2E_CODE_PERT)
+        coupled = lambda shp, seed, pert, into: coupled_model(sps, synth, shp, seed, pert, st, into)
+        # The coupled pair goes into the same device buffers (see coupled_model).
+        target = coupled(shape, args.seed + 1, 0.0, target)
+        draft = coupled(dshape, args.seed + 2, E2E_CODE_PERT, draft)
         e2e["coupled"] = pair_run(target, draft, "coupled pair")
-        del draft
-        torch.cuda.empty_cache()
         if dshape.dtype != "fp8":
             # The same coupled pair with the draft's projections in weight-only
             # FP8: half the draft's bytes per token. The accepted tokens still
             # follow the bf16 target exactly (any draft does); only the
             # acceptance rate and the draft time change.
-            draft = coupled(dshape.with_(dtype="fp8"), args.seed + 2, E2E_CODE_PERT)
-            e2e["coupled_fp8_draft"] = pair_run(target, draft, "coupled pair, fp8 draft", ars=False)
-            del draft
-            torch.cuda.empty_cache()
+            draft8 = coupled(dshape.with_(dtype="fp8"), args.seed + 2, E2E_CODE_PERT, None)
+            e2e["coupled_fp8_draft"] = pair_run(target, draft8, "coupled pair, fp8 draft", ars=False)
+            del draft8
+        del draft
+        torch.cuda.empty_cache()
 
     result = {
         "metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
