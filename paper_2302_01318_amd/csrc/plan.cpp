@@ -97,6 +97,12 @@ int attn_partials(int T_cap) {
 
 int modifier_max_vocab() { return kPerLane * kSampleThreads; }
 
+void cut_segments(int rows, int V, int* seg, int* nseg) {
+  const int n = std::max(1, std::min(kMaxRowSegments, (512 + rows - 1) / rows));
+  *seg = (V + n - 1) / n;
+  *nseg = (V + *seg - 1) / *seg;
+}
+
 // ---- buffer layouts ----------------------------------------------------
 
 bool valid_config(const sps_config* c) {

@@ -147,6 +147,14 @@ size_t workspace_bytes(const sps_config* cfg, int B, int max_tokens_per_seq, int
 // where the vocabulary is past what the cut-off handles.
 size_t cut_row_bytes(int V);
 
+// Segments of a row for the sampling kernels that take one segment per
+// work-group (the cut-off's histogram, the draft export): about 512
+// work-groups per launch, at most kMaxRowSegments per row (the draft draw
+// scans the segment totals with one wave), every segment non-empty:
+// *nseg = ceil(V / *seg). rows >= 1, V >= 1.
+constexpr int kMaxRowSegments = 32;
+void cut_segments(int rows, int V, int* seg, int* nseg);
+
 // Bytes of split-K partials the launches of one forward over M rows write.
 size_t forward_part_bytes(const Layout& L, int M);
 

@@ -1104,7 +1104,8 @@ __global__ __launch_bounds__(kCutSegThreads) void draft_draw_kernel(const char* 
   const int b = blockIdx.x, tid = threadIdx.x;
   const CutRowScratch cs = cut_row(const_cast<char*>(cut), cut_bytes, b);
   const size_t tok = static_cast<size_t>(b) * (K + 1);
-  // Wave 0: the segment totals in order (nseg <= 32), the threshold and the
+  static_assert(kMaxRowSegments <= 64, "one wave holds the segment totals");
+  // Wave 0: the segment totals in order (nseg <= kMaxRowSegments), the threshold and the
   // segment whose range of the cumulative weight holds it, for every wave.
   if (tid < 64) {
     const float u = philox_uniform(seed, loop, 0, b, t);
@@ -1472,15 +1473,6 @@ static hipError_t cutoff_lds(const void* kernel, float temperature, int top_k, f
     }
   }
   return hipSuccess;
-}
-
-// Segments of a row for the kernels that take one segment per work-group:
-// about 512 work-groups per launch, at most 32 per row (the draw scans the
-// segment totals with one wave); every segment non-empty.
-static void cut_segments(int rows, int V, int* seg, int* nseg) {
-  const int n = std::max(1, std::min(32, (512 + rows - 1) / rows));
-  *seg = (V + n - 1) / n;
-  *nseg = (V + *seg - 1) / *seg;
 }
 
 // The cut-off over several CUs for `rows` rows (logits row r rstride +

@@ -13,6 +13,8 @@
 //    sequence uses, and is 0 for requests no call admits (quickly: no loop
 //    over the requested count);
 //  * wide-GEMM plans cover their matrix; attention partials fit their region;
+//  * the sampling kernels' row segments tile every row, none empty, at most
+//    kMaxRowSegments per row;
 //  * config validation and the packed layout do no undefined arithmetic on
 //    extreme field values.
 #include <climits>
@@ -116,6 +118,22 @@ static void check_wide_plans() {
         }
 }
 
+// Row segments of the sampling kernels: between 1 and kMaxRowSegments per
+// row, none empty, together covering the row; about 512 work-groups per
+// launch at most.
+static void check_segments() {
+  const int Vs[] = {1, 2, 7, 31, 32, 33, 1000, 1024, 4095, 12289, 32000, 32768};
+  for (int rows = 1; rows <= kMaxRows; ++rows)
+    for (int V : Vs) {
+      int seg = 0, nseg = 0;
+      cut_segments(rows, V, &seg, &nseg);
+      CHECK(nseg >= 1 && nseg <= kMaxRowSegments && seg >= 1, "segments of rows %d V %d: %d x %d", rows, V, nseg, seg);
+      CHECK(static_cast<long>(nseg) * seg >= V && static_cast<long>(nseg - 1) * seg < V,
+            "segments of rows %d V %d do not tile the row: %d x %d", rows, V, nseg, seg);
+      CHECK(static_cast<long>(nseg) * rows <= 512 + rows, "rows %d V %d: %d segments per row", rows, V, nseg);
+    }
+}
+
 static void check_extremes() {
   const int vals[] = {INT_MIN, -1, 0, 1, 2, 31, 32, 64, 128, 4096, 16384, 16416, 1 << 20, (1 << 24) - 1, 1 << 24,
                       INT_MAX};
@@ -173,6 +191,7 @@ int main() {
   };
   for (const auto& s : shapes) check_shape(s.c, s.name);
   check_wide_plans();
+  check_segments();
   check_extremes();
   if (failures) {
     std::fprintf(stderr, "%d failures\n", failures);
