@@ -91,10 +91,14 @@ hipError_t launch_row_softmax(const float* logits, int rows, int V, float temper
 hipError_t launch_accept_probs(const float* p, const float* q, const int32_t* drafts,
                                const float* unif, uint64_t seed, uint64_t loop, int B, int K,
                                int V, int32_t* out, int32_t* n_acc, int* err, hipStream_t st);
+// The verify step's fused accept / resample (q from the logits and their
+// row statistics). cut (B x cut_row_bytes(V) bytes of scratch), if given,
+// takes the final draw over several CUs (V up to the cut-off's largest
+// row); otherwise one work-group per sequence does all.
 hipError_t launch_accept_logits(const float* p, const float* logits, const void* stats,
                                 float temperature, const int32_t* tokens, const float* unif,
                                 uint64_t seed, uint64_t loop, int B, int K, int V, int32_t* out,
-                                int32_t* n_acc, int* err, hipStream_t st);
+                                int32_t* n_acc, char* cut, int* err, hipStream_t st);
 // Draft step t: p_t of each sequence's last row into p_out and x~_{t+1}
 // drawn from it. stats (B rows) and cut (B x cut_row_bytes(V)), if given,
 // are scratch for the statistics, the cut (when a modifier is on), the

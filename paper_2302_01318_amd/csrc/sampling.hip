@@ -1320,11 +1320,63 @@ __device__ __forceinline__ int accept_draw(const Row& qr, const float* __restric
   return __syncthreads_or(nf) ? -2 : y;
 }
 
+// The accept tests of sequence b, left to right, r_t p_t(x~_t) < q_t(x~_t)
+// exact in fp64 (wave 0 of the work-group; lane t tests draft t): a = the
+// first rejected draft (K if none), bad = x~_a is out of range, nf = a value
+// the tests read or a target row of the sequence is non-finite. Every lane
+// of the wave returns the same values. drafts[t] is x~_{t+1}.
+template <class QS>
+__device__ __forceinline__ void accept_tests(const QS& qs, const float* __restrict__ p,
+                                             const int32_t* __restrict__ dr, const float* __restrict__ unif,
+                                             uint64_t seed, uint64_t loop, int K, int V, int b, int* a_out,
+                                             bool* bad_out, bool* nf_out) {
+  const int tid = threadIdx.x;
+  bool rejected = false, bad = false, nf = false;
+  if (tid < K) {
+    const int x = dr[tid];
+    if (x < 0 || x >= V) {
+      bad = true;
+      rejected = true;
+    } else {
+      const float rho = qs.row(b * (K + 1) + tid)(x);
+      const float pi = p[(static_cast<size_t>(b) * K + tid) * V + x];
+      const float r = unif ? unif[b * (K + 1) + tid] : philox_uniform(seed, loop, 1, b, tid);
+      nf = not_finite(rho) | not_finite(pi);
+      rejected = !(static_cast<double>(r) * static_cast<double>(pi) < static_cast<double>(rho));
+    }
+  }
+  if (tid <= K) nf |= qs.row(b * (K + 1) + tid).nonfinite();
+  const uint64_t rej = __ballot(rejected);
+  const uint64_t badm = __ballot(bad);
+  *nf_out = __ballot(nf) != 0;                     // wave-wide, outside any branch
+  const int a = rej ? __ffsll(static_cast<long long>(rej)) - 1 : K;
+  *a_out = a;
+  *bad_out = a < K && ((badm >> a) & 1ull) != 0;
+}
+
+// The outcome of sequence b from a and the draw y (-2: a non-finite value
+// was read, -1: every weight zero): out[b][0 .. K] = the accepted drafts, the
+// drawn token, then -1; n_acc[b] = a. A sequence whose inputs hold a
+// non-finite value -- a target row with a NaN / +Inf logit, a NaN or
+// infinite gathered probability, or one in a row of the final draw -- has
+// no defined outcome: it is given a = 0 and token 0, and the device flag is
+// raised.
+__device__ __forceinline__ void accept_finish(int b, int a, int y, const int32_t* __restrict__ dr, int K,
+                                              int32_t* __restrict__ out, int32_t* __restrict__ n_acc, int* err) {
+  const int tid = threadIdx.x;
+  if (y == -2) {
+    a = 0;
+    y = 0;
+    if (tid == 0) atomicOr(err, kErrNonFinite);
+  } else if (y < 0) {
+    y = 0;
+    if (tid == 0) atomicOr(err, kErrEmpty);
+  }
+  if (tid <= K) out[static_cast<size_t>(b) * (K + 1) + tid] = tid < a ? dr[tid] : (tid == a ? y : -1);
+  if (tid == 0) n_acc[b] = a;
+}
+
 // One block per sequence. drafts[b * dstride + doff + t] is x~_{t+1}.
-// A sequence whose inputs hold a non-finite value -- a target row with a
-// NaN / +Inf logit, a NaN or infinite gathered probability, or one in a row
-// of the final draw -- has no defined outcome: it is given a = 0 and token
-// 0, and the device flag is raised.
 template <class QS>
 __global__ __launch_bounds__(kSampleThreads) void accept_kernel(QS qs, const float* __restrict__ p,
                                                                 const int32_t* __restrict__ drafts, int dstride,
@@ -1337,31 +1389,20 @@ __global__ __launch_bounds__(kSampleThreads) void accept_kernel(QS qs, const flo
   const int b = blockIdx.x, tid = threadIdx.x;
   const int32_t* dr = drafts + static_cast<size_t>(b) * dstride + doff;
 
-  // 1. left-to-right accept tests r_t * p_t(x~_t) < q_t(x~_t), exact in fp64
+  // 1. left-to-right accept tests
   if (tid < 64) {
-    bool rejected = false, bad = false, nf = false;
-    if (tid < K) {
-      const int x = dr[tid];
-      if (x < 0 || x >= V) {
-        bad = true;
-        rejected = true;
-      } else {
-        const float rho = qs.row(b * (K + 1) + tid)(x);
-        const float pi = p[(static_cast<size_t>(b) * K + tid) * V + x];
-        const float r = unif ? unif[b * (K + 1) + tid] : philox_uniform(seed, loop, 1, b, tid);
-        nf = not_finite(rho) | not_finite(pi);
-        rejected = !(static_cast<double>(r) * static_cast<double>(pi) < static_cast<double>(rho));
-      }
+    int a;
+    bool bad, nf;
+    accept_tests(qs, p, dr, unif, seed, loop, K, V, b, &a, &bad, &nf);
+    if (tid == 0) {
+      if (bad) atomicOr(err, kErrBadToken);
+      s_a = a;
+      s_y = 0;
+      s_nf = nf;
     }
-    if (tid <= K) nf |= qs.row(b * (K + 1) + tid).nonfinite();
-    const uint64_t rej = __ballot(rejected);
-    const bool any_nf = __ballot(nf) != 0;          // wave-wide, outside any branch
-    const int a = rej ? __ffsll(static_cast<long long>(rej)) - 1 : K;
-    if (tid == a && bad) atomicOr(err, kErrBadToken);
-    if (tid == 0) { s_a = a; s_y = 0; s_nf = any_nf; }
   }
   __syncthreads();
-  int a = s_a;
+  const int a = s_a;
   const bool nf_in = s_nf != 0;
   const int row = b * (K + 1) + a;
   const bool resid = a < K;
@@ -1375,16 +1416,202 @@ __global__ __launch_bounds__(kSampleThreads) void accept_kernel(QS qs, const flo
     y = qr.modified() ? accept_draw<true>(qr, prow, resid, V, u, wsum, &s_y)
                       : accept_draw<false>(qr, prow, resid, V, u, wsum, &s_y);
   }
-  if (y == -2) {
-    a = 0;
-    y = 0;
-    if (tid == 0) atomicOr(err, kErrNonFinite);
-  } else if (y < 0) {
-    y = 0;
-    if (tid == 0) atomicOr(err, kErrEmpty);
+  accept_finish(b, a, y, dr, K, out, n_acc, err);
+}
+
+// ---------------------------------------------------------------------------
+// The verify step's accept / resample over several CUs (the same outcome as
+// accept_kernel). accept_part_kernel's work-groups take one segment of the
+// final draw's row each: every one runs the accept tests (K gathers) to find
+// that row, then adds its segment's residual weights (q - p)_+ and q
+// weights (the zero-residual fallback and the bonus draw) and flags a
+// non-finite value among them; accept_draw_kernel finds the segment that
+// holds the draw's threshold from the totals and scans only it. Integer sums
+// do not depend on their order, so the token is accept_kernel's.
+// Row scratch: cs.n[s] residual and cs.w[s] q totals of segment s,
+// cs.n[kAccNf + s] its non-finite flag, cs.n[kAccHead ..] a, the tests'
+// non-finite flag and the bad-token flag.
+// ---------------------------------------------------------------------------
+constexpr int kAccNf = 64, kAccHead = 128;
+static_assert(kAccNf >= kMaxRowSegments && kAccHead >= kAccNf + kMaxRowSegments && kAccHead + 3 <= kCutBuckets,
+              "accept totals fit the row scratch");
+
+template <bool MOD, class Row>
+__device__ __forceinline__ void segment_accept_weights(const Row& qr, const float* __restrict__ prow, bool resid,
+                                                       int i0, int i1, uint64_t* wr, uint64_t* wq, bool* nf) {
+  for (int i = i0 + static_cast<int>(threadIdx.x); i < i1; i += kCutSegThreads) {
+    const float xq = qr.template get<MOD>(i);
+    *nf |= not_finite(xq);
+    const uint64_t x = fixed_weight(xq);
+    *wq += x;
+    if (resid) {
+      const float xp = prow[i];
+      *nf |= not_finite(xp);
+      const uint64_t y = fixed_weight(xp);
+      *wr += x > y ? x - y : 0;
+    }
   }
-  if (tid <= K) out[static_cast<size_t>(b) * (K + 1) + tid] = tid < a ? dr[tid] : (tid == a ? y : -1);
-  if (tid == 0) n_acc[b] = a;
+}
+
+// Grid (segments, B), kCutSegThreads threads.
+template <class QS>
+__global__ __launch_bounds__(kCutSegThreads) void accept_part_kernel(QS qs, const float* __restrict__ p,
+                                                                     const int32_t* __restrict__ drafts, int dstride,
+                                                                     int doff, const float* __restrict__ unif,
+                                                                     uint64_t seed, uint64_t loop, int K, int V,
+                                                                     char* __restrict__ cut, size_t cut_bytes,
+                                                                     int seg) {
+  __shared__ int s_a, s_nf;
+  __shared__ uint64_t s_r[kCutSegThreads / 64], s_q[kCutSegThreads / 64];
+  __shared__ int s_bad[kCutSegThreads / 64];
+  const int b = blockIdx.y, s = blockIdx.x, tid = threadIdx.x;
+  const int32_t* dr = drafts + static_cast<size_t>(b) * dstride + doff;
+  const CutRowScratch cs = cut_row(cut, cut_bytes, b);
+  if (tid < 64) {
+    int a;
+    bool bad, nf;
+    accept_tests(qs, p, dr, unif, seed, loop, K, V, b, &a, &bad, &nf);
+    if (tid == 0) {
+      s_a = a;
+      s_nf = nf;
+      if (s == 0) {
+        cs.n[kAccHead] = static_cast<uint64_t>(a);
+        cs.n[kAccHead + 1] = nf ? 1u : 0u;
+        cs.n[kAccHead + 2] = bad ? 1u : 0u;
+      }
+    }
+  }
+  __syncthreads();
+  const int a = s_a;
+  uint64_t wr = 0, wq = 0;
+  bool nf = false;
+  if (!s_nf) {                                     // uniform: the tests' inputs were finite
+    const bool resid = a < K;
+    const typename QS::Row qr = qs.row(b * (K + 1) + a);
+    const float* prow = p + (static_cast<size_t>(b) * K + (resid ? a : 0)) * V;
+    const int i0 = s * seg, i1 = min(V, i0 + seg);
+    if (qr.modified())
+      segment_accept_weights<true>(qr, prow, resid, i0, i1, &wr, &wq, &nf);
+    else
+      segment_accept_weights<false>(qr, prow, resid, i0, i1, &wr, &wq, &nf);
+  }
+  wr = wave_sum_u64(wr);
+  wq = wave_sum_u64(wq);
+  const bool wnf = __ballot(nf) != 0;
+  if ((tid & 63) == 0) {
+    s_r[tid >> 6] = wr;
+    s_q[tid >> 6] = wq;
+    s_bad[tid >> 6] = wnf ? 1 : 0;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint64_t tr = 0, tq = 0;
+    int f = 0;
+    for (int v = 0; v < kCutSegThreads / 64; ++v) {
+      tr += s_r[v];
+      tq += s_q[v];
+      f |= s_bad[v];
+    }
+    cs.n[s] = tr;
+    cs.w[s] = tq;
+    cs.n[kAccNf + s] = static_cast<uint64_t>(f);
+  }
+}
+
+// One work-group (kCutSegThreads threads) per sequence.
+template <class QS>
+__global__ __launch_bounds__(kCutSegThreads) void accept_draw_kernel(QS qs, const float* __restrict__ p,
+                                                                     const int32_t* __restrict__ drafts, int dstride,
+                                                                     int doff, const float* __restrict__ unif,
+                                                                     uint64_t seed, uint64_t loop, int K, int V,
+                                                                     const char* __restrict__ cut, size_t cut_bytes,
+                                                                     int nseg, int seg, int32_t* __restrict__ out,
+                                                                     int32_t* __restrict__ n_acc, int* err) {
+  static_assert(kMaxRowSegments <= 64, "one wave holds the segment totals");
+  __shared__ uint64_t wsum[17];
+  __shared__ uint64_t s_thr, s_off;
+  __shared__ int s_seg, s_y, s_mode;
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int32_t* dr = drafts + static_cast<size_t>(b) * dstride + doff;
+  const CutRowScratch cs = cut_row(const_cast<char*>(cut), cut_bytes, b);
+  const int a = static_cast<int>(cs.n[kAccHead]);
+  const bool nf_in = cs.n[kAccHead + 1] != 0;
+  if (tid == 0 && cs.n[kAccHead + 2] != 0) atomicOr(err, kErrBadToken);
+  const bool resid = a < K;
+  // Wave 0: the segments' flags and totals; the weights drawn from (the
+  // residual, or q for the bonus and when the residual sums to 0); the
+  // threshold and the segment holding it.
+  if (tid < 64) {
+    const bool in = tid < nseg;
+    const bool nf = __ballot(in && cs.n[kAccNf + tid] != 0) != 0;
+    const uint64_t tr = in ? cs.n[tid] : 0, tq = in ? cs.w[tid] : 0;
+    uint64_t ir = tr, iq = tq;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint64_t o1 = shfl_up_u64(ir, d), o2 = shfl_up_u64(iq, d);
+      if (tid >= d) {
+        ir += o1;
+        iq += o2;
+      }
+    }
+    const uint64_t Wr = shfl_u64(ir, 63), Wq = shfl_u64(iq, 63);
+    const bool use_r = resid && Wr != 0;
+    const uint64_t W = use_r ? Wr : Wq, inc = use_r ? ir : iq, tot = use_r ? tr : tq;
+    const float u = unif ? unif[b * (K + 1) + K] : philox_uniform(seed, loop, 2, b, 0);
+    const uint64_t thr = grid_threshold(u, W);
+    const uint64_t hit = W ? __ballot(in && inc > thr) : 0;
+    const int sstar = hit ? __ffsll(static_cast<long long>(hit)) - 1 : -1;
+    const uint64_t off = shfl_u64(inc - tot, sstar < 0 ? 0 : sstar);
+    if (tid == 0) {
+      s_thr = thr;
+      s_off = off;
+      s_seg = sstar;
+      s_mode = nf_in || nf ? -2 : use_r ? 1 : 0;   // -2: a non-finite value was read
+      s_y = -1;
+    }
+  }
+  __syncthreads();
+  const int mode = s_mode, sstar = s_seg;
+  if (mode != -2 && sstar >= 0) {                 // uniform
+    const typename QS::Row qr = qs.row(b * (K + 1) + a);
+    const float* prow = p + (static_cast<size_t>(b) * K + (resid ? a : 0)) * V;
+    const bool mod = qr.modified();
+    auto wt = [&](int i) -> uint64_t {
+      const uint64_t x = fixed_weight(mod ? qr.template get<true>(i) : qr.template get<false>(i));
+      if (mode == 0) return x;
+      const uint64_t y = fixed_weight(prow[i]);
+      return x > y ? x - y : 0;
+    };
+    const uint64_t thr = s_thr;
+    const int i0 = sstar * seg, i1 = min(V, i0 + seg);
+    uint64_t run = s_off;
+    for (int base = i0; base < i1; base += kCutSegThreads * kDrawPer) {
+      uint64_t w[kDrawPer], lt = 0;
+      const int c0 = base + kDrawPer * tid;
+#pragma unroll
+      for (int k = 0; k < kDrawPer; ++k) {
+        w[k] = c0 + k < i1 ? wt(c0 + k) : 0;
+        lt += w[k];
+      }
+      uint64_t total;
+      const uint64_t ex = run + block_exscan_u64(lt, wsum, &total);
+      if (ex <= thr && thr < ex + lt) {            // exactly one thread
+        uint64_t acc = ex;
+        int hitk = -1;
+#pragma unroll
+        for (int k = 0; k < kDrawPer; ++k) {
+          acc += w[k];
+          if (hitk < 0 && acc > thr) hitk = k;
+        }
+        s_y = c0 + hitk;
+      }
+      __syncthreads();
+      if (s_y >= 0) break;                         // uniform
+      run += total;
+    }
+  }
+  __syncthreads();
+  accept_finish(b, a, mode == -2 ? -2 : s_y, dr, K, out, n_acc, err);
 }
 
 // Draft step t: p_t = softmax(logits of the last row of each sequence / T),
@@ -1528,9 +1755,22 @@ hipError_t launch_accept_probs(const float* p, const float* q, const int32_t* dr
 
 hipError_t launch_accept_logits(const float* p, const float* logits, const void* stats, float temperature,
                                 const int32_t* tokens, const float* unif, uint64_t seed, uint64_t loop, int B,
-                                int K, int V, int32_t* out, int32_t* n_acc, int* err, hipStream_t st) {
+                                int K, int V, int32_t* out, int32_t* n_acc, char* cut, int* err, hipStream_t st) {
   const float inv_t = temperature == 0.f ? 0.f : 1.0f / temperature;
   const QLogits qs{logits, reinterpret_cast<const RowStat*>(stats), inv_t, V};
+  if (cut && V <= modifier_max_vocab()) {
+    int seg = 0, nseg = 0;
+    cut_segments(B, V, &seg, &nseg);
+    const size_t cut_bytes = cut_row_bytes(V);
+    hipLaunchKernelGGL(accept_part_kernel<QLogits>, dim3(nseg, B), dim3(kCutSegThreads), 0, st, qs, p, tokens, K + 1,
+                       1, unif, seed, loop, K, V, cut, cut_bytes, seg);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(accept_draw_kernel<QLogits>, dim3(B), dim3(kCutSegThreads), 0, st, qs, p, tokens, K + 1, 1,
+                       unif, seed, loop, K, V, static_cast<const char*>(cut), cut_bytes, nseg, seg, out, n_acc,
+                       err);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(accept_kernel<QLogits>, dim3(B), dim3(kSampleThreads), 0, st, qs, p, tokens, K + 1, 1, unif,
                      seed, loop, K, V, out, n_acc, err);
   return hipGetLastError();

@@ -485,8 +485,8 @@ sps_status verify_impl(sps_model_t target, sps_kv_t kv, const int32_t* tokens, i
                                   stats, q_out, base + ws.cut, err, st));
   if (acc)
     SPS_HIP(sps::launch_accept_logits(acc->p_draft, logits, stats, sampling.temperature, tokens, acc->uniforms,
-                                      acc->rng.seed, acc->rng.loop, B, K, V, acc->out_tokens, acc->n_accepted, err,
-                                      st));
+                                      acc->rng.seed, acc->rng.loop, B, K, V, acc->out_tokens, acc->n_accepted,
+                                      base + ws.cut, err, st));
   return SPS_OK;
 }
 
