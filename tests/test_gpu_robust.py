@@ -121,6 +121,45 @@ def test_draft_draw_at_large_batch(sps, B, top_p):
         np.testing.assert_array_equal(got_p[:, 0], omod.modify_rows(p_plain[:, 0], 0, top_p))
 
 
+@pytest.mark.parametrize("B,K", [(40, 3), (64, 1)])
+def test_verify_accept_at_large_batch(sps, B, K):
+    """The verify step's fused accept / resample over 32000-token rows at
+    B = 40 (K = 3) and B = 64 (K = 1), where the final draw's row is cut into
+    13 and 8 segments and the chosen segment is scanned in two rounds: the
+    tokens and counts equal the oracle's accept_resample on the GPU's own q
+    rows, the drafts' p rows and the same uniforms, and a rerun gives the
+    same outputs."""
+    shape = configs.DRAFT_70B.with_(n_layers=1)
+    V, T_cap = shape.vocab, 64
+    print("verify accept B", B, "K", K, flush=True)
+    gm = sps.Model(shape, synth.weights(shape, 45))
+    kv = sps.KVCache(shape, B, T_cap)
+    p, _, drafts = synth.accept_case(46, B, K, V, 2.0, 0.5)
+    first = synth.tokens(47, B, 1, V)
+    toks = cuda(np.concatenate([first, drafts], 1).astype(np.int32), torch.int32)
+    ws = sps.workspace(shape, B, K + 1, T_cap)
+    q = torch.empty((B, K + 1, V), dtype=torch.float32, device="cuda")
+
+    def run():
+        kv.buf.zero_()
+        kv.lengths.fill_(8)
+        out = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+        nacc = torch.empty(B, dtype=torch.int32, device="cuda")
+        sps.verify_step(gm, kv, toks, K, 1.0, ws, q=q, p_draft=cuda(p, torch.float32), rng=(48, 2),
+                        out_tokens=out, n_accepted=nacc)
+        torch.cuda.synchronize()
+        assert sps.device_error() == 0
+        return out.cpu().numpy(), nacc.cpu().numpy()
+
+    out, nacc = run()
+    w_out, w_n, _ = oacc.accept_resample(p, q.cpu().numpy(), drafts, oacc.philox_uniforms(48, 2, B, K))
+    np.testing.assert_array_equal(out, w_out)
+    np.testing.assert_array_equal(nacc, w_n)
+    out2, nacc2 = run()
+    np.testing.assert_array_equal(out2, out)
+    np.testing.assert_array_equal(nacc2, nacc)
+
+
 # ----------------------------------------------------------- non-finite --
 
 def test_softmax_nonfinite_rows(sps):
