@@ -1462,8 +1462,8 @@ __global__ __launch_bounds__(kCutSegThreads) void accept_part_kernel(QS qs, cons
                                                                      char* __restrict__ cut, size_t cut_bytes,
                                                                      int seg) {
   __shared__ int s_a, s_nf;
-  __shared__ uint64_t s_r[kCutSegThreads / 64], s_q[kCutSegThreads / 64];
-  __shared__ int s_bad[kCutSegThreads / 64];
+  __shared__ uint64_t s_r[kCutSegThreads / 64], s_q[kCutSegThreads / 64];   // per wave: residual, q totals
+  __shared__ int s_wnf[kCutSegThreads / 64];                                  // per wave: a non-finite value
   const int b = blockIdx.y, s = blockIdx.x, tid = threadIdx.x;
   const int32_t* dr = drafts + static_cast<size_t>(b) * dstride + doff;
   const CutRowScratch cs = cut_row(cut, cut_bytes, b);
@@ -1501,7 +1501,7 @@ __global__ __launch_bounds__(kCutSegThreads) void accept_part_kernel(QS qs, cons
   if ((tid & 63) == 0) {
     s_r[tid >> 6] = wr;
     s_q[tid >> 6] = wq;
-    s_bad[tid >> 6] = wnf ? 1 : 0;
+    s_wnf[tid >> 6] = wnf ? 1 : 0;
   }
   __syncthreads();
   if (tid == 0) {
@@ -1510,7 +1510,7 @@ __global__ __launch_bounds__(kCutSegThreads) void accept_part_kernel(QS qs, cons
     for (int v = 0; v < kCutSegThreads / 64; ++v) {
       tr += s_r[v];
       tq += s_q[v];
-      f |= s_bad[v];
+      f |= s_wnf[v];
     }
     cs.n[s] = tr;
     cs.w[s] = tq;
