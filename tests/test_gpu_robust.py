@@ -160,6 +160,59 @@ def test_verify_accept_at_large_batch(sps, B, K):
     np.testing.assert_array_equal(nacc2, nacc)
 
 
+def test_vocabulary_past_the_multi_cu_sampling(sps):
+    """A 50257-token vocabulary, past the 32768 entries the multi-CU sampling
+    paths take (rows this long go through the one-work-group kernels, whose
+    statistics keep a running max and sum): the verify step's q rows equal
+    the softmax of its logits, its fused accept / resample equals the
+    oracle's on those rows, and the draft step's tokens are the oracle's
+    integer inverse-CDF draws from its exported p rows."""
+    from oracle import philox as ophil
+    shape = configs.ModelShape("v50257", 128, 1, 2, 64, 256, 50257, "gelu", "bf16")
+    V, T_cap, B = shape.vocab, 64, 2
+    print("vocabulary", V, flush=True)
+    gm = sps.Model(shape, synth.weights(shape, 49))
+    kv = sps.KVCache(shape, B, T_cap)
+    kv.buf.zero_()
+    kv.lengths.fill_(8)
+    # verify step, K = 4
+    K = 4
+    p, _, drafts = synth.accept_case(50, B, K, V, 2.0, 0.5)
+    toks = cuda(np.concatenate([synth.tokens(51, B, 1, V), drafts], 1).astype(np.int32), torch.int32)
+    ws = sps.workspace(shape, B, K + 1, T_cap)
+    logits = torch.empty((B, K + 1, V), dtype=torch.float32, device="cuda")
+    q = torch.empty_like(logits)
+    out = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+    nacc = torch.empty(B, dtype=torch.int32, device="cuda")
+    sps.verify_step(gm, kv, toks, K, 1.0, ws, logits=logits, q=q, p_draft=cuda(p, torch.float32), rng=(52, 1),
+                    out_tokens=out, n_accepted=nacc)
+    torch.cuda.synchronize()
+    assert sps.device_error() == 0
+    qg = q.cpu().numpy()
+    np.testing.assert_allclose(qg, osamp.softmax(logits.cpu().numpy().astype(np.float64), 1.0), rtol=2e-5, atol=1e-9)
+    w_out, w_n, _ = oacc.accept_resample(p, qg, drafts, oacc.philox_uniforms(52, 1, B, K))
+    np.testing.assert_array_equal(out.cpu().numpy(), w_out)
+    np.testing.assert_array_equal(nacc.cpu().numpy(), w_n)
+    # draft step, K = 3
+    Kd = 3
+    kv.lengths.fill_(8)
+    ctx = cuda(synth.tokens(53, B, 2, V), torch.int32)
+    wsd = sps.workspace(shape, B, 2, T_cap)
+    tokens = torch.empty((B, Kd + 1), dtype=torch.int32, device="cuda")
+    pd = torch.empty((B, Kd, V), dtype=torch.float32, device="cuda")
+    sps.draft_step(gm, kv, ctx, Kd, 1.0, (54, 2), tokens, pd, wsd)
+    torch.cuda.synchronize()
+    assert sps.device_error() == 0
+    got_t, got_p = tokens.cpu().numpy(), pd.cpu().numpy()
+    ud = ophil.uniforms(54, 2, ophil.PURPOSE_DRAFT, B, Kd)
+    for b in range(B):
+        for t in range(Kd):
+            row = got_p[b, t]
+            assert abs(float(row.astype(np.float64).sum()) - 1.0) < 1e-4
+            y, ok = osamp.categorical(osamp.to_weights(row), ud[b, t])
+            assert ok and got_t[b, t + 1] == y, (b, t)
+
+
 # ----------------------------------------------------------- non-finite --
 
 def test_softmax_nonfinite_rows(sps):
